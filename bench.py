@@ -1,0 +1,233 @@
+"""KV page-swap throughput on one MI355X.
+
+A step is one context switch of the hot path: a batched swap-out (gather)
+of the preempted prompts' KV blocks into the offload image, then a batched
+swap-in (scatter) of that image into fresh pool blocks -- validation, run
+planning, cross-stream ordering, both kernels and completion.  Steps
+alternate between two disjoint block sets, so every step moves the whole
+payload both ways.  The pool and the offload buffer are resident (HBM, or
+pinned host for the host-target workloads) before the timed region starts.
+
+Prints one JSON line.  The default workload is the Llama-3-8B-shaped pool
+(32 layers, 8 KV heads, head_dim 128, block 16, bf16, 16384 blocks) with 8
+of 16 fragmented 2048-token prompts preempted to an HBM offload region.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, read + write combined
+HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
+
+# HBM bytes per launch of the dominant kernel from rocprofv3 --pmc
+# (FETCH_SIZE, WRITE_SIZE), each scaled by the same counters' reading for a
+# plain copy of known size.  Keyed by the hash of the kernel source they
+# were taken on: a changed kernel reports null until measured again.
+MEASURED_TRAFFIC = {}
+
+
+def _kernel_hash() -> str:
+    p = os.path.join(ROOT, "paper_2407_21255_amd", "csrc", "swap_kernels.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+WORKLOADS = {
+    "llama8b_hbm": "Llama-3-8B-shaped KV (32 layers, 8 KV heads, head_dim 128, block 16, "
+                   "bf16, 16384-block pool): 8 of 16 fragmented 2048-token prompts "
+                   "swapped out to an HBM offload region and back into fresh blocks",
+    "llama8b_host": "Llama-3-8B-shaped KV, bf16: 8 x 4096-token prompts swapped out to "
+                    "pinned host memory (zero copy) and back",
+    "llama70b_hbm": "Llama-3-70B-shaped KV (80 layers, bf16, 4096-block pool): one "
+                    "32768-token prompt swapped out to an HBM offload region and back",
+    "llama70b_host": "Llama-3-70B-shaped KV, bf16: one 32768-token prompt swapped out to "
+                     "pinned host memory and back",
+    "tiny": "4 layers, 8 KV heads, head_dim 128, block 16, fp16, 256-block pool: one "
+            "512-token prompt out to an HBM buffer and back",
+}
+
+
+def _case(name):
+    from paper_2407_21255_amd import workload as wl
+    return {
+        "llama8b_hbm": lambda: (wl.llama8b_hbm_case(), False),
+        "llama8b_host": lambda: (wl.llama8b_host_case(), True),
+        "llama70b_hbm": lambda: (wl.llama70b_case(), False),
+        "llama70b_host": lambda: (wl.llama70b_case(), True),
+        "tiny": lambda: (wl.tiny_case(), False),
+    }[name]()
+
+
+def cpu_baseline(shape, target_seconds: float):
+    """The CPU oracle on a bounded sample of the same workload: the same
+    chunk shape on a 512-block pool, one 128-block (2048-token) prompt out
+    to a host image and back into other blocks, repeated for
+    ``target_seconds``; single thread."""
+    import numpy as np
+
+    import oracle
+    from paper_2407_21255_amd import workload as wl
+
+    L, H, T, D, dt = (shape.num_layers, shape.num_kv_heads, shape.block_tokens,
+                      shape.head_dim, shape.dtype)
+    small = wl.KVShape(L, 512, H, T, D, dt)
+    d = oracle.desc(*small.as_tuple())
+    rng = np.random.default_rng(2)
+    pool = rng.integers(0, 256, size=small.pool_bytes, dtype=np.uint8)
+    perm = wl.permutation(512, 2)
+    a, b = perm[:128], perm[128:256]
+    img = np.zeros(small.image_bytes(128), dtype=np.uint8)
+    assert oracle.swap_out(d, pool, [a], img) == 0  # touch every page once
+    assert oracle.swap_in(d, pool, [b], img) == 0
+    reps, moved = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        src, dst = (a, b) if reps % 2 == 0 else (b, a)
+        assert oracle.swap_out(d, pool, [src], img) == 0
+        assert oracle.swap_in(d, pool, [dst], img) == 0
+        reps += 1
+        moved += 2 * img.nbytes
+        el = time.perf_counter() - t0
+        if el >= target_seconds:
+            break
+    return {
+        "value": round(moved / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        "sample": f"{L}-layer chunks of {small.chunk_bytes} B on a 512-block pool: one "
+                  f"128-block prompt ({img.nbytes >> 20} MiB per direction) out and back in, "
+                  f"{reps} round trips in {el:.1f} s, single thread",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_hbm", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the swap path runs on a single MI355X "
+              "(no sharding, no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import aqua
+    from paper_2407_21255_amd import workload as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    aqua.load()
+    case, pinned = _case(args.workload)
+    s = case.shape
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, case.seed, case.owner)
+    payload = case.payload_bytes
+    if pinned:
+        img = torch.empty(payload, dtype=torch.uint8, pin_memory=True)
+    else:
+        img = torch.empty(payload, dtype=torch.uint8, device="cuda")
+    img.zero_()
+    torch.cuda.synchronize()
+
+    tab_a = aqua._csr(case.out_tables)
+    tab_b = aqua._csr(case.in_tables)
+    stream = torch.cuda.Stream()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    evs = []
+
+    def step(i, timed):
+        src, dst = (tab_a, tab_b) if i % 2 == 0 else (tab_b, tab_a)
+        if timed:
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(stream)
+        kv.swap_out(src, img, stream=stream)
+        if timed:
+            e1.record(stream)
+        kv.swap_in(dst, img, stream=stream)
+        if timed:
+            e2.record(stream)
+            evs.append((e0, e1, e2))
+
+    for i in range(args.warmup):
+        step(i, False)
+    kv.sync(0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, True)
+    kv.sync(0)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = kv.stats()
+    kv.close()
+
+    out_ms = np.array([a.elapsed_time(b) for a, b, _ in evs])
+    in_ms = np.array([b.elapsed_time(c) for _, b, c in evs])
+    ms_per_step = wall * 1e3 / args.steps
+    value = 2 * payload * args.steps / wall / 1e9
+    dom, dom_ms = ("gather (swap-out)", out_ms) if out_ms.mean() >= in_ms.mean() else \
+        ("scatter (swap-in)", in_ms)
+    if pinned:
+        bound, peak, alg = "host_link", HOST_LINK_PEAK_GBS, payload
+    else:
+        bound, peak, alg = "hbm", HBM_PEAK_GBS, 2 * payload
+    achieved = alg / (dom_ms.mean() * 1e-3) / 1e9
+    khash = _kernel_hash()
+    traffic = MEASURED_TRAFFIC.get((args.workload, khash))
+    res = {
+        "metric": "KV page swap GB/s (out+in) and % of HBM / host-link peak, 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.DTYPE_NAME[s.dtype],
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOADS[args.workload],
+            "layers": s.num_layers, "kv_heads": s.num_kv_heads, "head_dim": s.head_dim,
+            "block_tokens": s.block_tokens, "pool_blocks": s.num_blocks,
+            "chunk_bytes": s.chunk_bytes, "swapped_blocks": case.nblocks,
+            "payload_bytes_per_direction": payload,
+            "offload_target": "pinned_host" if pinned else "hbm",
+            "parallelism": "single_gpu",
+        },
+        "roofline": {
+            "bound": bound, "kernel": dom,
+            "achieved": round(achieved, 1), "peak": peak,
+            "unit": "GB/s", "frac": round(achieved / peak, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg,
+        },
+        "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
+                      "swap_out_min": round(float(out_ms.min()), 4),
+                      "swap_in_mean": round(float(in_ms.mean()), 4),
+                      "swap_in_min": round(float(in_ms.min()), 4)},
+        "swap_out_GBps": round(payload / (out_ms.mean() * 1e-3) / 1e9, 2),
+        "swap_in_GBps": round(payload / (in_ms.mean() * 1e-3) / 1e9, 2),
+        "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
+                                  2),
+        "kernel_source": khash,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

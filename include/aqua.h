@@ -1,0 +1,187 @@
+/*
+ * aqua.h -- C ABI of the MI355X KV page-swap library.
+ *
+ * Aqua (Vuppalapati et al., "Network-Accelerated Memory Offloading for LLMs
+ * in Scale-Up GPU Domains", ASPLOS '25) pages a preempted prompt's inference
+ * state out of GPU memory and back in at every context switch of its
+ * time-sliced scheduler (section 7, "Fair scheduling prompts").  Because the
+ * serving engine keeps one KV tensor per layer for all prompts, one prompt's
+ * state is many small discontiguous pieces; the paper gathers them into one
+ * contiguous tensor before moving it to the offload location and scatters
+ * them back on the way in (section 7, "Efficient context switching").  The
+ * offload location is a peer GPU's memory or, without a peer, host DRAM
+ * (section 6, "Allocating Aqua Tensors").  Moving state must not corrupt
+ * data while other work runs (section 8).
+ *
+ * This library implements those two operations for a paged KV pool with
+ * hand-written gfx950 kernels that write the gathered image directly to its
+ * destination:
+ *
+ *   pool   [num_layers][num_blocks][2 (K,V)][num_kv_heads][block_tokens][head_dim]
+ *          elements of 1 (fp8 e4m3) or 2 (fp16, bf16) bytes.  One (layer,
+ *          block) "chunk" of C = 2*H*T*D*elem bytes is contiguous.
+ *   image  of one sequence with block table bt[0..n): layer-major
+ *          [num_layers][n][C]; image chunk (l, i) is pool chunk (l, bt[i]).
+ *          Images of a multi-sequence call are packed one after another
+ *          (sequence s at sum_{q<s} L*n_q*C) unless img_offsets places them.
+ *
+ * Element values are opaque bytes: no conversion, no NaN canonicalisation.
+ * Whole blocks are copied, including unused token slots of a last block.
+ *
+ * Ordering: calls on one pool behave as if executed in issue order, across
+ * any streams, for the pool blocks and offload byte ranges they name; the
+ * library makes a call's stream wait on an earlier call's event only where
+ * the two touch the same block or overlapping offload bytes (read/write,
+ * write/read or write/write).  Memory touched outside the library (attention
+ * kernels reading the pool, the caller refilling a buffer) is ordered by the
+ * caller with streams, events, aqua_sync or aqua_stream_wait.
+ *
+ * Ownership: the pool memory, offload buffers and streams belong to the
+ * caller; the library borrows them.  A buffer must outlive the ticket of
+ * every call that names it, the pool must outlive aqua_kv_pool_destroy.
+ * block_ids, seq_offsets and img_offsets are host arrays read before the
+ * call returns.
+ *
+ * Errors: argument errors are found before anything is enqueued, so a
+ * failing call has no side effect and issues no ticket.  A HIP runtime
+ * failure after enqueueing is latched on the pool: aqua_sync returns
+ * AQUA_ERR_HIP and every later swap call returns AQUA_ERR_STATE.
+ *
+ * Threads: a pool handle is used from one thread at a time.  Separate pools
+ * are independent (but do not order against each other).
+ */
+#ifndef AQUA_H
+#define AQUA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define AQUA_API __attribute__((visibility("default")))
+#else
+#define AQUA_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct aqua_kv_pool* aqua_kv_pool_t; /* opaque */
+typedef int32_t aqua_status;
+
+enum {
+    AQUA_OK = 0,
+    AQUA_ERR_INVALID = -1,   /* null pointer, bad shape, misalignment,
+                                target/pointer-class mismatch, bad stream */
+    AQUA_ERR_RANGE = -2,     /* a block id < 0 or >= num_blocks */
+    AQUA_ERR_DUPLICATE = -3, /* swap-in names one pool block twice, or a
+                                swap-out's image ranges overlap */
+    AQUA_ERR_CAPACITY = -4,  /* an image does not fit the buffer, or the
+                                pool memory is smaller than the shape */
+    AQUA_ERR_HIP = -5,       /* HIP runtime failure (launch, event, copy) */
+    AQUA_ERR_STATE = -6      /* pool unusable after a latched HIP failure */
+};
+
+/* Element types.  Only the byte width matters to the copy. */
+enum { AQUA_F16 = 1, AQUA_BF16 = 2, AQUA_FP8_E4M3 = 3 };
+
+/* Offload targets.  DEVICE: device memory on the pool's GPU (a carved-out
+ * HBM region standing in for a scale-up peer's memory).  HOST: page-locked
+ * host memory from hipHostMalloc (torch pin_memory), written and read by
+ * the kernels directly over the host link (zero copy). */
+enum { AQUA_TARGET_DEVICE = 0, AQUA_TARGET_HOST = 1 };
+
+typedef struct {
+    uint32_t num_layers;   /* L */
+    uint32_t num_blocks;   /* N, pool blocks per layer */
+    uint32_t num_kv_heads; /* H */
+    uint32_t block_tokens; /* T, tokens per block */
+    uint32_t head_dim;     /* D */
+    int32_t dtype;         /* AQUA_F16 / AQUA_BF16 / AQUA_FP8_E4M3 */
+} aqua_kv_desc;
+
+typedef struct {
+    uint64_t calls_out, calls_in;         /* successful swap calls */
+    uint64_t bytes_out, bytes_in;         /* image bytes moved (payload) */
+    uint64_t bytes_host;                  /* of which to/from host memory */
+    uint64_t descriptors;                 /* run descriptors launched */
+    uint64_t waits_inserted;              /* cross-stream waits enqueued */
+    uint64_t waits_elided;                /* conflicts already complete */
+    uint64_t host_ns;                     /* host time in swap calls */
+    int32_t hip_error;                    /* latched hipError_t, 0 if none */
+    int32_t reserved;
+} aqua_pool_stats;
+
+/* Bind a pool to caller-owned device memory.
+ *   desc       shape; C = 2*H*T*D*elem must be a multiple of 16 bytes.
+ *   pool_base  device pointer on the current device, 16-byte aligned, with
+ *              [pool_base, pool_base + pool_bytes) inside one allocation.
+ *   pool_bytes >= L*N*C, else AQUA_ERR_CAPACITY.
+ *   out        receives the handle; untouched on failure.
+ * Allocates the library's own descriptor rings and events. */
+AQUA_API aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
+                                uint64_t pool_bytes, aqua_kv_pool_t* out);
+
+/* Wait for every outstanding call, then free the library's state (not the
+ * pool memory).  Returns a latched HIP error if there was one. */
+AQUA_API aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t pool);
+
+/* Swap-out (gather): for each sequence s, layer l and table position i,
+ * copy pool chunk (l, bt_s[i]) to image chunk (l, i) of s.
+ *   block_ids    concatenated block tables (int32), seq_offsets[num_seqs]
+ *                entries; the same block may appear more than once.
+ *   seq_offsets  CSR offsets, num_seqs+1 entries, seq_offsets[0] == 0,
+ *                non-decreasing.
+ *   dst          device pointer (target DEVICE) or pinned host pointer
+ *                (target HOST), 16-byte aligned; dst_bytes its usable size.
+ *   img_offsets  NULL for packed images, else num_seqs byte offsets (each a
+ *                multiple of 16) into dst; non-empty images must not overlap.
+ *   stream       hipStream_t of the caller (NULL: the null stream).
+ *   ticket       receives the call's ticket (may be NULL).
+ * Pool bytes are only read. */
+AQUA_API aqua_status aqua_swap_out(aqua_kv_pool_t pool, uint32_t num_seqs,
+                          const int32_t* block_ids,
+                          const uint64_t* seq_offsets, void* dst,
+                          uint64_t dst_bytes, const uint64_t* img_offsets,
+                          int32_t target, void* stream, uint64_t* ticket);
+
+/* Swap-in (scatter): for each sequence s, layer l and table position i,
+ * copy image chunk (l, i) of s into pool chunk (l, bt_s[i]).  Destination
+ * blocks must be distinct within the call (AQUA_ERR_DUPLICATE).  Arguments
+ * as for aqua_swap_out with src read only. */
+AQUA_API aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs,
+                         const int32_t* block_ids,
+                         const uint64_t* seq_offsets, const void* src,
+                         uint64_t src_bytes, const uint64_t* img_offsets,
+                         int32_t target, void* stream, uint64_t* ticket);
+
+/* Block the host until `ticket` (0: every outstanding call) has completed.
+ * Returns AQUA_ERR_HIP if a HIP failure was latched. */
+AQUA_API aqua_status aqua_sync(aqua_kv_pool_t pool, uint64_t ticket);
+
+/* Make `stream` wait (on the device, without blocking the host) until
+ * `ticket` has completed.  Tickets already complete need no wait. */
+AQUA_API aqua_status aqua_stream_wait(aqua_kv_pool_t pool, uint64_t ticket,
+                             void* stream);
+
+/* 1 if `ticket` has completed, 0 if not, negative status on error. */
+AQUA_API aqua_status aqua_query(aqua_kv_pool_t pool, uint64_t ticket);
+
+/* Cap the number of workgroups of later launches for one target (0: the
+ * library's default).  Used to leave compute units to concurrent work while
+ * a host-link-bound swap runs. */
+AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
+                                            int32_t target,
+                                            uint32_t max_workgroups);
+
+/* Copy the pool's counters into *out. */
+AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* out);
+
+/* Static text for a status code. */
+AQUA_API const char* aqua_status_str(aqua_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AQUA_H */

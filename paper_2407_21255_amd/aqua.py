@@ -1,0 +1,263 @@
+"""Python binding of the C ABI in ``include/aqua.h`` (ctypes).
+
+Argument marshalling only: every byte of a swap is moved by the library's
+HIP kernels.  The low-level functions carry the C names and return the
+C status (plus the ticket where the C call writes one); ``KVPool`` wraps
+them for torch tensors and raises ``AquaError`` on a failed call.
+
+torch is imported before the library is loaded so that the library binds
+to the HIP runtime torch already holds (both carry the same soname), and
+pointers and streams from torch are valid in it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libaqua.so")
+
+AQUA_OK = 0
+AQUA_ERR_INVALID = -1
+AQUA_ERR_RANGE = -2
+AQUA_ERR_DUPLICATE = -3
+AQUA_ERR_CAPACITY = -4
+AQUA_ERR_HIP = -5
+AQUA_ERR_STATE = -6
+
+AQUA_F16, AQUA_BF16, AQUA_FP8_E4M3 = 1, 2, 3
+AQUA_TARGET_DEVICE, AQUA_TARGET_HOST = 0, 1
+
+EXPORTS = (
+    "aqua_kv_pool_create", "aqua_kv_pool_destroy", "aqua_swap_out",
+    "aqua_swap_in", "aqua_sync", "aqua_stream_wait", "aqua_query",
+    "aqua_kv_pool_set_max_workgroups", "aqua_pool_stats_get", "aqua_status_str",
+)
+
+
+class aqua_kv_desc(ctypes.Structure):
+    _fields_ = [
+        ("num_layers", ctypes.c_uint32),
+        ("num_blocks", ctypes.c_uint32),
+        ("num_kv_heads", ctypes.c_uint32),
+        ("block_tokens", ctypes.c_uint32),
+        ("head_dim", ctypes.c_uint32),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class aqua_pool_stats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in (
+        "calls_out", "calls_in", "bytes_out", "bytes_in", "bytes_host",
+        "descriptors", "waits_inserted", "waits_elided", "host_ns")] + [
+        ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class AquaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {aqua_status_str(status)} ({status})")
+        self.status = status
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads the library; fails loudly when it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(
+            f"{path} is missing: build it with "
+            "`python -m paper_2407_21255_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(path)
+    P, u32, u64, i32 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32
+    L.aqua_kv_pool_create.argtypes = [ctypes.POINTER(aqua_kv_desc), P, u64,
+                                      ctypes.POINTER(P)]
+    L.aqua_kv_pool_destroy.argtypes = [P]
+    L.aqua_swap_out.argtypes = [P, u32, P, P, P, u64, P, i32, P, ctypes.POINTER(u64)]
+    L.aqua_swap_in.argtypes = [P, u32, P, P, P, u64, P, i32, P, ctypes.POINTER(u64)]
+    L.aqua_sync.argtypes = [P, u64]
+    L.aqua_stream_wait.argtypes = [P, u64, P]
+    L.aqua_query.argtypes = [P, u64]
+    L.aqua_kv_pool_set_max_workgroups.argtypes = [P, i32, u32]
+    L.aqua_pool_stats_get.argtypes = [P, ctypes.POINTER(aqua_pool_stats)]
+    L.aqua_status_str.argtypes = [i32]
+    L.aqua_status_str.restype = ctypes.c_char_p
+    for n in EXPORTS:
+        if n != "aqua_status_str":
+            getattr(L, n).restype = i32
+    _lib = L
+    return L
+
+
+# -- the C entry points, one to one ------------------------------------------
+
+def aqua_kv_pool_create(desc: aqua_kv_desc, pool_base: int, pool_bytes: int):
+    h = ctypes.c_void_p()
+    st = load().aqua_kv_pool_create(ctypes.byref(desc), pool_base, pool_bytes,
+                                    ctypes.byref(h))
+    return st, h
+
+
+def aqua_kv_pool_destroy(pool) -> int:
+    return load().aqua_kv_pool_destroy(pool)
+
+
+def aqua_swap_out(pool, num_seqs, block_ids, seq_offsets, dst, dst_bytes,
+                  img_offsets, target, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_out(pool, num_seqs, block_ids, seq_offsets, dst, dst_bytes,
+                              img_offsets, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_in(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
+                 img_offsets, target, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_in(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
+                             img_offsets, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_sync(pool, ticket: int = 0) -> int:
+    return load().aqua_sync(pool, ticket)
+
+
+def aqua_stream_wait(pool, ticket: int, stream) -> int:
+    return load().aqua_stream_wait(pool, ticket, stream)
+
+
+def aqua_query(pool, ticket: int) -> int:
+    return load().aqua_query(pool, ticket)
+
+
+def aqua_kv_pool_set_max_workgroups(pool, target: int, n: int) -> int:
+    return load().aqua_kv_pool_set_max_workgroups(pool, target, n)
+
+
+def aqua_pool_stats_get(pool):
+    s = aqua_pool_stats()
+    st = load().aqua_pool_stats_get(pool, ctypes.byref(s))
+    return st, s
+
+
+def aqua_status_str(status: int) -> str:
+    try:
+        return load().aqua_status_str(status).decode()
+    except FileNotFoundError:
+        return f"status {status}"
+
+
+# -- torch-facing wrapper ------------------------------------------------------
+
+def _csr(tables):
+    """(int32 ids, uint64 offsets) from a list of tables or an (ids, offs) pair."""
+    if isinstance(tables, tuple) and len(tables) == 2 and isinstance(tables[0], np.ndarray):
+        ids, offs = tables
+    else:
+        ids = np.asarray([b for t in tables for b in t], dtype=np.int32)
+        offs = np.zeros(len(tables) + 1, dtype=np.uint64)
+        if len(tables):
+            offs[1:] = np.cumsum([len(t) for t in tables])
+    return (np.ascontiguousarray(ids, dtype=np.int32),
+            np.ascontiguousarray(offs, dtype=np.uint64))
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, int):
+        return stream or None
+    return stream.cuda_stream or None
+
+
+def _target_of(t: torch.Tensor) -> int:
+    if t.is_cuda:
+        return AQUA_TARGET_DEVICE
+    if t.is_pinned():
+        return AQUA_TARGET_HOST
+    raise AquaError(AQUA_ERR_INVALID, "offload buffer must be a device or pinned host tensor")
+
+
+class KVPool:
+    """A paged KV pool bound to a caller-owned uint8 device tensor."""
+
+    def __init__(self, shape: Sequence[int], pool: torch.Tensor):
+        L, N, H, T, D, dtype = shape
+        self.desc = aqua_kv_desc(L, N, H, T, D, dtype)
+        self.pool = pool
+        st, h = aqua_kv_pool_create(self.desc, pool.data_ptr(),
+                                    pool.numel() * pool.element_size())
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_kv_pool_create")
+        self.handle = h
+
+    def _swap(self, fn, name, tables, buf, img_offsets, stream, target):
+        ids, offs = _csr(tables)
+        io = None
+        if img_offsets is not None:
+            io = np.ascontiguousarray(img_offsets, dtype=np.uint64)
+        tgt = _target_of(buf) if target is None else target
+        st, ticket = fn(self.handle, len(offs) - 1, ids.ctypes.data, offs.ctypes.data,
+                        buf.data_ptr(), buf.numel() * buf.element_size(),
+                        None if io is None else io.ctypes.data, tgt,
+                        _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, name)
+        return ticket
+
+    def swap_out(self, tables, dst: torch.Tensor, img_offsets=None, stream=None,
+                 target=None) -> int:
+        return self._swap(aqua_swap_out, "aqua_swap_out", tables, dst, img_offsets,
+                          stream, target)
+
+    def swap_in(self, tables, src: torch.Tensor, img_offsets=None, stream=None,
+                target=None) -> int:
+        return self._swap(aqua_swap_in, "aqua_swap_in", tables, src, img_offsets,
+                          stream, target)
+
+    def sync(self, ticket: int = 0) -> None:
+        st = aqua_sync(self.handle, ticket)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_sync")
+
+    def stream_wait(self, ticket: int, stream=None) -> None:
+        st = aqua_stream_wait(self.handle, ticket, _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_stream_wait")
+
+    def query(self, ticket: int) -> bool:
+        st = aqua_query(self.handle, ticket)
+        if st < 0:
+            raise AquaError(st, "aqua_query")
+        return st == 1
+
+    def set_max_workgroups(self, target: int, n: int) -> None:
+        st = aqua_kv_pool_set_max_workgroups(self.handle, target, n)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_kv_pool_set_max_workgroups")
+
+    def stats(self) -> dict:
+        st, s = aqua_pool_stats_get(self.handle)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_pool_stats_get")
+        return {n: getattr(s, n) for n, _ in s._fields_ if n != "reserved"}
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            st = aqua_kv_pool_destroy(self.handle)
+            self.handle = None
+            if st != AQUA_OK:
+                raise AquaError(st, "aqua_kv_pool_destroy")
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -1,0 +1,533 @@
+// aqua_capi.hip -- the C ABI: pools, tickets, descriptor staging, cross-stream
+// ordering and the launches of the gather/scatter kernels.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <vector>
+
+#include "aqua.h"
+#include "aqua_core.h"
+#include "swap_kernels.h"
+
+namespace {
+
+using aqua::HazardTracker;
+using aqua::RunDesc;
+
+constexpr uint64_t kDefaultRingBytes = 1ull << 20;  // 32768 descriptors
+constexpr uint64_t kDefaultUnitBytes = 64ull << 10;
+
+uint64_t env_u64(const char* name, uint64_t dflt) {
+    const char* v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    char* end = nullptr;
+    const unsigned long long x = std::strtoull(v, &end, 0);
+    return (end && *end == 0) ? (uint64_t)x : dflt;
+}
+
+struct Outstanding {
+    uint64_t ticket;
+    hipEvent_t ev;
+};
+
+struct RingUse {
+    uint64_t lo, hi, ticket;
+};
+
+}  // namespace
+
+struct aqua_kv_pool {
+    aqua::Shape shape;
+    int device = 0;
+    uint8_t* base = nullptr;
+    uint64_t bytes = 0;
+
+    aqua::DupMarks marks;
+    HazardTracker tracker;
+    std::vector<RunDesc> plan;
+    std::vector<std::pair<uint64_t, uint64_t>> ranges;
+    std::vector<HazardTracker::Dep> deps;
+
+    std::vector<hipStream_t> lane_stream;               // lane -> stream
+    std::vector<std::deque<Outstanding>> outstanding;   // per lane, in order
+    std::vector<hipEvent_t> spare_events;
+
+    // Descriptor staging: pinned host ring copied to a device ring.
+    uint8_t* ring_host = nullptr;
+    uint8_t* ring_dev = nullptr;
+    uint64_t ring_bytes = 0;
+    uint64_t ring_head = 0;
+    std::deque<RingUse> ring_uses;
+
+    uint64_t next_ticket = 1;
+    uint64_t unit_bytes = kDefaultUnitBytes;
+    uint32_t max_wg[2] = {0, 0};
+    aqua_pool_stats stats{};
+    hipError_t sticky = hipSuccess;
+};
+
+namespace {
+
+// Switches to the pool's device for the duration of a call.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) {
+            ok = false;
+            return;
+        }
+        if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+        if (prev == dev) prev = -1;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+aqua_status latch(aqua_kv_pool* p, hipError_t e) {
+    if (e != hipSuccess && p->sticky == hipSuccess) {
+        p->sticky = e;
+        p->stats.hip_error = (int32_t)e;
+    }
+    return AQUA_ERR_HIP;
+}
+
+uint32_t lane_for(aqua_kv_pool* p, hipStream_t s) {
+    for (uint32_t m = 0; m < p->lane_stream.size(); ++m)
+        if (p->lane_stream[m] == s) return m;
+    p->lane_stream.push_back(s);
+    p->outstanding.emplace_back();
+    return (uint32_t)(p->lane_stream.size() - 1);
+}
+
+hipError_t take_event(aqua_kv_pool* p, hipEvent_t* ev) {
+    if (!p->spare_events.empty()) {
+        *ev = p->spare_events.back();
+        p->spare_events.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreateWithFlags(ev, hipEventDisableTiming);
+}
+
+// Everything on lane m up to `ticket` is known complete: recycle events.
+void retire(aqua_kv_pool* p, uint32_t m, uint64_t ticket) {
+    auto& q = p->outstanding[m];
+    while (!q.empty() && q.front().ticket <= ticket) {
+        p->spare_events.push_back(q.front().ev);
+        q.pop_front();
+    }
+    p->tracker.complete(m, ticket);
+}
+
+// Non-blocking: retire whatever has finished.
+aqua_status poll(aqua_kv_pool* p) {
+    for (uint32_t m = 0; m < p->outstanding.size(); ++m) {
+        auto& q = p->outstanding[m];
+        while (!q.empty()) {
+            const hipError_t e = hipEventQuery(q.front().ev);
+            if (e == hipErrorNotReady) break;
+            if (e != hipSuccess) return latch(p, e);
+            retire(p, m, q.front().ticket);
+        }
+    }
+    return AQUA_OK;
+}
+
+hipEvent_t event_of(aqua_kv_pool* p, uint64_t ticket) {
+    const uint32_t m = p->tracker.lane_of(ticket);
+    for (const Outstanding& o : p->outstanding[m])
+        if (o.ticket == ticket) return o.ev;
+    return nullptr;
+}
+
+// Blocks until `ticket` has completed.
+aqua_status wait_ticket(aqua_kv_pool* p, uint64_t ticket) {
+    const uint32_t m = p->tracker.lane_of(ticket);
+    if (ticket <= p->tracker.completed(m)) return AQUA_OK;
+    hipEvent_t ev = event_of(p, ticket);
+    if (!ev) return AQUA_OK;  // retired already
+    const hipError_t e = hipEventSynchronize(ev);
+    if (e != hipSuccess) return latch(p, e);
+    retire(p, m, ticket);
+    return AQUA_OK;
+}
+
+aqua_status wait_all(aqua_kv_pool* p) {
+    for (uint32_t m = 0; m < p->outstanding.size(); ++m) {
+        auto& q = p->outstanding[m];
+        if (q.empty()) continue;
+        const uint64_t last = q.back().ticket;
+        const hipError_t e = hipEventSynchronize(q.back().ev);
+        if (e != hipSuccess) return latch(p, e);
+        retire(p, m, last);
+    }
+    p->ring_uses.clear();
+    return AQUA_OK;
+}
+
+void free_rings(aqua_kv_pool* p) {
+    if (p->ring_dev) (void)hipFree(p->ring_dev);
+    if (p->ring_host) (void)hipHostFree(p->ring_host);
+    p->ring_dev = nullptr;
+    p->ring_host = nullptr;
+    p->ring_bytes = 0;
+    p->ring_head = 0;
+}
+
+aqua_status alloc_rings(aqua_kv_pool* p, uint64_t bytes) {
+    hipError_t e = hipMalloc((void**)&p->ring_dev, bytes);
+    if (e == hipSuccess) e = hipHostMalloc((void**)&p->ring_host, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        free_rings(p);
+        return AQUA_ERR_HIP;
+    }
+    p->ring_bytes = bytes;
+    p->ring_head = 0;
+    return AQUA_OK;
+}
+
+// Reserves `bytes` of the descriptor rings, waiting for the calls that used
+// the space last.  Grows the rings when one call needs more than they hold.
+aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off) {
+    bytes = (bytes + 255) & ~255ull;
+    if (bytes > p->ring_bytes) {
+        aqua_status st = wait_all(p);
+        if (st != AQUA_OK) return st;
+        uint64_t nb = p->ring_bytes ? p->ring_bytes : kDefaultRingBytes;
+        while (nb < bytes) nb *= 2;
+        free_rings(p);
+        st = alloc_rings(p, nb);
+        if (st != AQUA_OK) return st;
+    }
+    uint64_t lo = p->ring_head;
+    if (lo + bytes > p->ring_bytes) lo = 0;
+    const uint64_t hi = lo + bytes;
+    for (;;) {
+        bool overlap = false;
+        for (const RingUse& u : p->ring_uses)
+            if (u.lo < hi && lo < u.hi) {
+                overlap = true;
+                break;
+            }
+        if (!overlap) break;
+        const aqua_status st = wait_ticket(p, p->ring_uses.front().ticket);
+        if (st != AQUA_OK) return st;
+        p->ring_uses.pop_front();
+    }
+    p->ring_head = hi;
+    *off = lo;
+    return AQUA_OK;
+}
+
+// Device-accessible address of the buffer, after checking that its memory
+// class matches the target and that [ptr, ptr + bytes) lies in one
+// allocation.
+aqua_status resolve_buffer(aqua_kv_pool* p, const void* ptr, uint64_t bytes,
+                           int32_t target, uint8_t** dev) {
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof(attr));
+    hipError_t e = hipPointerGetAttributes(&attr, ptr);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return AQUA_ERR_INVALID;
+    }
+    if (target == AQUA_TARGET_DEVICE) {
+        if (attr.type != hipMemoryTypeDevice || attr.device != p->device)
+            return AQUA_ERR_INVALID;
+        *dev = (uint8_t*)const_cast<void*>(ptr);
+    } else {
+        if (attr.type != hipMemoryTypeHost || !attr.devicePointer)
+            return AQUA_ERR_INVALID;
+        *dev = (uint8_t*)attr.devicePointer;
+    }
+    hipDeviceptr_t rbase = nullptr;
+    size_t rsize = 0;
+    e = hipMemGetAddressRange(&rbase, &rsize, (hipDeviceptr_t)*dev);
+    if (e == hipSuccess && rbase) {
+        const uintptr_t b = (uintptr_t)rbase, x = (uintptr_t)*dev;
+        if (x < b || x - b > rsize || bytes > rsize - (x - b)) return AQUA_ERR_INVALID;
+    } else {
+        (void)hipGetLastError();
+        if (target == AQUA_TARGET_DEVICE) return AQUA_ERR_INVALID;
+    }
+    return AQUA_OK;
+}
+
+aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
+                    const int32_t* ids, const uint64_t* offs, const void* buf,
+                    uint64_t buf_bytes, const uint64_t* img_offsets,
+                    int32_t target, void* stream_ptr, uint64_t* ticket_out) {
+    if (!p) return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
+    const auto t0 = std::chrono::steady_clock::now();
+
+    aqua::CallArgs a;
+    a.num_seqs = num_seqs;
+    a.ids = ids;
+    a.offs = offs;
+    a.img_offsets = img_offsets;
+    a.buf = (uintptr_t)buf;
+    a.buf_bytes = buf_bytes;
+    a.is_in = is_in;
+    aqua_status st = (target == AQUA_TARGET_DEVICE || target == AQUA_TARGET_HOST)
+                         ? aqua::validate_call(p->shape, a, p->marks)
+                         : AQUA_ERR_INVALID;
+    if (st == AQUA_ERR_INVALID) return st;
+    const uint64_t total = num_seqs ? offs[num_seqs] : 0;
+
+    DeviceGuard dg(p->device);
+    if (!dg.ok) {
+        (void)hipGetLastError();
+        return AQUA_ERR_HIP;  // nothing enqueued: not latched
+    }
+
+    uint8_t* dbuf = nullptr;
+    if (total) {
+        const aqua_status pc = resolve_buffer(p, buf, buf_bytes, target, &dbuf);
+        if (pc != AQUA_OK) return pc;
+    }
+    if (st != AQUA_OK) return st;
+
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    st = poll(p);
+    if (st != AQUA_OK) return st;
+
+    const uint32_t lane = lane_for(p, stream);
+    const uint64_t ticket = p->next_ticket;
+
+    p->plan.clear();
+    aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
+    aqua::image_ranges(p->shape, a, &p->ranges);
+    for (auto& r : p->ranges) {  // tracked by the caller's address of the buffer
+        r.first += a.buf;
+        r.second += a.buf;
+    }
+
+    // Reserve descriptor space before registering the ticket: a reservation
+    // may wait on earlier tickets.
+    uint64_t ring_off = 0;
+    const uint64_t dbytes = p->plan.size() * sizeof(RunDesc);
+    if (dbytes) {
+        st = ring_reserve(p, dbytes, &ring_off);
+        if (st != AQUA_OK) return st;
+    }
+
+    p->stats.waits_elided += p->tracker.issue(ticket, lane, is_in, ids, (size_t)total,
+                                              p->ranges.data(), p->ranges.size(),
+                                              &p->deps);
+    p->next_ticket++;
+
+    for (const HazardTracker::Dep& d : p->deps) {
+        hipEvent_t ev = event_of(p, d.ticket);
+        if (!ev) continue;
+        const hipError_t e = hipStreamWaitEvent(stream, ev, 0);
+        if (e != hipSuccess) return latch(p, e);
+        p->stats.waits_inserted++;
+    }
+
+    if (dbytes) {
+        std::memcpy(p->ring_host + ring_off, p->plan.data(), dbytes);
+        hipError_t e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
+                                      hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return latch(p, e);
+        aqua::SwapLaunch L;
+        L.out = !is_in;
+        L.pool = p->base;
+        L.img = dbuf;
+        L.descs = reinterpret_cast<const RunDesc*>(p->ring_dev + ring_off);
+        L.ndesc = (uint32_t)p->plan.size();
+        L.num_layers = p->shape.L;
+        L.chunk_bytes = p->shape.C;
+        L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
+        L.max_workgroups = p->max_wg[target];
+        (void)hipGetLastError();
+        e = aqua::launch_swap(L, stream);
+        if (e != hipSuccess) return latch(p, e);
+    }
+
+    hipEvent_t ev = nullptr;
+    hipError_t e = take_event(p, &ev);
+    if (e == hipSuccess) e = hipEventRecord(ev, stream);
+    if (e != hipSuccess) return latch(p, e);
+    p->outstanding[lane].push_back({ticket, ev});
+    if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
+
+    const uint64_t moved = (uint64_t)p->shape.L * total * p->shape.C;
+    if (is_in) {
+        p->stats.calls_in++;
+        p->stats.bytes_in += moved;
+    } else {
+        p->stats.calls_out++;
+        p->stats.bytes_out += moved;
+    }
+    if (target == AQUA_TARGET_HOST) p->stats.bytes_host += moved;
+    p->stats.descriptors += p->plan.size();
+    p->stats.host_ns += (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                            std::chrono::steady_clock::now() - t0)
+                            .count();
+    if (ticket_out) *ticket_out = ticket;
+    return AQUA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
+                                uint64_t pool_bytes, aqua_kv_pool_t* out) {
+    if (!out) return AQUA_ERR_INVALID;
+    aqua::Shape s;
+    aqua_status st = aqua::make_shape(desc, &s);
+    if (st != AQUA_OK) return st;
+    if (!pool_base || ((uintptr_t)pool_base % 16)) return AQUA_ERR_INVALID;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return AQUA_ERR_HIP;
+    }
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof(attr));
+    if (hipPointerGetAttributes(&attr, pool_base) != hipSuccess) {
+        (void)hipGetLastError();
+        return AQUA_ERR_INVALID;
+    }
+    if (attr.type != hipMemoryTypeDevice || attr.device != dev) return AQUA_ERR_INVALID;
+    hipDeviceptr_t rbase = nullptr;
+    size_t rsize = 0;
+    if (hipMemGetAddressRange(&rbase, &rsize, (hipDeviceptr_t)pool_base) != hipSuccess) {
+        (void)hipGetLastError();
+        return AQUA_ERR_INVALID;
+    }
+    const uintptr_t b = (uintptr_t)rbase, x = (uintptr_t)pool_base;
+    if (x < b || pool_bytes > rsize - (x - b)) return AQUA_ERR_INVALID;
+    if (pool_bytes < s.pool_bytes) return AQUA_ERR_CAPACITY;
+
+    aqua_kv_pool* p = new (std::nothrow) aqua_kv_pool();
+    if (!p) return AQUA_ERR_HIP;
+    p->shape = s;
+    p->device = dev;
+    p->base = (uint8_t*)pool_base;
+    p->bytes = pool_bytes;
+    p->tracker.reset(s.N);
+    // Work per workgroup; capped so that a run's 16-byte vector count fits
+    // the kernels' 32-bit counters.
+    p->unit_bytes = env_u64("AQUA_UNIT_BYTES", kDefaultUnitBytes);
+    if (!p->unit_bytes) p->unit_bytes = kDefaultUnitBytes;
+    if (p->unit_bytes > aqua::kMaxChunkBytes) p->unit_bytes = aqua::kMaxChunkBytes;
+    st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
+    if (st != AQUA_OK) {
+        delete p;
+        return st;
+    }
+    *out = p;
+    return AQUA_OK;
+}
+
+aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
+    if (!p) return AQUA_ERR_INVALID;
+    aqua_status st = AQUA_OK;
+    {
+        DeviceGuard dg(p->device);
+        if (p->sticky == hipSuccess) st = wait_all(p);
+        for (auto& q : p->outstanding)
+            for (const Outstanding& o : q) (void)hipEventDestroy(o.ev);
+        for (hipEvent_t ev : p->spare_events) (void)hipEventDestroy(ev);
+        free_rings(p);
+        if (p->sticky != hipSuccess) st = AQUA_ERR_HIP;
+    }
+    delete p;
+    return st;
+}
+
+aqua_status aqua_swap_out(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* block_ids,
+                          const uint64_t* seq_offsets, void* dst, uint64_t dst_bytes,
+                          const uint64_t* img_offsets, int32_t target, void* stream,
+                          uint64_t* ticket) {
+    return do_swap(pool, false, num_seqs, block_ids, seq_offsets, dst, dst_bytes, img_offsets,
+                   target, stream, ticket);
+}
+
+aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* block_ids,
+                         const uint64_t* seq_offsets, const void* src, uint64_t src_bytes,
+                         const uint64_t* img_offsets, int32_t target, void* stream,
+                         uint64_t* ticket) {
+    return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
+                   target, stream, ticket);
+}
+
+aqua_status aqua_sync(aqua_kv_pool_t p, uint64_t ticket) {
+    if (!p) return AQUA_ERR_INVALID;
+    if (ticket >= p->next_ticket) return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_HIP;
+    DeviceGuard dg(p->device);
+    aqua_status st = ticket ? wait_ticket(p, ticket) : wait_all(p);
+    if (st == AQUA_OK && p->sticky != hipSuccess) st = AQUA_ERR_HIP;
+    return st;
+}
+
+aqua_status aqua_stream_wait(aqua_kv_pool_t p, uint64_t ticket, void* stream) {
+    if (!p) return AQUA_ERR_INVALID;
+    if (ticket >= p->next_ticket) return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
+    DeviceGuard dg(p->device);
+    aqua_status st = poll(p);
+    if (st != AQUA_OK) return st;
+    for (uint32_t m = 0; m < p->outstanding.size(); ++m) {
+        const auto& q = p->outstanding[m];
+        if (q.empty()) continue;
+        hipEvent_t ev = nullptr;
+        if (ticket == 0) {
+            ev = q.back().ev;
+        } else if (p->tracker.lane_of(ticket) == m) {
+            ev = event_of(p, ticket);
+        }
+        if (!ev) continue;
+        const hipError_t e = hipStreamWaitEvent((hipStream_t)stream, ev, 0);
+        if (e != hipSuccess) return latch(p, e);
+    }
+    return AQUA_OK;
+}
+
+aqua_status aqua_query(aqua_kv_pool_t p, uint64_t ticket) {
+    if (!p || ticket == 0 || ticket >= p->next_ticket) return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
+    DeviceGuard dg(p->device);
+    const aqua_status st = poll(p);
+    if (st != AQUA_OK) return st;
+    return ticket <= p->tracker.completed(p->tracker.lane_of(ticket)) ? 1 : 0;
+}
+
+aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t p, int32_t target,
+                                            uint32_t max_workgroups) {
+    if (!p || (target != AQUA_TARGET_DEVICE && target != AQUA_TARGET_HOST))
+        return AQUA_ERR_INVALID;
+    p->max_wg[target] = max_workgroups;
+    return AQUA_OK;
+}
+
+aqua_status aqua_pool_stats_get(aqua_kv_pool_t p, aqua_pool_stats* out) {
+    if (!p || !out) return AQUA_ERR_INVALID;
+    *out = p->stats;
+    return AQUA_OK;
+}
+
+const char* aqua_status_str(aqua_status s) {
+    switch (s) {
+        case AQUA_OK: return "ok";
+        case AQUA_ERR_INVALID: return "invalid argument";
+        case AQUA_ERR_RANGE: return "block id out of range";
+        case AQUA_ERR_DUPLICATE: return "duplicate destination";
+        case AQUA_ERR_CAPACITY: return "image does not fit the buffer";
+        case AQUA_ERR_HIP: return "HIP runtime failure";
+        case AQUA_ERR_STATE: return "pool unusable after a HIP failure";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

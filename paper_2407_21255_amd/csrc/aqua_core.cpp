@@ -1,0 +1,278 @@
+// aqua_core.cpp -- validation, run planning and hazard tracking (host only).
+#include "aqua_core.h"
+
+#include <algorithm>
+
+namespace aqua {
+
+namespace {
+
+uint64_t elem_bytes(int32_t dtype) {
+    switch (dtype) {
+        case AQUA_F16:
+        case AQUA_BF16:
+            return 2;
+        case AQUA_FP8_E4M3:
+            return 1;
+        default:
+            return 0;
+    }
+}
+
+}  // namespace
+
+aqua_status make_shape(const aqua_kv_desc* d, Shape* out) {
+    if (!d || !out) return AQUA_ERR_INVALID;
+    const uint64_t e = elem_bytes(d->dtype);
+    if (!d->num_layers || !d->num_blocks || !d->num_kv_heads ||
+        !d->block_tokens || !d->head_dim || !e)
+        return AQUA_ERR_INVALID;
+    if (d->num_blocks > 0x7fffffffu) return AQUA_ERR_INVALID;  // int32 ids
+    // Bounds that keep every byte offset, and every kernel's 16-byte vector
+    // count per run, far from overflow.
+    if (d->num_kv_heads > 65536 || d->block_tokens > 65536 || d->head_dim > 65536)
+        return AQUA_ERR_INVALID;
+    const unsigned __int128 C = (unsigned __int128)2 * d->num_kv_heads *
+                                d->block_tokens * d->head_dim * e;
+    if (C > kMaxChunkBytes) return AQUA_ERR_INVALID;
+    if ((unsigned __int128)d->num_layers * d->num_blocks * C > kMaxBytes)
+        return AQUA_ERR_INVALID;
+    Shape s;
+    s.L = d->num_layers;
+    s.N = d->num_blocks;
+    s.H = d->num_kv_heads;
+    s.T = d->block_tokens;
+    s.D = d->head_dim;
+    s.dtype = d->dtype;
+    s.C = 2ull * s.H * s.T * s.D * e;
+    if (s.C % 16) return AQUA_ERR_INVALID;
+    s.pool_bytes = (uint64_t)s.L * s.N * s.C;
+    *out = s;
+    return AQUA_OK;
+}
+
+uint64_t image_offset(const Shape& s, const CallArgs& a, uint32_t k) {
+    if (a.img_offsets) return a.img_offsets[k];
+    // Packed: images one after another in sequence order.
+    return (uint64_t)s.L * a.offs[k] * s.C;
+}
+
+aqua_status validate_call(const Shape& s, const CallArgs& a, DupMarks& marks) {
+    // -- invalid
+    if (a.num_seqs && !a.offs) return AQUA_ERR_INVALID;
+    const uint64_t total = a.num_seqs ? a.offs[a.num_seqs] : 0;
+    if (a.num_seqs) {
+        if (a.offs[0] != 0) return AQUA_ERR_INVALID;
+        for (uint32_t k = 0; k < a.num_seqs; ++k)
+            if (a.offs[k + 1] < a.offs[k]) return AQUA_ERR_INVALID;
+    }
+    if (total && (!a.ids || !a.buf)) return AQUA_ERR_INVALID;
+    if (a.buf % 16) return AQUA_ERR_INVALID;
+    if (a.img_offsets)
+        for (uint32_t k = 0; k < a.num_seqs; ++k)
+            if (a.img_offsets[k] % 16) return AQUA_ERR_INVALID;
+
+    // -- range
+    for (uint64_t j = 0; j < total; ++j)
+        if (a.ids[j] < 0 || (uint32_t)a.ids[j] >= s.N) return AQUA_ERR_RANGE;
+
+    // -- duplicate
+    if (a.is_in) {
+        if (marks.mark.size() < s.N) {
+            marks.mark.assign(s.N, 0);
+            marks.epoch = 0;
+        }
+        if (++marks.epoch == 0) {  // wrapped: clear and restart
+            std::fill(marks.mark.begin(), marks.mark.end(), 0);
+            marks.epoch = 1;
+        }
+        for (uint64_t j = 0; j < total; ++j) {
+            uint32_t& m = marks.mark[(uint32_t)a.ids[j]];
+            if (m == marks.epoch) return AQUA_ERR_DUPLICATE;
+            m = marks.epoch;
+        }
+    } else if (a.img_offsets) {
+        // Packed images never overlap; placed ones must not either.
+        std::vector<std::pair<uint64_t, uint64_t>> r;
+        image_ranges(s, a, &r);
+        std::sort(r.begin(), r.end());
+        for (size_t k = 1; k < r.size(); ++k)
+            if (r[k].first < r[k - 1].second) return AQUA_ERR_DUPLICATE;
+    }
+
+    // -- capacity (128-bit so that absurd tables cannot wrap around)
+    for (uint32_t k = 0; k < a.num_seqs; ++k) {
+        const uint64_t n = a.offs[k + 1] - a.offs[k];
+        if (!n) continue;
+        const unsigned __int128 off =
+            a.img_offsets ? (unsigned __int128)a.img_offsets[k]
+                          : (unsigned __int128)s.L * a.offs[k] * s.C;
+        const unsigned __int128 len = (unsigned __int128)s.L * n * s.C;
+        if (off + len > a.buf_bytes) return AQUA_ERR_CAPACITY;
+    }
+    return AQUA_OK;
+}
+
+void image_ranges(const Shape& s, const CallArgs& a,
+                  std::vector<std::pair<uint64_t, uint64_t>>* out) {
+    out->clear();
+    for (uint32_t k = 0; k < a.num_seqs; ++k) {
+        const uint64_t n = a.offs[k + 1] - a.offs[k];
+        if (!n) continue;
+        const uint64_t lo = image_offset(s, a, k);
+        out->emplace_back(lo, lo + (uint64_t)s.L * n * s.C);
+    }
+}
+
+size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
+                 std::vector<RunDesc>* out) {
+    const size_t before = out->size();
+    const uint64_t max_run = std::max<uint64_t>(1, max_unit_bytes / s.C);
+    for (uint32_t k = 0; k < a.num_seqs; ++k) {
+        const uint64_t first = a.offs[k], n = a.offs[k + 1] - first;
+        if (!n) continue;
+        const int32_t* bt = a.ids + first;
+        const uint64_t base = image_offset(s, a, k);
+        const uint64_t lstride = n * s.C;
+        uint64_t i = 0;
+        while (i < n) {
+            uint64_t len = 1;
+            while (i + len < n && len < max_run &&
+                   bt[i + len] == bt[i + len - 1] + 1)
+                ++len;
+            RunDesc d;
+            d.img_off = base + i * s.C;
+            d.img_lstride = lstride;
+            d.block = (uint32_t)bt[i];
+            d.nchunks = (uint32_t)len;
+            d.reserved0 = d.reserved1 = 0;
+            out->push_back(d);
+            i += len;
+        }
+    }
+    return out->size() - before;
+}
+
+// ---------------------------------------------------------------------------
+
+void HazardTracker::reset(uint32_t num_blocks) {
+    last_writer_.assign(num_blocks, 0);
+    readers_.assign(num_blocks, {});
+    ranges_.clear();
+    done_.clear();
+    dep_.clear();
+    ticket_lane_.assign(1, 0);
+    last_ticket_ = 0;
+}
+
+void HazardTracker::ensure_lane(uint32_t lane) {
+    if (lane >= done_.size()) {
+        done_.resize(lane + 1, 0);
+        dep_.resize(lane + 1, 0);
+    }
+}
+
+uint32_t HazardTracker::lane_of(uint64_t ticket) const {
+    return ticket < ticket_lane_.size() ? ticket_lane_[ticket] : 0;
+}
+
+bool HazardTracker::done(uint64_t ticket) const {
+    const uint32_t m = lane_of(ticket);
+    return ticket <= done_[m];
+}
+
+uint64_t HazardTracker::completed(uint32_t lane) const {
+    return lane < done_.size() ? done_[lane] : 0;
+}
+
+void HazardTracker::complete(uint32_t lane, uint64_t ticket) {
+    ensure_lane(lane);
+    if (ticket > done_[lane]) done_[lane] = ticket;
+}
+
+void HazardTracker::need(uint64_t ticket, uint32_t lane, uint64_t* elided) {
+    if (!ticket) return;
+    if (done(ticket)) {
+        ++*elided;
+        return;
+    }
+    const uint32_t m = lane_of(ticket);
+    if (m == lane) return;  // same stream: ordered by the stream itself
+    if (ticket > dep_[m]) dep_[m] = ticket;
+}
+
+uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, bool is_in,
+                              const int32_t* blocks, size_t nblocks,
+                              const std::pair<uint64_t, uint64_t>* ranges,
+                              size_t nranges, std::vector<Dep>* deps) {
+    ensure_lane(lane);
+    deps->clear();
+    std::fill(dep_.begin(), dep_.end(), 0);
+    if (ticket_lane_.size() <= ticket) ticket_lane_.resize(ticket + 1, 0);
+    ticket_lane_[ticket] = lane;
+    last_ticket_ = ticket;
+    uint64_t elided = 0;
+
+    // Offload ranges: drop finished records, then look for overlaps.
+    size_t w = 0;
+    for (size_t k = 0; k < ranges_.size(); ++k)
+        if (!done(ranges_[k].ticket)) ranges_[w++] = ranges_[k];
+    ranges_.resize(w);
+    const size_t old = ranges_.size();
+    for (size_t r = 0; r < nranges; ++r) {
+        const uint64_t lo = ranges[r].first, hi = ranges[r].second;
+        for (size_t k = 0; k < old; ++k) {
+            const RangeRec& q = ranges_[k];
+            if (q.lo < hi && lo < q.hi && (q.write || !is_in))
+                need(q.ticket, lane, &elided);
+        }
+    }
+    if (!is_in) {
+        // A write that covers an earlier record is ordered after it, and
+        // every later access that conflicts with the record conflicts with
+        // the write too: the record can go.
+        size_t k = 0;
+        for (size_t i = 0; i < old; ++i) {
+            bool covered = false;
+            for (size_t r = 0; r < nranges && !covered; ++r)
+                covered = ranges[r].first <= ranges_[i].lo && ranges_[i].hi <= ranges[r].second;
+            if (!covered) ranges_[k++] = ranges_[i];
+        }
+        ranges_.resize(k);
+    }
+    for (size_t r = 0; r < nranges; ++r)
+        ranges_.push_back({ranges[r].first, ranges[r].second, ticket, lane, !is_in});
+
+    // Pool blocks.
+    for (size_t j = 0; j < nblocks; ++j) {
+        const uint32_t b = (uint32_t)blocks[j];
+        need(last_writer_[b], lane, &elided);
+        std::vector<Reader>& rd = readers_[b];
+        if (is_in) {
+            for (const Reader& q : rd) need(q.ticket, lane, &elided);
+            rd.clear();
+            last_writer_[b] = ticket;
+        } else {
+            bool found = false;
+            for (Reader& q : rd)
+                if (q.lane == lane) {
+                    q.ticket = ticket;
+                    found = true;
+                }
+            if (!found) {
+                // Forget readers that have finished before adding one.
+                size_t k = 0;
+                for (size_t i = 0; i < rd.size(); ++i)
+                    if (!done(rd[i].ticket)) rd[k++] = rd[i];
+                rd.resize(k);
+                rd.push_back({lane, ticket});
+            }
+        }
+    }
+
+    for (uint32_t m = 0; m < dep_.size(); ++m)
+        if (dep_[m]) deps->push_back({m, dep_[m]});
+    return elided;
+}
+
+}  // namespace aqua

@@ -1,0 +1,141 @@
+// aqua_core.h -- host-side core of the KV page-swap library: argument
+// validation, run planning and cross-stream hazard tracking.  Pure C++17,
+// no HIP types, so that it builds and is tested on a machine without a GPU.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <utility>
+#include <vector>
+
+#include "aqua.h"
+
+namespace aqua {
+
+// Pool geometry.  One (layer, block) chunk of the pool
+// [L][N][2][H][T][D] is C = 2*H*T*D*elem contiguous bytes.
+struct Shape {
+    uint32_t L = 0, N = 0, H = 0, T = 0, D = 0;
+    int32_t dtype = 0;
+    uint64_t C = 0;          // chunk bytes
+    uint64_t pool_bytes = 0; // L*N*C
+};
+
+// Largest chunk (1 GiB) and largest pool or image (2^62 bytes) accepted.
+constexpr uint64_t kMaxChunkBytes = 1ull << 30;
+constexpr uint64_t kMaxBytes = 1ull << 62;
+
+// Fills *out from a descriptor; AQUA_ERR_INVALID for a zero dimension, an
+// unknown dtype, or a chunk that is not a multiple of 16 bytes.
+aqua_status make_shape(const aqua_kv_desc* d, Shape* out);
+
+// One swap call as the caller described it.
+struct CallArgs {
+    uint32_t num_seqs = 0;
+    const int32_t* ids = nullptr;
+    const uint64_t* offs = nullptr;        // num_seqs+1 CSR offsets
+    const uint64_t* img_offsets = nullptr; // nullptr: packed images
+    uintptr_t buf = 0;                     // offload buffer address
+    uint64_t buf_bytes = 0;
+    bool is_in = false;                    // swap-in: destinations are blocks
+};
+
+// Work item of the copy kernels: a run of `nchunks` consecutive pool blocks
+// starting at `block` whose image chunks are also consecutive.  In layer l
+// the pool side starts at (l*N + block)*C and the image side at
+// img_off + l*img_lstride.  32 bytes so that one scalar load fetches it.
+struct alignas(16) RunDesc {
+    uint64_t img_off;
+    uint64_t img_lstride;
+    uint32_t block;
+    uint32_t nchunks;
+    uint32_t reserved0;
+    uint32_t reserved1;
+};
+static_assert(sizeof(RunDesc) == 32, "descriptor layout is shared with the kernels");
+
+// Reusable scratch for duplicate detection (epoch-stamped marks, O(n)).
+struct DupMarks {
+    std::vector<uint32_t> mark;
+    uint32_t epoch = 0;
+};
+
+// Validation in the library's precedence: invalid -> range -> duplicate ->
+// capacity.  Pointer classes are checked by the caller (they need HIP).
+aqua_status validate_call(const Shape& s, const CallArgs& a, DupMarks& marks);
+
+// Byte offset of sequence k's image inside the buffer.
+uint64_t image_offset(const Shape& s, const CallArgs& a, uint32_t k);
+
+// Coalesces each table into runs bt[i+1] == bt[i] + 1, split so that a run
+// covers at most max(1, max_unit_bytes / C) chunks.  Appends to *out and
+// returns the number of descriptors appended.
+size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
+                 std::vector<RunDesc>* out);
+
+// Half-open byte ranges [lo, hi) of the buffer that the call touches (one
+// per non-empty sequence).
+void image_ranges(const Shape& s, const CallArgs& a,
+                  std::vector<std::pair<uint64_t, uint64_t>>* out);
+
+// ---------------------------------------------------------------------------
+// Hazard tracker.
+//
+// Every call gets a ticket (1, 2, 3, ...) and runs on a "lane" (one lane
+// per distinct stream).  Work on one lane completes in issue order, so a
+// dependency on ticket t of lane m is satisfied by waiting on the newest
+// conflicting ticket of m.  Per pool block the tracker keeps the last
+// writing ticket and, per lane, the newest ticket reading it since that
+// write; per offload byte range it keeps the in-flight readers and writers.
+// Tickets known complete (per-lane watermark) are never waited on.
+class HazardTracker {
+public:
+    struct Dep {
+        uint32_t lane;
+        uint64_t ticket;
+    };
+
+    explicit HazardTracker(uint32_t num_blocks = 0) { reset(num_blocks); }
+    void reset(uint32_t num_blocks);
+
+    // Registers call `ticket` (must exceed every earlier ticket) on `lane`.
+    // Swap-out (is_in false) reads `blocks` and writes `ranges`; swap-in
+    // reads `ranges` and writes `blocks`.  Writes into *deps, per other
+    // lane, the newest earlier ticket the call must wait for.  Returns the
+    // number of conflicts that were skipped because already complete.
+    uint64_t issue(uint64_t ticket, uint32_t lane, bool is_in,
+                   const int32_t* blocks, size_t nblocks,
+                   const std::pair<uint64_t, uint64_t>* ranges, size_t nranges,
+                   std::vector<Dep>* deps);
+
+    // Everything on `lane` up to and including `ticket` has completed.
+    void complete(uint32_t lane, uint64_t ticket);
+    uint64_t completed(uint32_t lane) const;
+    uint32_t lane_of(uint64_t ticket) const;
+    size_t live_ranges() const { return ranges_.size(); }
+    uint64_t last_ticket() const { return last_ticket_; }
+
+private:
+    struct Reader {
+        uint32_t lane;
+        uint64_t ticket;
+    };
+    struct RangeRec {
+        uint64_t lo, hi, ticket;
+        uint32_t lane;
+        bool write;
+    };
+    void ensure_lane(uint32_t lane);
+    bool done(uint64_t ticket) const;
+    void need(uint64_t ticket, uint32_t lane, uint64_t* elided);
+
+    std::vector<uint64_t> last_writer_;
+    std::vector<std::vector<Reader>> readers_;
+    std::vector<RangeRec> ranges_;
+    std::vector<uint64_t> done_;        // per lane watermark
+    std::vector<uint64_t> dep_;         // per lane, scratch of one issue()
+    std::vector<uint32_t> ticket_lane_; // index: ticket
+    uint64_t last_ticket_ = 0;
+};
+
+}  // namespace aqua

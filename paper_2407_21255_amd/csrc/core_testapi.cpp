@@ -1,0 +1,85 @@
+// core_testapi.cpp -- C entry points into the host core for CPU tests.
+// Built into a separate library (libaqua_core.so) with the system C++
+// compiler; the GPU library does not contain these symbols.
+#include <cstring>
+#include <vector>
+
+#include "aqua.h"
+#include "aqua_core.h"
+
+extern "C" {
+
+aqua_status aqua_core_validate(const aqua_kv_desc* desc, uint32_t num_seqs,
+                               const int32_t* ids, const uint64_t* offs,
+                               uint64_t buf_addr, uint64_t buf_bytes,
+                               const uint64_t* img_offsets, int32_t is_in) {
+    aqua::Shape s;
+    aqua_status st = aqua::make_shape(desc, &s);
+    if (st != AQUA_OK) return st;
+    aqua::CallArgs a;
+    a.num_seqs = num_seqs;
+    a.ids = ids;
+    a.offs = offs;
+    a.img_offsets = img_offsets;
+    a.buf = (uintptr_t)buf_addr;
+    a.buf_bytes = buf_bytes;
+    a.is_in = is_in != 0;
+    aqua::DupMarks marks;
+    return aqua::validate_call(s, a, marks);
+}
+
+// Writes up to max_out descriptors (32 bytes each) and returns how many the
+// plan has; negative status for an invalid shape.
+int64_t aqua_core_plan(const aqua_kv_desc* desc, uint32_t num_seqs,
+                       const int32_t* ids, const uint64_t* offs,
+                       const uint64_t* img_offsets, uint64_t unit_bytes,
+                       void* out, uint64_t max_out) {
+    aqua::Shape s;
+    aqua_status st = aqua::make_shape(desc, &s);
+    if (st != AQUA_OK) return st;
+    aqua::CallArgs a;
+    a.num_seqs = num_seqs;
+    a.ids = ids;
+    a.offs = offs;
+    a.img_offsets = img_offsets;
+    std::vector<aqua::RunDesc> plan;
+    aqua::plan_runs(s, a, unit_bytes, &plan);
+    const uint64_t n = plan.size() < max_out ? plan.size() : max_out;
+    if (n) std::memcpy(out, plan.data(), n * sizeof(aqua::RunDesc));
+    return (int64_t)plan.size();
+}
+
+void* aqua_core_tracker_new(uint32_t num_blocks) {
+    return new aqua::HazardTracker(num_blocks);
+}
+
+void aqua_core_tracker_free(void* t) { delete static_cast<aqua::HazardTracker*>(t); }
+
+// ranges: nranges pairs (lo, hi).  Returns the number of dependencies and
+// writes them to dep_lanes / dep_tickets (at most max_deps).
+int64_t aqua_core_tracker_issue(void* t, uint64_t ticket, uint32_t lane,
+                                int32_t is_in, const int32_t* blocks,
+                                uint64_t nblocks, const uint64_t* ranges,
+                                uint64_t nranges, uint32_t* dep_lanes,
+                                uint64_t* dep_tickets, uint64_t max_deps) {
+    auto* tr = static_cast<aqua::HazardTracker*>(t);
+    std::vector<std::pair<uint64_t, uint64_t>> r(nranges);
+    for (uint64_t k = 0; k < nranges; ++k) r[k] = {ranges[2 * k], ranges[2 * k + 1]};
+    std::vector<aqua::HazardTracker::Dep> deps;
+    tr->issue(ticket, lane, is_in != 0, blocks, nblocks, r.data(), r.size(), &deps);
+    for (uint64_t k = 0; k < deps.size() && k < max_deps; ++k) {
+        dep_lanes[k] = deps[k].lane;
+        dep_tickets[k] = deps[k].ticket;
+    }
+    return (int64_t)deps.size();
+}
+
+void aqua_core_tracker_complete(void* t, uint32_t lane, uint64_t ticket) {
+    static_cast<aqua::HazardTracker*>(t)->complete(lane, ticket);
+}
+
+uint64_t aqua_core_tracker_live_ranges(void* t) {
+    return static_cast<aqua::HazardTracker*>(t)->live_ranges();
+}
+
+}  // extern "C"

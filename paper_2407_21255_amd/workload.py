@@ -412,3 +412,25 @@ def preemption_schedule(shape: KVShape = LLAMA8B_FP8, seed: int = 5,
                             {p: list(t) for p, t in tables.items()}))
     return Schedule(shape, seed, lengths, nblocks, slot_offsets, region,
                     list(range(n_resident)), initial_tables, slices)
+
+
+def mutation_writes(sched: Schedule, s: int):
+    """Host writes after slice s, so that a stale image cannot pass as a
+    fresh one: (pool byte offsets, 16-byte payloads) for every resident
+    prompt -- two copies of a 64-bit word at the start of its last logical
+    block in layer s mod L -- and the offload slots just swapped back in,
+    which are overwritten with CONSUMED_BYTE: [(offset, length)]."""
+    sh = sched.shape
+    C = sh.chunk_bytes
+    l = s % sh.num_layers
+    sl = sched.slices[s]
+    offs, words = [], []
+    for p in sl.resident_after:
+        b = sl.tables_after[p][-1]
+        offs.append((l * sh.num_blocks + b) * C)
+        w = sched.mutation(s, p)
+        words.append(np.frombuffer(w.to_bytes(8, "little") * 2, dtype=np.uint8))
+    slots = [(sched.slot_offsets[p], sh.image_bytes(sched.nblocks[p]))
+             for p in sl.in_prompts]
+    return (np.asarray(offs, dtype=np.int64),
+            np.stack(words) if words else np.zeros((0, 16), np.uint8), slots)

@@ -42,13 +42,17 @@ def image_chunks(buf: np.ndarray, off: int, L: int, n: int, C: int) -> np.ndarra
     return buf[off:off + L * n * C].reshape(L, n, C)
 
 
-def assert_bytes_equal(a: np.ndarray, b: np.ndarray, what: str = "") -> None:
-    """Byte-exact comparison that names the first differing offset."""
+def assert_bytes_equal(a: np.ndarray, b: np.ndarray, what: str = "",
+                       slab: int = 1 << 28) -> None:
+    """Byte-exact comparison that names the first differing offset.  Large
+    arrays are compared slab by slab to bound temporary memory."""
     a = np.ascontiguousarray(a).reshape(-1).view(np.uint8)
     b = np.ascontiguousarray(b).reshape(-1).view(np.uint8)
     assert a.size == b.size, f"{what}: size {a.size} != {b.size}"
-    if not np.array_equal(a, b):
-        bad = np.flatnonzero(a != b)
-        raise AssertionError(
-            f"{what}: {bad.size} bytes differ, first at {int(bad[0])} "
-            f"({int(a[bad[0]]):#04x} != {int(b[bad[0]]):#04x})")
+    for s in range(0, a.size, slab):
+        x, y = a[s:s + slab], b[s:s + slab]
+        if not np.array_equal(x, y):
+            bad = np.flatnonzero(x != y)
+            raise AssertionError(
+                f"{what}: {bad.size} bytes differ in slab at {s}, first at "
+                f"{s + int(bad[0])} ({int(x[bad[0]]):#04x} != {int(y[bad[0]]):#04x})")

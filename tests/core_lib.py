@@ -1,0 +1,102 @@
+"""ctypes access to libaqua_core.so: the library's host core (validation,
+run planning, hazard tracking) built without HIP for CPU tests."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CORE = os.path.join(ROOT, "paper_2407_21255_amd", "libaqua_core.so")
+
+RUN_DESC = np.dtype([("img_off", "<u8"), ("img_lstride", "<u8"), ("block", "<u4"),
+                     ("nchunks", "<u4"), ("r0", "<u4"), ("r1", "<u4")])
+assert RUN_DESC.itemsize == 32
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_uint32), ("num_blocks", ctypes.c_uint32),
+                ("num_kv_heads", ctypes.c_uint32), ("block_tokens", ctypes.c_uint32),
+                ("head_dim", ctypes.c_uint32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(CORE):
+            from paper_2407_21255_amd import build
+            build.build_core()
+        L = ctypes.CDLL(CORE)
+        P, u32, u64, i32, i64 = (ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64,
+                                 ctypes.c_int32, ctypes.c_int64)
+        L.aqua_core_validate.argtypes = [ctypes.POINTER(Desc), u32, P, P, u64, u64, P, i32]
+        L.aqua_core_validate.restype = i32
+        L.aqua_core_plan.argtypes = [ctypes.POINTER(Desc), u32, P, P, P, u64, P, u64]
+        L.aqua_core_plan.restype = i64
+        L.aqua_core_tracker_new.argtypes = [u32]
+        L.aqua_core_tracker_new.restype = P
+        L.aqua_core_tracker_free.argtypes = [P]
+        L.aqua_core_tracker_issue.argtypes = [P, u64, u32, i32, P, u64, P, u64, P, P, u64]
+        L.aqua_core_tracker_issue.restype = i64
+        L.aqua_core_tracker_complete.argtypes = [P, u32, u64]
+        L.aqua_core_tracker_live_ranges.argtypes = [P]
+        L.aqua_core_tracker_live_ranges.restype = u64
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def validate(desc: Desc, ids, offs, buf_addr, buf_bytes, img_offsets=None, is_in=False,
+             num_seqs=None):
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    offs = np.ascontiguousarray(offs, dtype=np.uint64)
+    io = None if img_offsets is None else np.ascontiguousarray(img_offsets, dtype=np.uint64)
+    ns = len(offs) - 1 if num_seqs is None else num_seqs
+    return lib().aqua_core_validate(ctypes.byref(desc), ns, _p(ids), _p(offs), buf_addr,
+                                    buf_bytes, _p(io), int(is_in))
+
+
+def plan(desc: Desc, ids, offs, img_offsets=None, unit_bytes=64 << 10):
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    offs = np.ascontiguousarray(offs, dtype=np.uint64)
+    io = None if img_offsets is None else np.ascontiguousarray(img_offsets, dtype=np.uint64)
+    n = lib().aqua_core_plan(ctypes.byref(desc), len(offs) - 1, _p(ids), _p(offs), _p(io),
+                             unit_bytes, None, 0)
+    assert n >= 0, n
+    out = np.zeros(n, dtype=RUN_DESC)
+    lib().aqua_core_plan(ctypes.byref(desc), len(offs) - 1, _p(ids), _p(offs), _p(io),
+                         unit_bytes, _p(out), n)
+    return out
+
+
+class Tracker:
+    def __init__(self, num_blocks: int):
+        self.h = lib().aqua_core_tracker_new(num_blocks)
+
+    def issue(self, ticket, lane, is_in, blocks, ranges):
+        b = np.ascontiguousarray(blocks, dtype=np.int32)
+        r = np.ascontiguousarray(np.asarray(ranges, dtype=np.uint64).reshape(-1))
+        lanes = np.zeros(64, dtype=np.uint32)
+        tickets = np.zeros(64, dtype=np.uint64)
+        n = lib().aqua_core_tracker_issue(self.h, ticket, lane, int(is_in), _p(b), b.size,
+                                          _p(r), r.size // 2, _p(lanes), _p(tickets), 64)
+        assert 0 <= n <= 64
+        return [(int(lanes[k]), int(tickets[k])) for k in range(n)]
+
+    def complete(self, lane, ticket):
+        lib().aqua_core_tracker_complete(self.h, lane, ticket)
+
+    def live_ranges(self):
+        return int(lib().aqua_core_tracker_live_ranges(self.h))
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            lib().aqua_core_tracker_free(self.h)
+            self.h = None

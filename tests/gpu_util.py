@@ -1,0 +1,93 @@
+"""Helpers for the GPU parity tests: generated inputs on the device, host
+copies for the oracle, and the oracle's replay of a preemption schedule."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2407_21255_amd import workload as wl
+
+
+def say(*a):
+    """Progress line that reaches the log even if the process dies next."""
+    print(*a, file=sys.stderr, flush=True)
+
+
+def odesc(shape: wl.KVShape) -> oracle.KVDesc:
+    return oracle.desc(*shape.as_tuple())
+
+
+def device_pool(shape: wl.KVShape, seed: int, owner=None, extra: int = 0) -> torch.Tensor:
+    pool = torch.empty(shape.pool_bytes + extra, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, shape, seed, owner)
+    if extra:
+        pool[shape.pool_bytes:].fill_(wl.GUARD_BYTE)
+    return pool
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    """Host copy (pageable numpy array) of a tensor."""
+    torch.cuda.synchronize()
+    return t.detach().to("cpu", copy=True).numpy()
+
+
+def guarded_buffer(nbytes: int, guard: int = 4096, pinned: bool = False) -> torch.Tensor:
+    if pinned:
+        buf = torch.empty(nbytes + 2 * guard, dtype=torch.uint8, pin_memory=True)
+    else:
+        buf = torch.empty(nbytes + 2 * guard, dtype=torch.uint8, device="cuda")
+    buf.fill_(wl.GUARD_BYTE)
+    return buf
+
+
+def region_for(sched: wl.Schedule, device="cuda") -> torch.Tensor:
+    """Offload region of a preemption schedule: guard bytes everywhere, and
+    the initial images of the prompts that start swapped out."""
+    reg = torch.empty(sched.region_bytes, dtype=torch.uint8, device=device)
+    reg.fill_(wl.GUARD_BYTE)
+    sh = sched.shape
+    C = sh.chunk_bytes
+    for p in range(len(sched.nblocks)):
+        if p in sched.initial_resident:
+            continue
+        o, n = sched.slot_offsets[p], sched.nblocks[p]
+        wl.fill_chunks(reg[o:o + sh.image_bytes(n)].view(-1, C),
+                       wl.image_keys(sh, sched.seed, p, n), C, sh.dtype)
+    return reg
+
+
+def schedule_owner(sched: wl.Schedule) -> dict:
+    return {b: (p, i) for p, t in sched.initial_tables.items() for i, b in enumerate(t)}
+
+
+def apply_mutations_host(sched, s, pool_np, region_np):
+    offs, words, slots = wl.mutation_writes(sched, s)
+    for o, w in zip(offs, words):
+        pool_np[o:o + 16] = w
+    for o, n in slots:
+        region_np[o:o + n] = wl.CONSUMED_BYTE
+
+
+def apply_mutations_device(sched, s, pool_t, region_t):
+    offs, words, slots = wl.mutation_writes(sched, s)
+    if len(offs):
+        idx = torch.from_numpy(offs).to(pool_t.device).reshape(-1, 1) + \
+            torch.arange(16, device=pool_t.device).reshape(1, -1)
+        pool_t[idx.reshape(-1)] = torch.from_numpy(words.reshape(-1)).to(pool_t.device)
+    for o, n in slots:
+        region_t[o:o + n].fill_(wl.CONSUMED_BYTE)
+
+
+def oracle_replay(sched, pool_np, region_np, first, count):
+    """The oracle's run of slices [first, first+count) in issue order."""
+    d = odesc(sched.shape)
+    for s in range(first, first + count):
+        sl = sched.slices[s]
+        out_off = [sched.slot_offsets[p] for p in sl.out_prompts]
+        in_off = [sched.slot_offsets[p] for p in sl.in_prompts]
+        assert oracle.swap_out(d, pool_np, sl.out_tables, region_np, out_off) == 0
+        assert oracle.swap_in(d, pool_np, sl.in_tables, region_np, in_off) == 0
+        apply_mutations_host(sched, s, pool_np, region_np)

@@ -1,0 +1,133 @@
+"""Host core on the CPU: validation parity with the oracle, and the run plan."""
+import numpy as np
+import pytest
+
+import oracle
+from tests import core_lib
+
+
+def _desc(L, N, H, T, D, dt):
+    return core_lib.Desc(L, N, H, T, D, dt)
+
+
+def test_validation_status_matches_oracle_on_random_calls():
+    """The library's validation gives the oracle's status for the same call,
+    valid or not (same codes, same precedence)."""
+    rng = np.random.default_rng(21)
+    for case in range(4000):
+        L = int(rng.integers(1, 3))
+        N = int(rng.integers(1, 9))
+        d = (L, N, 1, 2, 8, oracle.F16)
+        C = 2 * 1 * 2 * 8 * 2
+        S = int(rng.integers(0, 4))
+        lens = rng.integers(0, 4, size=S)
+        ids = rng.integers(-1, N + 1, size=int(lens.sum())).astype(np.int32)
+        if rng.random() < 0.5:
+            ids = np.clip(ids, 0, N - 1).astype(np.int32)
+        offs = np.zeros(S + 1, dtype=np.uint64)
+        offs[1:] = np.cumsum(lens)
+        img_offsets = None
+        if rng.random() < 0.5:
+            img_offsets = (rng.integers(0, 6, size=S) * (L * C) +
+                           (8 if rng.random() < 0.05 else 0)).astype(np.uint64)
+        buf = np.zeros(int(rng.integers(0, 8)) * L * C + 16, dtype=np.uint8)
+        pool = np.zeros(L * N * C, dtype=np.uint8)
+        is_in = bool(rng.random() < 0.5)
+        od = oracle.desc(*d)
+        fn = oracle.swap_in if is_in else oracle.swap_out
+        want = fn(od, pool, None, buf, img_offsets, ids=ids, offs=offs,
+                  dst_bytes=buf.nbytes - 16) if not is_in else \
+            fn(od, pool, None, buf, img_offsets, ids=ids, offs=offs,
+               src_bytes=buf.nbytes - 16)
+        got = core_lib.validate(_desc(*d), ids, offs, buf.ctypes.data, buf.nbytes - 16,
+                                img_offsets, is_in)
+        assert got == want, (case, d, ids, offs, img_offsets, is_in)
+
+
+def test_shape_validation():
+    ok = core_lib.validate(_desc(2, 4, 1, 2, 8, oracle.BF16), [], [0], 0, 0)
+    assert ok == 0
+    for bad in [(0, 4, 1, 2, 8, 2), (2, 0, 1, 2, 8, 2), (2, 4, 0, 2, 8, 2),
+                (2, 4, 1, 0, 8, 2), (2, 4, 1, 2, 0, 2), (2, 4, 1, 2, 8, 7),
+                (2, 4, 1, 1, 4, 3),                 # chunk of 8 bytes
+                (2, 4, 1 << 17, 2, 8, 2),           # absurd head count
+                (1 << 31, 1 << 30, 64, 64, 128, 2)]:  # pool beyond 2^62 bytes
+        assert core_lib.validate(_desc(*bad), [], [0], 0, 0) == oracle.ERR_INVALID, bad
+
+
+def test_capacity_arithmetic_cannot_wrap():
+    d = _desc(80, 4096, 8, 16, 128, oracle.BF16)
+    C = 64 * 1024
+    # An image offset near 2^64 must be a capacity error, not a wrapped fit.
+    big = np.array([(1 << 64) - 16], dtype=np.uint64)
+    assert core_lib.validate(d, [1], [0, 1], 4096, 80 * C, big) == oracle.ERR_CAPACITY
+    assert core_lib.validate(d, [1], [0, 1], 4096, 80 * C, [0]) == 0
+    assert core_lib.validate(d, [1], [0, 1], 4096, 80 * C - 16, [0]) == oracle.ERR_CAPACITY
+
+
+def _check_plan(desc_t, tables, img_offsets, unit_bytes):
+    L, N, H, T, D, dt = desc_t
+    e = 1 if dt == oracle.FP8_E4M3 else 2
+    C = 2 * H * T * D * e
+    ids = np.asarray([b for t in tables for b in t], dtype=np.int32)
+    offs = np.zeros(len(tables) + 1, dtype=np.uint64)
+    offs[1:] = np.cumsum([len(t) for t in tables])
+    runs = core_lib.plan(_desc(*desc_t), ids, offs, img_offsets, unit_bytes)
+    max_run = max(1, unit_bytes // C)
+    k = 0
+    packed = 0
+    for s, t in enumerate(tables):
+        n = len(t)
+        base = packed if img_offsets is None else int(img_offsets[s])
+        packed += L * n * C
+        i = 0
+        while i < n:
+            r = runs[k]
+            assert r["block"] == t[i]
+            assert r["img_off"] == base + i * C
+            assert r["img_lstride"] == n * C
+            ln = int(r["nchunks"])
+            assert 1 <= ln <= max_run
+            assert list(t[i:i + ln]) == list(range(t[i], t[i] + ln))
+            # Maximal: the next entry does not extend the run unless capped.
+            if i + ln < n and ln < max_run:
+                assert t[i + ln] != t[i + ln - 1] + 1
+            i += ln
+            k += 1
+    assert k == len(runs)
+    return runs
+
+
+def test_plan_random_tables_cover_exactly_and_are_maximal():
+    rng = np.random.default_rng(22)
+    for case in range(500):
+        N = 64
+        S = int(rng.integers(0, 5))
+        tables = []
+        for _ in range(S):
+            n = int(rng.integers(0, 12))
+            if rng.random() < 0.5:
+                start = int(rng.integers(0, N - n + 1))
+                t = list(range(start, start + n))
+                if n > 2 and rng.random() < 0.5:
+                    t[n // 2] = int(rng.integers(0, N))
+            else:
+                t = [int(x) for x in rng.integers(0, N, size=n)]
+            tables.append(t)
+        dt = oracle.FP8_E4M3 if rng.random() < 0.5 else oracle.BF16
+        unit = int(rng.choice([256, 512, 1024, 4096, 1 << 16]))
+        io = None
+        if rng.random() < 0.5:
+            io = np.cumsum([0] + [3 * 64 * 4 * len(t) for t in tables])[:-1]
+        _check_plan((3, N, 1, 4, 8, dt), tables, io, unit)
+
+
+def test_plan_coalesces_contiguous_tables():
+    # C = 2*8*16*128*1 = 32 KiB (fp8) and 64 KiB units: runs of two.
+    runs = _check_plan((2, 100, 8, 16, 128, oracle.FP8_E4M3), [list(range(10, 20))], None,
+                       64 << 10)
+    assert len(runs) == 5 and all(runs["nchunks"] == 2)
+    # bf16 (64 KiB chunks): one chunk per run whatever the table.
+    runs = _check_plan((2, 100, 8, 16, 128, oracle.BF16), [list(range(10, 20))], None,
+                       64 << 10)
+    assert len(runs) == 10

@@ -1,0 +1,278 @@
+"""GPU parity: the HIP gather/scatter path against the CPU oracle, byte for
+byte, through the C ABI.  Every input comes from the seeded generator; every
+expected value from the oracle run on a host copy of the same input."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_21255_amd import aqua
+from paper_2407_21255_amd import workload as wl
+from tests.checkers import assert_bytes_equal
+from tests.gpu_util import (device_pool, guarded_buffer, host, odesc, say)
+
+pytestmark = pytest.mark.gpu
+
+G = 4096  # guard bytes on each side of an image
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    aqua.load()  # fails loudly when the library is missing
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
+               buf_bytes=None, pinned=False, sentinel=True, stream=None):
+    """swap_out(out_tables) then swap_in(in_tables) on the GPU and in the
+    oracle; compares the image, guards and the whole pool."""
+    C = shape.chunk_bytes
+    d = odesc(shape)
+    pool = device_pool(shape, seed, owner)
+    if sentinel:
+        P = pool.view(shape.num_layers, shape.num_blocks, C)
+        ids = torch.tensor(sorted({b for t in in_tables for b in t}), dtype=torch.long,
+                           device="cuda")
+        if len(ids):
+            P[:, ids] = wl.SENTINEL_BYTE
+    pool_h = host(pool)
+    nb = sum(len(t) for t in out_tables)
+    size = buf_bytes if buf_bytes is not None else shape.image_bytes(nb)
+    buf = guarded_buffer(size, G, pinned)
+    inner = buf[G:G + size]
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        t1 = kv.swap_out(out_tables, inner, img_offsets, stream=stream)
+        kv.sync(t1)
+        img_h = host(buf)
+        want = np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, out_tables, want[G:G + size], img_offsets) == 0
+        assert_bytes_equal(img_h, want, f"{shape} image")
+        assert_bytes_equal(host(pool), pool_h, "swap-out changed the pool")
+        t2 = kv.swap_in(in_tables, inner, img_offsets, stream=stream)
+        assert t2 == t1 + 1
+        kv.sync(0)
+        assert oracle.swap_in(d, pool_h, in_tables, want[G:G + size], img_offsets) == 0
+        assert_bytes_equal(host(pool), pool_h, f"{shape} pool after swap-in")
+        assert_bytes_equal(host(buf), want, "swap-in changed the image or guards")
+        st = kv.stats()
+        assert st["calls_out"] == 1 and st["calls_in"] == 1 and st["hip_error"] == 0
+    finally:
+        kv.close()
+    return pool_h
+
+
+def test_tiny_config_round_trip():
+    """4 layers, 8 KV heads, head_dim 128, block 16, fp16; one 512-token
+    prompt on a random block subset, back into a random free subset."""
+    case = wl.tiny_case()
+    say("tiny round trip", case.shape)
+    pool_h = _roundtrip(case.shape, case.seed, case.out_tables, case.in_tables, case.owner)
+    s = case.shape
+    P = pool_h.reshape(s.num_layers, s.num_blocks, s.chunk_bytes)
+    # Round trip identity: the new blocks hold the old blocks' bytes.
+    fresh = np.empty(s.pool_bytes, dtype=np.uint8)
+    wl.fill_pool(torch.from_numpy(fresh), s, case.seed, case.owner)
+    F = fresh.reshape(P.shape)
+    assert np.array_equal(P[:, case.in_tables[0]], F[:, case.out_tables[0]])
+
+
+RAGGED = [
+    # (L, N, H, T, D, dtype): 48-byte chunks, 8 KiB chunks, 32 KiB fp8, 64 KiB.
+    wl.KVShape(3, 300, 1, 3, 8, wl.FP8_E4M3),
+    wl.KVShape(2, 64, 2, 16, 64, wl.BF16),
+    wl.KVShape(2, 96, 8, 16, 128, wl.FP8_E4M3),
+    wl.KVShape(3, 64, 8, 16, 128, wl.F16),
+]
+
+
+@pytest.mark.parametrize("shape", RAGGED, ids=lambda s: f"C{s.chunk_bytes}")
+def test_multi_sequence_ragged_and_coalesced(shape):
+    """Several sequences per call: fragmented tables, contiguous runs that
+    coalesce (and split at the unit size), an empty table, placed images
+    with gaps between them."""
+    N = shape.num_blocks
+    perm = wl.permutation(N, 41)
+    a = perm[:7]                                  # fragmented
+    b = list(range(5, 5 + min(40, N // 3)))       # contiguous
+    b = [x for x in b if x not in a]
+    c = []                                        # empty
+    e = [perm[-1]]                                # single block
+    out_tables = [a, b, c, e]
+    used = set(a) | set(b) | set(e)
+    free = [x for x in perm if x not in used]
+    in_tables, k = [], 0
+    for t in out_tables:
+        in_tables.append(free[k:k + len(t)])
+        k += len(t)
+    sizes = [shape.image_bytes(len(t)) for t in out_tables]
+    offs, pos = [], 0
+    for sz in sizes:
+        pos += 4096 + 48  # gap, keeps 16-byte alignment
+        pos = (pos + 15) // 16 * 16
+        offs.append(pos)
+        pos += sz
+    say("ragged", shape, [len(t) for t in out_tables])
+    _roundtrip(shape, 7, out_tables, in_tables, None, img_offsets=offs, buf_bytes=pos + 4096)
+
+
+@pytest.mark.parametrize("unit", [16, 1 << 20])
+def test_unit_size_extremes(unit, monkeypatch):
+    """One chunk per workgroup, and runs long enough for several unrolled
+    iterations plus a tail, give the same bytes."""
+    monkeypatch.setenv("AQUA_UNIT_BYTES", str(unit))
+    shape = wl.KVShape(2, 1024, 1, 3, 8, wl.FP8_E4M3)  # 48-byte chunks
+    out_tables = [list(range(100, 400)), list(range(49, -1, -1))]
+    in_tables = [list(range(400, 700)), list(range(700, 750))]
+    say("unit", unit)
+    _roundtrip(shape, 9, out_tables, in_tables, None)
+
+
+def test_pinned_host_target_round_trip():
+    """The offload image in pinned host memory, written and read zero-copy."""
+    case = wl.tiny_case(seed=11)
+    say("host target tiny")
+    _roundtrip(case.shape, case.seed, case.out_tables, case.in_tables, case.owner,
+               pinned=True)
+
+
+def test_errors_match_oracle_and_leave_no_trace():
+    shape = wl.KVShape(2, 32, 1, 2, 8, wl.BF16)
+    C = shape.chunk_bytes
+    d = odesc(shape)
+    pool = device_pool(shape, 3)
+    pool_h = host(pool)
+    buf = torch.zeros(shape.image_bytes(4), dtype=torch.uint8, device="cuda")
+    hbuf = np.zeros(buf.numel(), dtype=np.uint8)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        cases = [
+            ("out", [[0, -1]], None), ("in", [[0, 32]], None),
+            ("in", [[1, 2], [2]], None), ("out", [[1], [2]], [0, C]),
+            ("out", [[1, 2, 3, 4, 5]], None), ("in", [[1]], [buf.numel() - C]),
+            ("out", [[1]], [8]), ("in", [[32, 32]], [8]), ("in", [[32, 1, 1]], None),
+            ("in", [[1, 1, 2, 3, 4]], None),
+        ]
+        for kind, tables, io in cases:
+            fn = kv.swap_out if kind == "out" else kv.swap_in
+            ofn = oracle.swap_out if kind == "out" else oracle.swap_in
+            want = ofn(d, pool_h.copy(), tables, hbuf.copy(), io)
+            assert want != 0
+            with pytest.raises(aqua.AquaError) as ei:
+                fn(tables, buf, io)
+            assert ei.value.status == want, (kind, tables, io)
+        # Target / pointer-class mismatches.
+        for target, b in [(aqua.AQUA_TARGET_HOST, buf),
+                          (aqua.AQUA_TARGET_DEVICE, torch.zeros(buf.numel(), dtype=torch.uint8,
+                                                                pin_memory=True)),
+                          (aqua.AQUA_TARGET_HOST, torch.zeros(buf.numel(), dtype=torch.uint8)),
+                          (7, buf)]:
+            with pytest.raises(aqua.AquaError) as ei:
+                kv.swap_out([[1]], b, target=target)
+            assert ei.value.status == aqua.AQUA_ERR_INVALID
+        # A buffer size beyond its allocation is refused, not written.
+        st, _ = aqua.aqua_swap_out(kv.handle, 1, np.array([1], np.int32).ctypes.data,
+                                   np.array([0, 1], np.uint64).ctypes.data, buf.data_ptr(),
+                                   1 << 40, None, 0, None)
+        assert st == aqua.AQUA_ERR_INVALID
+        torch.cuda.synchronize()
+        assert_bytes_equal(host(pool), pool_h, "pool after failing calls")
+        assert not host(buf).any()
+        # No ticket was spent on the failures.
+        t = kv.swap_out([[1]], buf)
+        assert t == 1
+        kv.sync()
+        # Bad tickets.
+        assert aqua.aqua_sync(kv.handle, 99) == aqua.AQUA_ERR_INVALID
+        assert aqua.aqua_query(kv.handle, 0) == aqua.AQUA_ERR_INVALID
+    finally:
+        kv.close()
+    # Pool creation checks.
+    with pytest.raises(aqua.AquaError) as ei:
+        aqua.KVPool(shape.as_tuple(), pool[:shape.pool_bytes - 16])
+    assert ei.value.status == aqua.AQUA_ERR_CAPACITY
+    with pytest.raises(aqua.AquaError) as ei:
+        aqua.KVPool(shape.as_tuple(), pool[8:])
+    assert ei.value.status == aqua.AQUA_ERR_INVALID
+    with pytest.raises(aqua.AquaError) as ei:
+        aqua.KVPool(shape.as_tuple(), torch.zeros(shape.pool_bytes, dtype=torch.uint8))
+    assert ei.value.status == aqua.AQUA_ERR_INVALID
+
+
+def test_empty_calls_issue_tickets():
+    shape = wl.KVShape(2, 8, 1, 2, 8, wl.BF16)
+    pool = device_pool(shape, 4)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        t1 = kv.swap_out([], pool[:0])
+        t2 = kv.swap_in([[], []], pool[:0])
+        assert (t1, t2) == (1, 2)
+        kv.sync(t2)
+        assert kv.query(t1) and kv.query(t2)
+    finally:
+        kv.close()
+
+
+def test_cross_stream_reuse_is_ordered():
+    """A swap-in on stream B that reuses the blocks a swap-out on stream A
+    reads must wait for it.  Stream A is held back by real work queued
+    ahead of the swap-out, so without the library's wait B would overwrite
+    the blocks first.  The result must equal the sequential oracle."""
+    shape = wl.KVShape(8, 2048, 8, 16, 128, wl.BF16)
+    C = shape.chunk_bytes
+    d = odesc(shape)
+    pool = device_pool(shape, 12)
+    pool_h = host(pool)
+    X = wl.permutation(shape.num_blocks, 5)[:256]
+    other_img = torch.empty(shape.image_bytes(256), dtype=torch.uint8, device="cuda")
+    wl.fill_chunks(other_img.view(-1, C), torch.arange(8 * 256, dtype=torch.int64) * 7919 + 3,
+                   C, shape.dtype)
+    other_h = host(other_img)
+    img = torch.zeros(shape.image_bytes(256), dtype=torch.uint8, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        with torch.cuda.stream(sa):
+            for _ in range(200):         # milliseconds of work ahead of the swap-out
+                a = (a @ a).clamp_(-1, 1)
+        kv.swap_out([X], img, stream=sa)
+        kv.swap_in([X], other_img, stream=sb)
+        st = kv.stats()
+        kv.sync(0)
+        assert st["waits_inserted"] == 1
+        want_img = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [X], want_img) == 0
+        assert oracle.swap_in(d, pool_h, [X], other_h) == 0
+        assert_bytes_equal(host(img), want_img, "image of the delayed swap-out")
+        assert_bytes_equal(host(pool), pool_h, "pool after the reusing swap-in")
+    finally:
+        kv.close()
+
+
+def test_stream_wait_orders_caller_work():
+    shape = wl.KVShape(4, 256, 8, 16, 128, wl.F16)
+    pool = device_pool(shape, 13)
+    pool_h = host(pool)
+    img = torch.zeros(shape.image_bytes(64), dtype=torch.uint8, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        bt = list(range(0, 128, 2))
+        t = kv.swap_out([bt], img, stream=s1)
+        kv.stream_wait(t, s2)
+        with torch.cuda.stream(s2):
+            snap = img.clone()
+        s2.synchronize()
+        want = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(odesc(shape), pool_h, [bt], want) == 0
+        assert_bytes_equal(host(snap), want, "copy made after aqua_stream_wait")
+        assert kv.query(t)
+    finally:
+        kv.close()
