@@ -40,14 +40,15 @@ def _run(cmd):
     subprocess.check_call(cmd)
 
 
-def build_hip(out: str = HIP_LIB) -> str:
+def build_hip(out: str = HIP_LIB, extra=()) -> str:
+    """``extra``: additional compiler flags (measurement variants)."""
     srcs = []
     for s in HIP_SOURCES:
         p = os.path.join(CSRC, s)
         # hipcc compiles .cpp files as host code unless told they are HIP.
         srcs += (["-x", "hip", p] if s.endswith(".hip") else ["-x", "c++", p])
     tmp = out + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp])
+    _run([HIPCC, *HIP_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp])
     os.replace(tmp, out)
     return out
 

@@ -24,7 +24,30 @@ namespace {
 
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
+// Launch shape and cache hints.  The defaults are the shipped
+// configuration; the macros exist so that measurement sweeps can build
+// variants.
+#ifndef AQUA_THREADS
+#define AQUA_THREADS 256
+#endif
+#ifndef AQUA_UNROLL
+#define AQUA_UNROLL 16
+#endif
+#ifndef AQUA_NT_OUT_LD   // swap-out: pool loads
+#define AQUA_NT_OUT_LD 1
+#endif
+#ifndef AQUA_NT_OUT_ST   // swap-out: image stores
+#define AQUA_NT_OUT_ST 1
+#endif
+#ifndef AQUA_NT_IN_LD    // swap-in: image loads
+#define AQUA_NT_IN_LD 1
+#endif
+#ifndef AQUA_NT_IN_ST    // swap-in: pool stores
+#define AQUA_NT_IN_ST 0
+#endif
+
+constexpr int kThreads = AQUA_THREADS;
+constexpr int kUnroll = AQUA_UNROLL;
 
 template <bool NT>
 __device__ __forceinline__ v4u ld(const v4u* p) {
@@ -84,11 +107,11 @@ __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
         uint8_t* m = img + dsc.img_off + (uint64_t)l * dsc.img_lstride;
         const uint32_t nvec = (uint32_t)((uint64_t)dsc.nchunks * chunk_bytes / 16);
         if constexpr (OUT)
-            copy_span<UNROLL, true, true>(reinterpret_cast<const v4u*>(p),
-                                          reinterpret_cast<v4u*>(m), nvec);
+            copy_span<UNROLL, AQUA_NT_OUT_LD, AQUA_NT_OUT_ST>(
+                reinterpret_cast<const v4u*>(p), reinterpret_cast<v4u*>(m), nvec);
         else
-            copy_span<UNROLL, true, false>(reinterpret_cast<const v4u*>(m),
-                                           reinterpret_cast<v4u*>(p), nvec);
+            copy_span<UNROLL, AQUA_NT_IN_LD, AQUA_NT_IN_ST>(
+                reinterpret_cast<const v4u*>(m), reinterpret_cast<v4u*>(p), nvec);
     }
 }
 
@@ -104,11 +127,11 @@ hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
         uint32_t grid = units;
         if (a.max_workgroups && grid > a.max_workgroups) grid = a.max_workgroups;
         if (a.out)
-            hipLaunchKernelGGL((swap_runs_kernel<true, 16>), dim3(grid), dim3(kThreads), 0,
+            hipLaunchKernelGGL((swap_runs_kernel<true, kUnroll>), dim3(grid), dim3(kThreads), 0,
                                stream, a.pool, a.img, a.descs, a.ndesc, l0, units,
                                a.chunk_bytes, a.pool_lstride);
         else
-            hipLaunchKernelGGL((swap_runs_kernel<false, 16>), dim3(grid), dim3(kThreads), 0,
+            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll>), dim3(grid), dim3(kThreads), 0,
                                stream, a.pool, a.img, a.descs, a.ndesc, l0, units,
                                a.chunk_bytes, a.pool_lstride);
         const hipError_t e = hipGetLastError();

@@ -42,3 +42,8 @@ def run_slices(pool: aqua.KVPool, region: torch.Tensor, sched: Schedule,
         pool.sync(0)
         if between is not None:
             between(s)
+            # The caller's writes ran on its current stream: the next
+            # slice's swaps must not start before them.
+            cur = torch.cuda.current_stream()
+            out_stream.wait_stream(cur)
+            in_stream.wait_stream(cur)

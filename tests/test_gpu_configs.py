@@ -42,6 +42,7 @@ def _full_round_trip(case: wl.SwapCase, pinned: bool, gemm: bool = False):
     else:
         img = torch.empty(size, dtype=torch.uint8, device="cuda")
     img.fill_(wl.GUARD_BYTE)
+    torch.cuda.synchronize()  # fills ran on the current stream; swaps use another
     swap = torch.cuda.Stream()
     comp = torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
