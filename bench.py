@@ -32,7 +32,11 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # (FETCH_SIZE, WRITE_SIZE), each scaled by the same counters' reading for a
 # plain copy of known size.  Keyed by the hash of the kernel source they
 # were taken on: a changed kernel reports null until measured again.
-MEASURED_TRAFFIC = {}
+# Recorded with the profile summary of the same kernel under profiles/.
+MEASURED_TRAFFIC = {
+    ("llama8b_hbm", "35d08644ad681be3"): {
+        "gather (swap-out)": 4295902800, "scatter (swap-in)": 4295816800},
+}
 
 
 def _kernel_hash() -> str:
@@ -52,6 +56,9 @@ WORKLOADS = {
                      "pinned host memory and back",
     "tiny": "4 layers, 8 KV heads, head_dim 128, block 16, fp16, 256-block pool: one "
             "512-token prompt out to an HBM buffer and back",
+    "cycle": "time-sliced preemption on a Llama-3-8B-shaped fp8 e4m3 pool (16384 blocks): "
+             "64 prompts of 128..8192 tokens, each slice swaps the 16 longest-resident out "
+             "on one stream and the 16 longest-waiting in on another",
 }
 
 
@@ -106,28 +113,29 @@ def cpu_baseline(shape, target_seconds: float):
     }
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama8b_hbm", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the swap path runs on a single MI355X "
-              "(no sharding, no collectives); run it with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+def gemm_rate(stream, iters=20):
+    """ms per 4096^3 bf16 GEMM on ``stream`` (the compute-stream load)."""
+    import torch
+    a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            c = a @ b
+        e1.record(stream)
+    return a, b, e0, e1
 
+
+def run_pair(args, res_common):
+    """Steps of (swap-out of the preempted prompts, swap-in into fresh blocks)."""
     import numpy as np
     import torch
 
     from paper_2407_21255_amd import aqua
     from paper_2407_21255_amd import workload as wl
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    aqua.load()
     case, pinned = _case(args.workload)
     s = case.shape
     pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
@@ -138,12 +146,19 @@ def main():
     else:
         img = torch.empty(payload, dtype=torch.uint8, device="cuda")
     img.zero_()
+    if args.copy_reference and not pinned:
+        # A plain device-to-device copy of the payload size, for scaling the
+        # HBM traffic counters of the swap kernels.
+        img.copy_(pool[:payload])
     torch.cuda.synchronize()
 
     tab_a = aqua._csr(case.out_tables)
     tab_b = aqua._csr(case.in_tables)
     stream = torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
+    if args.max_workgroups:
+        kv.set_max_workgroups(aqua.AQUA_TARGET_HOST if pinned else aqua.AQUA_TARGET_DEVICE,
+                              args.max_workgroups)
     evs = []
 
     def step(i, timed):
@@ -159,11 +174,34 @@ def main():
             e2.record(stream)
             evs.append((e0, e1, e2))
 
+    gemm = None
+    if args.gemm:
+        comp = torch.cuda.Stream()
+        g = gemm_rate(comp)
+        torch.cuda.synchronize()
+        alone_ms = g[2].elapsed_time(g[3]) / 20
     for i in range(args.warmup):
+        if i == 1:
+            kv.sync(0)
+            tw = time.perf_counter()
         step(i, False)
     kv.sync(0)
     torch.cuda.synchronize()
+    step_s = (time.perf_counter() - tw) / (args.warmup - 1) if args.warmup > 1 else 0.0
     t0 = time.perf_counter()
+    if args.gemm:
+        # GEMMs on the compute stream for about the length of the timed window
+        # (estimated from the warm-up steps).
+        a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n_g = max(1, int(args.steps * step_s * 1e3 / alone_ms))
+        with torch.cuda.stream(comp):
+            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            g0.record(comp)
+            for _ in range(n_g):
+                c = a @ a
+            g1.record(comp)
     for i in range(args.steps):
         step(args.warmup + i, True)
     kv.sync(0)
@@ -171,10 +209,13 @@ def main():
     wall = time.perf_counter() - t0
     st = kv.stats()
     kv.close()
+    if args.gemm:
+        during_ms = g0.elapsed_time(g1) / n_g
+        gemm = {"gemm_ms_alone": round(alone_ms, 4), "gemm_ms_during_swaps": round(during_ms, 4),
+                "gemm_iters": n_g, "slowdown": round(during_ms / alone_ms - 1, 4)}
 
     out_ms = np.array([a.elapsed_time(b) for a, b, _ in evs])
     in_ms = np.array([b.elapsed_time(c) for _, b, c in evs])
-    ms_per_step = wall * 1e3 / args.steps
     value = 2 * payload * args.steps / wall / 1e9
     dom, dom_ms = ("gather (swap-out)", out_ms) if out_ms.mean() >= in_ms.mean() else \
         ("scatter (swap-in)", in_ms)
@@ -184,20 +225,11 @@ def main():
         bound, peak, alg = "hbm", HBM_PEAK_GBS, 2 * payload
     achieved = alg / (dom_ms.mean() * 1e-3) / 1e9
     khash = _kernel_hash()
-    traffic = MEASURED_TRAFFIC.get((args.workload, khash))
-    res = {
-        "metric": "KV page swap GB/s (out+in) and % of HBM / host-link peak, 1 MI355X",
+    res = dict(res_common)
+    res.update({
         "value": round(value, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
         "dtype": wl.DTYPE_NAME[s.dtype],
-        "data": "synthetic",
         "config": {
             "workload": WORKLOADS[args.workload],
             "layers": s.num_layers, "kv_heads": s.num_kv_heads, "head_dim": s.head_dim,
@@ -211,7 +243,7 @@ def main():
             "bound": bound, "kernel": dom,
             "achieved": round(achieved, 1), "peak": peak,
             "unit": "GB/s", "frac": round(achieved / peak, 4),
-            "traffic": traffic,
+            "traffic": MEASURED_TRAFFIC.get((args.workload, khash), {}).get(dom),
             "algorithmic_bytes_per_launch": alg,
         },
         "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
@@ -223,9 +255,134 @@ def main():
         "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
                                   2),
         "kernel_source": khash,
+    })
+    if gemm:
+        res["compute_stream"] = gemm
+    return res, s
+
+
+def run_cycle(args, res_common):
+    """Slices of the preemption schedule: out on one stream, in on another."""
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import aqua
+    from paper_2407_21255_amd import workload as wl
+    from paper_2407_21255_amd.cycle import slice_tables
+
+    n = args.warmup + args.steps
+    sched = wl.preemption_schedule(n_slices=n)
+    s = sched.shape
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, sched.seed, wl.schedule_owner(sched))
+    region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_region(region, sched)
+    torch.cuda.synchronize()
+    prepared = [slice_tables(sched, k) for k in range(n)]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    evs, moved = [], 0
+    C = s.chunk_bytes
+
+    def one(k, timed):
+        out, out_off, inn, in_off = prepared[k]
+        if timed:
+            a0, a1, b0, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
+            a0.record(sa)
+            b0.record(sb)
+        kv.swap_out(out, region, out_off, stream=sa)
+        if timed:
+            a1.record(sa)
+        kv.swap_in(inn, region, in_off, stream=sb)
+        if timed:
+            b1.record(sb)
+            evs.append((a0, a1, b0, b1, len(out[0]), len(inn[0])))
+        kv.sync(0)
+
+    for k in range(args.warmup):
+        one(k, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.warmup, n):
+        one(k, True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = kv.stats()
+    kv.close()
+    out_b = np.array([e[4] for e in evs]) * s.num_layers * C
+    in_b = np.array([e[5] for e in evs]) * s.num_layers * C
+    out_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    in_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    moved = float(out_b.sum() + in_b.sum())
+    achieved = float((2 * out_b / (out_ms * 1e-3)).mean()) / 1e9
+    res = dict(res_common)
+    res.update({
+        "value": round(moved / wall / 1e9, 2),
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "dtype": wl.DTYPE_NAME[s.dtype],
+        "config": {
+            "workload": WORKLOADS["cycle"], "layers": s.num_layers,
+            "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
+            "pool_blocks": s.num_blocks, "chunk_bytes": C, "prompts": len(sched.nblocks),
+            "swaps_per_slice": 16, "slices_timed": args.steps,
+            "mean_payload_bytes_per_direction": round(float(out_b.mean())),
+            "offload_target": "hbm", "parallelism": "single_gpu",
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "gather (swap-out), concurrent with the scatter",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": round(float(2 * out_b.mean())),
+        },
+        "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
+                      "swap_in_mean": round(float(in_ms.mean()), 4)},
+        "slice_hbm_GBps": round(2 * moved / wall / 1e9, 1),
+        "waits_inserted": st["waits_inserted"],
+        "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
+                                  2),
+        "kernel_source": _kernel_hash(),
+    })
+    return res, s
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_hbm", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gemm", action="store_true",
+                    help="run 4096^3 bf16 GEMMs on a compute stream during the swaps")
+    ap.add_argument("--max-workgroups", type=int, default=0,
+                    help="cap the swap kernels' grid (0: library default)")
+    ap.add_argument("--copy-reference", action="store_true",
+                    help="one plain device copy of the payload size before timing")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the swap path runs on a single MI355X "
+              "(no sharding, no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2407_21255_amd import aqua
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    aqua.load()
+    common = {
+        "metric": "KV page swap GB/s (out+in) and % of HBM / host-link peak, 1 MI355X",
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "data": "synthetic",
     }
+    if args.workload == "cycle":
+        res, shape = run_cycle(args, common)
+    else:
+        res, shape = run_pair(args, common)
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 

@@ -21,6 +21,15 @@ using aqua::RunDesc;
 constexpr uint64_t kDefaultRingBytes = 1ull << 20;  // 32768 descriptors
 constexpr uint64_t kDefaultUnitBytes = 64ull << 10;
 
+// How run descriptors reach the kernels.  2 (shipped): the kernels read
+// them straight from the pinned, coherent host ring -- one 32-byte scalar
+// load per workgroup, and no copy on the call's stream.  0 and 1 exist for
+// measurement: 0 copies them to a device ring on the call's stream, 1 on
+// the library's upload stream, which the call's stream then waits for.
+#ifndef AQUA_DESC_MODE
+#define AQUA_DESC_MODE 2
+#endif
+
 uint64_t env_u64(const char* name, uint64_t dflt) {
     const char* v = std::getenv(name);
     if (!v || !*v) return dflt;
@@ -32,6 +41,7 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
 struct Outstanding {
     uint64_t ticket;
     hipEvent_t ev;
+    hipEvent_t up_ev;  // descriptor upload, or nullptr
 };
 
 struct RingUse {
@@ -57,6 +67,8 @@ struct aqua_kv_pool {
     std::vector<hipEvent_t> spare_events;
 
     // Descriptor staging: pinned host ring copied to a device ring.
+    hipStream_t upload = nullptr;
+    uint8_t* ring_host_dev = nullptr;  // device address of ring_host
     uint8_t* ring_host = nullptr;
     uint8_t* ring_dev = nullptr;
     uint64_t ring_bytes = 0;
@@ -119,6 +131,7 @@ void retire(aqua_kv_pool* p, uint32_t m, uint64_t ticket) {
     auto& q = p->outstanding[m];
     while (!q.empty() && q.front().ticket <= ticket) {
         p->spare_events.push_back(q.front().ev);
+        if (q.front().up_ev) p->spare_events.push_back(q.front().up_ev);
         q.pop_front();
     }
     p->tracker.complete(m, ticket);
@@ -180,8 +193,15 @@ void free_rings(aqua_kv_pool* p) {
 }
 
 aqua_status alloc_rings(aqua_kv_pool* p, uint64_t bytes) {
-    hipError_t e = hipMalloc((void**)&p->ring_dev, bytes);
-    if (e == hipSuccess) e = hipHostMalloc((void**)&p->ring_host, bytes, hipHostMallocDefault);
+    hipError_t e = hipSuccess;
+#if AQUA_DESC_MODE != 2
+    e = hipMalloc((void**)&p->ring_dev, bytes);
+#endif
+    if (e == hipSuccess)
+        e = hipHostMalloc((void**)&p->ring_host, bytes,
+                          hipHostMallocMapped | hipHostMallocCoherent);
+    if (e == hipSuccess)
+        e = hipHostGetDevicePointer((void**)&p->ring_host_dev, p->ring_host, 0);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         free_rings(p);
@@ -331,16 +351,29 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         p->stats.waits_inserted++;
     }
 
+    hipEvent_t up_ev = nullptr;
     if (dbytes) {
         std::memcpy(p->ring_host + ring_off, p->plan.data(), dbytes);
-        hipError_t e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
-                                      hipMemcpyHostToDevice, stream);
+        hipError_t e = hipSuccess;
+        const uint8_t* descs = p->ring_host_dev + ring_off;
+#if AQUA_DESC_MODE == 0
+        descs = p->ring_dev + ring_off;
+        e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
+                           hipMemcpyHostToDevice, stream);
+#elif AQUA_DESC_MODE == 1
+        descs = p->ring_dev + ring_off;
+        e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
+                           hipMemcpyHostToDevice, p->upload);
+        if (e == hipSuccess) e = take_event(p, &up_ev);
+        if (e == hipSuccess) e = hipEventRecord(up_ev, p->upload);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, up_ev, 0);
+#endif
         if (e != hipSuccess) return latch(p, e);
         aqua::SwapLaunch L;
         L.out = !is_in;
         L.pool = p->base;
         L.img = dbuf;
-        L.descs = reinterpret_cast<const RunDesc*>(p->ring_dev + ring_off);
+        L.descs = reinterpret_cast<const RunDesc*>(descs);
         L.ndesc = (uint32_t)p->plan.size();
         L.num_layers = p->shape.L;
         L.chunk_bytes = p->shape.C;
@@ -355,7 +388,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     hipError_t e = take_event(p, &ev);
     if (e == hipSuccess) e = hipEventRecord(ev, stream);
     if (e != hipSuccess) return latch(p, e);
-    p->outstanding[lane].push_back({ticket, ev});
+    p->outstanding[lane].push_back({ticket, ev, up_ev});
     if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
 
     const uint64_t moved = (uint64_t)p->shape.L * total * p->shape.C;
@@ -421,6 +454,13 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     if (!p->unit_bytes) p->unit_bytes = kDefaultUnitBytes;
     if (p->unit_bytes > aqua::kMaxChunkBytes) p->unit_bytes = aqua::kMaxChunkBytes;
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
+#if AQUA_DESC_MODE == 1
+    if (st == AQUA_OK && hipStreamCreateWithFlags(&p->upload, hipStreamNonBlocking) != hipSuccess) {
+        (void)hipGetLastError();
+        free_rings(p);
+        st = AQUA_ERR_HIP;
+    }
+#endif
     if (st != AQUA_OK) {
         delete p;
         return st;
@@ -436,9 +476,13 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
         DeviceGuard dg(p->device);
         if (p->sticky == hipSuccess) st = wait_all(p);
         for (auto& q : p->outstanding)
-            for (const Outstanding& o : q) (void)hipEventDestroy(o.ev);
+            for (const Outstanding& o : q) {
+                (void)hipEventDestroy(o.ev);
+                if (o.up_ev) (void)hipEventDestroy(o.up_ev);
+            }
         for (hipEvent_t ev : p->spare_events) (void)hipEventDestroy(ev);
         free_rings(p);
+        if (p->upload) (void)hipStreamDestroy(p->upload);
         if (p->sticky != hipSuccess) st = AQUA_ERR_HIP;
     }
     delete p;

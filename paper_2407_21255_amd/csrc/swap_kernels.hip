@@ -2,12 +2,12 @@
 //
 // The work is pure data movement (Aqua, section 7, "Efficient context
 // switching"): no arithmetic on the values, so no MFMA and no LDS.  Each
-// workgroup of 256 lanes (4 wave64s) copies one run of chunks of one layer;
-// every lane moves 16-byte vectors, a wave covers 1 KiB contiguous per
-// instruction, and UNROLL independent loads are issued before the first
-// store so that each workgroup keeps UNROLL * 4 KiB in flight.  The run
-// descriptor is uniform across the workgroup and is fetched with scalar
-// loads.  The offload side is written (swap-out) or read (swap-in) with
+// workgroup of 1024 lanes (16 wave64s) copies one run of chunks of one
+// layer; every lane moves 16-byte vectors, a wave covers 1 KiB contiguous
+// per instruction, and UNROLL = 4 independent loads are issued before the
+// first store, so a workgroup has 64 KiB -- one bf16 chunk -- in flight.
+// The run descriptor is uniform across the workgroup and is fetched with
+// scalar loads.  The offload side is written (swap-out) or read (swap-in) with
 // nontemporal hints: it is touched once and should not displace the pool's
 // working set in L2 and MALL.
 #include <hip/hip_runtime.h>
@@ -28,10 +28,10 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 // configuration; the macros exist so that measurement sweeps can build
 // variants.
 #ifndef AQUA_THREADS
-#define AQUA_THREADS 256
+#define AQUA_THREADS 1024
 #endif
 #ifndef AQUA_UNROLL
-#define AQUA_UNROLL 16
+#define AQUA_UNROLL 4
 #endif
 #ifndef AQUA_NT_OUT_LD   // swap-out: pool loads
 #define AQUA_NT_OUT_LD 1

@@ -434,3 +434,22 @@ def mutation_writes(sched: Schedule, s: int):
              for p in sl.in_prompts]
     return (np.asarray(offs, dtype=np.int64),
             np.stack(words) if words else np.zeros((0, 16), np.uint8), slots)
+
+
+def fill_region(region: torch.Tensor, sched: Schedule) -> None:
+    """Offload region of a preemption schedule: guard bytes everywhere, and
+    the generated initial images of the prompts that start swapped out."""
+    region.fill_(GUARD_BYTE)
+    sh = sched.shape
+    C = sh.chunk_bytes
+    for p in range(len(sched.nblocks)):
+        if p in sched.initial_resident:
+            continue
+        o, n = sched.slot_offsets[p], sched.nblocks[p]
+        fill_chunks(region[o:o + sh.image_bytes(n)].view(-1, C),
+                    image_keys(sh, sched.seed, p, n), C, sh.dtype)
+
+
+def schedule_owner(sched: Schedule) -> dict:
+    """Physical block -> (prompt, logical block) of the initial residents."""
+    return {b: (p, i) for p, t in sched.initial_tables.items() for i, b in enumerate(t)}

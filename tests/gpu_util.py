@@ -44,23 +44,13 @@ def guarded_buffer(nbytes: int, guard: int = 4096, pinned: bool = False) -> torc
 
 
 def region_for(sched: wl.Schedule, device="cuda") -> torch.Tensor:
-    """Offload region of a preemption schedule: guard bytes everywhere, and
-    the initial images of the prompts that start swapped out."""
     reg = torch.empty(sched.region_bytes, dtype=torch.uint8, device=device)
-    reg.fill_(wl.GUARD_BYTE)
-    sh = sched.shape
-    C = sh.chunk_bytes
-    for p in range(len(sched.nblocks)):
-        if p in sched.initial_resident:
-            continue
-        o, n = sched.slot_offsets[p], sched.nblocks[p]
-        wl.fill_chunks(reg[o:o + sh.image_bytes(n)].view(-1, C),
-                       wl.image_keys(sh, sched.seed, p, n), C, sh.dtype)
+    wl.fill_region(reg, sched)
     return reg
 
 
 def schedule_owner(sched: wl.Schedule) -> dict:
-    return {b: (p, i) for p, t in sched.initial_tables.items() for i, b in enumerate(t)}
+    return wl.schedule_owner(sched)
 
 
 def apply_mutations_host(sched, s, pool_np, region_np):
