@@ -113,19 +113,34 @@ def cpu_baseline(shape, target_seconds: float):
     }
 
 
-def gemm_rate(stream, iters=20):
-    """ms per 4096^3 bf16 GEMM on ``stream`` (the compute-stream load)."""
+def gemm_run(stream, a, iters, per_kernel=True):
+    """Enqueues ``iters`` 4096^3 bf16 GEMMs on ``stream``; returns the event
+    pairs bracketing each GEMM (or the whole run)."""
     import torch
-    a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
-    b = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
-    torch.cuda.synchronize()
+    evs = []
     with torch.cuda.stream(stream):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        if not per_kernel:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
         for _ in range(iters):
-            c = a @ b
-        e1.record(stream)
-    return a, b, e0, e1
+            if per_kernel:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            c = a @ a
+            if per_kernel:
+                e1 = torch.cuda.Event(enable_timing=True)
+                e1.record(stream)
+                evs.append((e0, e1))
+        if not per_kernel:
+            e1 = torch.cuda.Event(enable_timing=True)
+            e1.record(stream)
+            evs.append((e0, e1))
+    del c
+    return evs
+
+
+def gemm_ms(evs):
+    return sum(x.elapsed_time(y) for x, y in evs) / len(evs)
 
 
 def run_pair(args, res_common):
@@ -159,6 +174,9 @@ def run_pair(args, res_common):
     if args.max_workgroups:
         kv.set_max_workgroups(aqua.AQUA_TARGET_HOST if pinned else aqua.AQUA_TARGET_DEVICE,
                               args.max_workgroups)
+    if pinned:
+        kv.set_host_path(aqua.AQUA_HOST_STAGED if args.host_path == "staged"
+                         else aqua.AQUA_HOST_ZERO_COPY)
     evs = []
 
     def step(i, timed):
@@ -175,11 +193,6 @@ def run_pair(args, res_common):
             evs.append((e0, e1, e2))
 
     gemm = None
-    if args.gemm:
-        comp = torch.cuda.Stream()
-        g = gemm_rate(comp)
-        torch.cuda.synchronize()
-        alone_ms = g[2].elapsed_time(g[3]) / 20
     for i in range(args.warmup):
         if i == 1:
             kv.sync(0)
@@ -190,19 +203,27 @@ def run_pair(args, res_common):
     step_s = (time.perf_counter() - tw) / (args.warmup - 1) if args.warmup > 1 else 0.0
     t0 = time.perf_counter()
     if args.gemm:
-        # GEMMs on the compute stream for about the length of the timed window
-        # (estimated from the warm-up steps).
+        # GEMMs on a compute stream for about the length of the timed window
+        # (estimated from the warm-up steps), enqueued step by step beside the
+        # swaps so that both streams start together.  The same number of
+        # GEMMs is first timed alone, after a warm-up, so that both figures
+        # cover the same span of sustained work.
+        comp = torch.cuda.Stream()
         a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+        gemm_run(comp, a, 20)
         torch.cuda.synchronize()
+        est = gemm_run(comp, a, 20, per_kernel=False)
+        torch.cuda.synchronize()
+        per_step = max(1, int(step_s * 1e3 / (gemm_ms(est) / 20)))
+        n_g = per_step * args.steps
+        alone = gemm_run(comp, a, n_g)
+        torch.cuda.synchronize()
+        alone_ms = gemm_ms(alone)
         t0 = time.perf_counter()
-        n_g = max(1, int(args.steps * step_s * 1e3 / alone_ms))
-        with torch.cuda.stream(comp):
-            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            g0.record(comp)
-            for _ in range(n_g):
-                c = a @ a
-            g1.record(comp)
+        during = []
     for i in range(args.steps):
+        if args.gemm:
+            during += gemm_run(comp, a, per_step)
         step(args.warmup + i, True)
     kv.sync(0)
     torch.cuda.synchronize()
@@ -210,7 +231,9 @@ def run_pair(args, res_common):
     st = kv.stats()
     kv.close()
     if args.gemm:
-        during_ms = g0.elapsed_time(g1) / n_g
+        # Kernel time of each GEMM alone and while the swaps run (gaps in the
+        # compute stream are not counted).
+        during_ms = gemm_ms(during)
         gemm = {"gemm_ms_alone": round(alone_ms, 4), "gemm_ms_during_swaps": round(during_ms, 4),
                 "gemm_iters": n_g, "slowdown": round(during_ms / alone_ms - 1, 4)}
 
@@ -237,6 +260,7 @@ def run_pair(args, res_common):
             "chunk_bytes": s.chunk_bytes, "swapped_blocks": case.nblocks,
             "payload_bytes_per_direction": payload,
             "offload_target": "pinned_host" if pinned else "hbm",
+            "host_path": args.host_path if pinned else None,
             "parallelism": "single_gpu",
         },
         "roofline": {
@@ -254,11 +278,44 @@ def run_pair(args, res_common):
         "swap_in_GBps": round(payload / (in_ms.mean() * 1e-3) / 1e9, 2),
         "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
                                   2),
+        "host_wait_us_per_call": round(st["wait_ns"] / max(1, st["calls_out"] + st["calls_in"]) /
+                                       1e3, 2),
         "kernel_source": khash,
     })
     if gemm:
         res["compute_stream"] = gemm
+    if pinned:
+        res["link_ceiling"] = link_ceiling()
+        res["host_link_frac"] = {
+            "swap_out": round(res["swap_out_GBps"] / HOST_LINK_PEAK_GBS, 4),
+            "swap_in": round(res["swap_in_GBps"] / HOST_LINK_PEAK_GBS, 4),
+            "swap_out_vs_copy_engine": round(res["swap_out_GBps"] / res["link_ceiling"]["d2h"], 4),
+            "swap_in_vs_copy_engine": round(res["swap_in_GBps"] / res["link_ceiling"]["h2d"], 4),
+        }
     return res, s
+
+
+def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
+    """GB/s of the copy engines over the host link: plain 1 GiB copies between
+    pinned host memory and the device (hipMemcpyAsync), each direction."""
+    import torch
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    h.fill_(1)
+    d.fill_(2)
+    torch.cuda.synchronize()
+    out = {}
+    for name, dst, src in (("h2d", d, h), ("d2h", h, d)):
+        dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            dst.copy_(src, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = round(nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 2)
+    return out
 
 
 def run_cycle(args, res_common):
@@ -357,6 +414,9 @@ def main():
                     help="run 4096^3 bf16 GEMMs on a compute stream during the swaps")
     ap.add_argument("--max-workgroups", type=int, default=0,
                     help="cap the swap kernels' grid (0: library default)")
+    ap.add_argument("--host-path", default="staged", choices=["zero_copy", "staged"],
+                    help="pinned-host workloads: kernels over the link, or HBM staging "
+                         "plus the copy engines")
     ap.add_argument("--copy-reference", action="store_true",
                     help="one plain device copy of the payload size before timing")
     args = ap.parse_args()

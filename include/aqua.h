@@ -107,7 +107,11 @@ typedef struct {
     uint64_t descriptors;                 /* run descriptors launched */
     uint64_t waits_inserted;              /* cross-stream waits enqueued */
     uint64_t waits_elided;                /* conflicts already complete */
-    uint64_t host_ns;                     /* host time in swap calls */
+    uint64_t host_ns;                     /* host time in swap calls, not
+                                             counting wait_ns */
+    uint64_t wait_ns;                     /* host time blocked inside swap
+                                             calls until descriptor space
+                                             used by earlier calls is free */
     int32_t hip_error;                    /* latched hipError_t, 0 if none */
     int32_t reserved;
 } aqua_pool_stats;
@@ -167,12 +171,29 @@ AQUA_API aqua_status aqua_stream_wait(aqua_kv_pool_t pool, uint64_t ticket,
 /* 1 if `ticket` has completed, 0 if not, negative status on error. */
 AQUA_API aqua_status aqua_query(aqua_kv_pool_t pool, uint64_t ticket);
 
-/* Cap the number of workgroups of later launches for one target (0: the
- * library's default).  Used to leave compute units to concurrent work while
- * a host-link-bound swap runs. */
+/* Cap the number of workgroups of later kernel launches for one target
+ * (0: no cap, one workgroup per (layer, run)).  For the host target the cap
+ * applies to zero-copy swaps; staged swaps gather in HBM without a cap. */
 AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
                                             int32_t target,
                                             uint32_t max_workgroups);
+
+/* How swaps with a pinned-host target move their bytes.
+ *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
+ *     (section 7, "Efficient context switching").  Layers pass through two
+ *     HBM slots owned by the library (256 MiB each by default, allocated on
+ *     the first staged call, after waiting for every outstanding call):
+ *     the gather kernel fills a slot and the copy engines move it over the
+ *     link while the next slot is filled, and the reverse on swap-in.  The
+ *     compute units are busy only for the short gathers, so concurrent
+ *     kernels keep running.
+ *   AQUA_HOST_ZERO_COPY: the gather and scatter kernels read and write the
+ *     host image directly over the link, with no HBM staging.  Their
+ *     workgroups stay resident for the whole transfer, so the library caps
+ *     the grid (16 workgroups unless aqua_kv_pool_set_max_workgroups says
+ *     otherwise), which is enough to saturate the link. */
+enum { AQUA_HOST_ZERO_COPY = 0, AQUA_HOST_STAGED = 1 };
+AQUA_API aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t pool, int32_t path);
 
 /* Copy the pool's counters into *out. */
 AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* out);

@@ -31,11 +31,13 @@ AQUA_ERR_STATE = -6
 
 AQUA_F16, AQUA_BF16, AQUA_FP8_E4M3 = 1, 2, 3
 AQUA_TARGET_DEVICE, AQUA_TARGET_HOST = 0, 1
+AQUA_HOST_ZERO_COPY, AQUA_HOST_STAGED = 0, 1
 
 EXPORTS = (
     "aqua_kv_pool_create", "aqua_kv_pool_destroy", "aqua_swap_out",
     "aqua_swap_in", "aqua_sync", "aqua_stream_wait", "aqua_query",
-    "aqua_kv_pool_set_max_workgroups", "aqua_pool_stats_get", "aqua_status_str",
+    "aqua_kv_pool_set_max_workgroups", "aqua_kv_pool_set_host_path",
+    "aqua_pool_stats_get", "aqua_status_str",
 )
 
 
@@ -53,7 +55,7 @@ class aqua_kv_desc(ctypes.Structure):
 class aqua_pool_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "calls_out", "calls_in", "bytes_out", "bytes_in", "bytes_host",
-        "descriptors", "waits_inserted", "waits_elided", "host_ns")] + [
+        "descriptors", "waits_inserted", "waits_elided", "host_ns", "wait_ns")] + [
         ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
@@ -86,6 +88,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_stream_wait.argtypes = [P, u64, P]
     L.aqua_query.argtypes = [P, u64]
     L.aqua_kv_pool_set_max_workgroups.argtypes = [P, i32, u32]
+    L.aqua_kv_pool_set_host_path.argtypes = [P, i32]
     L.aqua_pool_stats_get.argtypes = [P, ctypes.POINTER(aqua_pool_stats)]
     L.aqua_status_str.argtypes = [i32]
     L.aqua_status_str.restype = ctypes.c_char_p
@@ -139,6 +142,10 @@ def aqua_query(pool, ticket: int) -> int:
 
 def aqua_kv_pool_set_max_workgroups(pool, target: int, n: int) -> int:
     return load().aqua_kv_pool_set_max_workgroups(pool, target, n)
+
+
+def aqua_kv_pool_set_host_path(pool, path: int) -> int:
+    return load().aqua_kv_pool_set_host_path(pool, path)
 
 
 def aqua_pool_stats_get(pool):
@@ -242,6 +249,11 @@ class KVPool:
         st = aqua_kv_pool_set_max_workgroups(self.handle, target, n)
         if st != AQUA_OK:
             raise AquaError(st, "aqua_kv_pool_set_max_workgroups")
+
+    def set_host_path(self, path: int) -> None:
+        st = aqua_kv_pool_set_host_path(self.handle, path)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_kv_pool_set_host_path")
 
     def stats(self) -> dict:
         st, s = aqua_pool_stats_get(self.handle)

@@ -1,7 +1,9 @@
-// aqua_capi.hip -- the C ABI: pools, tickets, descriptor staging, cross-stream
-// ordering and the launches of the gather/scatter kernels.
+// aqua_capi.hip -- the C ABI: pools, tickets, descriptor delivery,
+// cross-stream ordering, the staged host path and the launches of the
+// gather/scatter kernels.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <chrono>
 #include <cstdlib>
 #include <cstring>
@@ -18,8 +20,10 @@ namespace {
 using aqua::HazardTracker;
 using aqua::RunDesc;
 
-constexpr uint64_t kDefaultRingBytes = 1ull << 20;  // 32768 descriptors
+constexpr uint64_t kDefaultRingBytes = 4ull << 20;  // 131072 descriptors
 constexpr uint64_t kDefaultUnitBytes = 64ull << 10;
+constexpr uint64_t kDefaultSlotBytes = 256ull << 20;  // staged path, per slot
+constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 
 // How run descriptors reach the kernels.  2 (shipped): the kernels read
 // them straight from the pinned, coherent host ring -- one 32-byte scalar
@@ -40,12 +44,18 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
 
 struct Outstanding {
     uint64_t ticket;
-    hipEvent_t ev;
-    hipEvent_t up_ev;  // descriptor upload, or nullptr
+    hipEvent_t ev;                 // recorded on the call's stream, last
+    std::vector<hipEvent_t> aux;   // events inside the call (staging, uploads)
 };
 
 struct RingUse {
     uint64_t lo, hi, ticket;
+};
+
+// One sequence of a staged call: image offset in the caller's buffer, its
+// first entry in the concatenated table, and its table length.
+struct StagedSeq {
+    uint64_t off, first, n;
 };
 
 }  // namespace
@@ -66,7 +76,8 @@ struct aqua_kv_pool {
     std::vector<std::deque<Outstanding>> outstanding;   // per lane, in order
     std::vector<hipEvent_t> spare_events;
 
-    // Descriptor staging: pinned host ring copied to a device ring.
+    // Run descriptors: a pinned host ring (read by the kernels directly, or
+    // copied to a device ring in the measurement modes).
     hipStream_t upload = nullptr;
     uint8_t* ring_host_dev = nullptr;  // device address of ring_host
     uint8_t* ring_host = nullptr;
@@ -75,9 +86,20 @@ struct aqua_kv_pool {
     uint64_t ring_head = 0;
     std::deque<RingUse> ring_uses;
 
+    // Staged host path: two HBM slots and a copy stream for the copy engines.
+    int32_t host_path = AQUA_HOST_STAGED;
+    hipStream_t copy = nullptr;
+    uint8_t* staging = nullptr;
+    uint64_t staging_bytes = 0;
+    uint64_t slot_target = kDefaultSlotBytes;
+    std::vector<StagedSeq> sseq;
+    std::vector<uint64_t> slot_offsets;  // per sequence, in a slot
+
     uint64_t next_ticket = 1;
     uint64_t unit_bytes = kDefaultUnitBytes;
-    uint32_t max_wg[2] = {0, 0};
+    // Grid caps per target (0: one workgroup per unit).  Zero-copy host
+    // swaps are link-bound: 16 workgroups of 1024 lanes saturate the link.
+    uint32_t max_wg[2] = {0, kHostZeroCopyWorkgroups};
     aqua_pool_stats stats{};
     hipError_t sticky = hipSuccess;
 };
@@ -131,7 +153,7 @@ void retire(aqua_kv_pool* p, uint32_t m, uint64_t ticket) {
     auto& q = p->outstanding[m];
     while (!q.empty() && q.front().ticket <= ticket) {
         p->spare_events.push_back(q.front().ev);
-        if (q.front().up_ev) p->spare_events.push_back(q.front().up_ev);
+        for (hipEvent_t e : q.front().aux) p->spare_events.push_back(e);
         q.pop_front();
     }
     p->tracker.complete(m, ticket);
@@ -245,6 +267,29 @@ aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off) {
     return AQUA_OK;
 }
 
+// Makes the staging buffer hold at least `bytes`, waiting for every
+// outstanding call before it is replaced.
+aqua_status ensure_staging(aqua_kv_pool* p, uint64_t bytes) {
+    if (bytes <= p->staging_bytes) return AQUA_OK;
+    aqua_status st = wait_all(p);
+    if (st != AQUA_OK) return st;
+    if (p->staging) (void)hipFree(p->staging);
+    p->staging = nullptr;
+    p->staging_bytes = 0;
+    if (!p->copy && hipStreamCreateWithFlags(&p->copy, hipStreamNonBlocking) != hipSuccess) {
+        (void)hipGetLastError();
+        p->copy = nullptr;
+        return AQUA_ERR_HIP;
+    }
+    if (hipMalloc((void**)&p->staging, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        p->staging = nullptr;
+        return AQUA_ERR_HIP;
+    }
+    p->staging_bytes = bytes;
+    return AQUA_OK;
+}
+
 // Device-accessible address of the buffer, after checking that its memory
 // class matches the target and that [ptr, ptr + bytes) lies in one
 // allocation.
@@ -276,6 +321,99 @@ aqua_status resolve_buffer(aqua_kv_pool* p, const void* ptr, uint64_t bytes,
         (void)hipGetLastError();
         if (target == AQUA_TARGET_DEVICE) return AQUA_ERR_INVALID;
     }
+    return AQUA_OK;
+}
+
+aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const RunDesc* descs,
+                             uint32_t ndesc, int32_t target) {
+    aqua::SwapLaunch L;
+    L.out = !is_in;
+    L.pool = p->base;
+    L.img = img;
+    L.img_l0 = 0;
+    L.descs = descs;
+    L.ndesc = ndesc;
+    L.first_layer = 0;
+    L.num_layers = p->shape.L;
+    L.chunk_bytes = p->shape.C;
+    L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
+    L.max_workgroups = p->max_wg[target];
+    return L;
+}
+
+// Staged host path.  Layers go through two HBM slots of G layers each.  A
+// slot holds, sequence after sequence, the sequence's G layers in image
+// order ([G][n_s][C] at G * first_s * C), so each sequence's piece of a
+// layer group is contiguous both in the slot and in the host image: one
+// copy per sequence per group.  Swap-out: the gather fills a slot on the
+// call's stream, then the copy stream moves the pieces to the host image.
+// Swap-in: the copy stream fills a slot from the host image, then the
+// scatter drains it on the call's stream.  A slot is refilled only after
+// its previous user has finished with it.
+aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStream_t stream,
+                           const RunDesc* descs, uint32_t ndesc, uint64_t slot, uint32_t G,
+                           Outstanding* rec) {
+    const uint64_t C = p->shape.C;
+    const uint32_t L = p->shape.L;
+    hipError_t e = hipSuccess;
+    auto ev = [&](hipEvent_t* x) -> hipError_t {
+        hipError_t r = take_event(p, x);
+        if (r == hipSuccess) rec->aux.push_back(*x);
+        return r;
+    };
+    // The copy stream starts after everything the call's stream must wait
+    // for (ordering waits inserted for this call, earlier work).
+    hipEvent_t start = nullptr;
+    if ((e = ev(&start)) != hipSuccess) return latch(p, e);
+    if ((e = hipEventRecord(start, stream)) != hipSuccess) return latch(p, e);
+    if ((e = hipStreamWaitEvent(p->copy, start, 0)) != hipSuccess) return latch(p, e);
+
+    hipEvent_t slot_free[2] = {nullptr, nullptr};
+    hipEvent_t last_copy = nullptr;
+    for (uint32_t l0 = 0, k = 0; l0 < L; l0 += G, ++k) {
+        const uint32_t nl = std::min<uint32_t>(G, L - l0);
+        uint8_t* s = p->staging + (k % 2) * slot;
+        // The kernels only touch HBM here: no host-link grid cap.
+        aqua::SwapLaunch Lk = make_launch(p, is_in, s, descs, ndesc, AQUA_TARGET_DEVICE);
+        Lk.first_layer = l0;
+        Lk.num_layers = nl;
+        Lk.img_l0 = l0;
+        hipEvent_t e1 = nullptr, e2 = nullptr;
+        if ((e = ev(&e1)) != hipSuccess || (e = ev(&e2)) != hipSuccess) return latch(p, e);
+        hipStream_t first = is_in ? p->copy : stream;   // fills the slot
+        hipStream_t second = is_in ? stream : p->copy;  // drains it
+        if (slot_free[k % 2] && (e = hipStreamWaitEvent(first, slot_free[k % 2], 0)))
+            return latch(p, e);
+        if (is_in) {
+            for (const StagedSeq& q : p->sseq) {
+                e = hipMemcpyAsync(s + G * q.first * C, (const uint8_t*)buf + q.off + l0 * q.n * C,
+                                   nl * q.n * C, hipMemcpyHostToDevice, p->copy);
+                if (e != hipSuccess) return latch(p, e);
+            }
+        } else {
+            (void)hipGetLastError();
+            if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
+        }
+        if ((e = hipEventRecord(e1, first)) != hipSuccess) return latch(p, e);
+        if ((e = hipStreamWaitEvent(second, e1, 0)) != hipSuccess) return latch(p, e);
+        if (is_in) {
+            (void)hipGetLastError();
+            if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
+        } else {
+            for (const StagedSeq& q : p->sseq) {
+                e = hipMemcpyAsync((uint8_t*)const_cast<void*>(buf) + q.off + l0 * q.n * C,
+                                   s + G * q.first * C, nl * q.n * C, hipMemcpyDeviceToHost,
+                                   p->copy);
+                if (e != hipSuccess) return latch(p, e);
+            }
+        }
+        if ((e = hipEventRecord(e2, second)) != hipSuccess) return latch(p, e);
+        slot_free[k % 2] = e2;
+        if (!is_in) last_copy = e2;
+    }
+    // The call completes on its own stream: after the last copy.
+    if (last_copy && (e = hipStreamWaitEvent(stream, last_copy, 0)) != hipSuccess)
+        return latch(p, e);
     return AQUA_OK;
 }
 
@@ -320,27 +458,76 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
 
     const uint32_t lane = lane_for(p, stream);
     const uint64_t ticket = p->next_ticket;
+    const bool staged = target == AQUA_TARGET_HOST && p->host_path == AQUA_HOST_STAGED && total;
 
+    // Plan.  The staged path plans the concatenated table as one packed
+    // sequence (its layout in the HBM slots).
     p->plan.clear();
-    aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
+    uint64_t slot = 0;
+    uint32_t G = 0;
+    if (staged) {
+        const uint64_t per_layer = total * p->shape.C;
+        G = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(p->shape.L, p->slot_target / per_layer));
+        slot = (uint64_t)G * per_layer;
+        // Descriptors for the slot layout: sequence s at G * first_s * C.
+        p->sseq.clear();
+        p->slot_offsets.assign(num_seqs, 0);
+        for (uint32_t k = 0; k < num_seqs; ++k) {
+            p->slot_offsets[k] = (uint64_t)G * offs[k] * p->shape.C;
+            if (offs[k + 1] > offs[k])
+                p->sseq.push_back({aqua::image_offset(p->shape, a, k), offs[k], offs[k + 1] - offs[k]});
+        }
+        aqua::CallArgs c = a;
+        c.img_offsets = p->slot_offsets.data();
+        aqua::plan_runs(p->shape, c, p->unit_bytes, &p->plan);
+        st = ensure_staging(p, 2 * slot);
+        if (st != AQUA_OK) return st;
+    } else {
+        aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
+    }
     aqua::image_ranges(p->shape, a, &p->ranges);
     for (auto& r : p->ranges) {  // tracked by the caller's address of the buffer
         r.first += a.buf;
         r.second += a.buf;
     }
+    const std::pair<uint64_t, uint64_t> stage_range{
+        (uint64_t)(uintptr_t)p->staging, (uint64_t)(uintptr_t)p->staging + 2 * slot};
 
     // Reserve descriptor space before registering the ticket: a reservation
     // may wait on earlier tickets.
     uint64_t ring_off = 0;
     const uint64_t dbytes = p->plan.size() * sizeof(RunDesc);
+    uint64_t waited_ns = 0;
     if (dbytes) {
+        const auto w0 = std::chrono::steady_clock::now();
         st = ring_reserve(p, dbytes, &ring_off);
+        waited_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                        std::chrono::steady_clock::now() - w0)
+                        .count();
         if (st != AQUA_OK) return st;
     }
 
-    p->stats.waits_elided += p->tracker.issue(ticket, lane, is_in, ids, (size_t)total,
-                                              p->ranges.data(), p->ranges.size(),
-                                              &p->deps);
+    // Accesses: swap-out reads the table's blocks and writes the images,
+    // swap-in reads the images and writes the blocks; the staged path also
+    // writes its slots.
+    HazardTracker::Access acc;
+    if (is_in) {
+        acc.blocks_written = ids;
+        acc.n_blocks_written = (size_t)total;
+        acc.ranges_read = p->ranges.data();
+        acc.n_ranges_read = p->ranges.size();
+        if (staged) {
+            acc.ranges_written = &stage_range;
+            acc.n_ranges_written = 1;
+        }
+    } else {
+        acc.blocks_read = ids;
+        acc.n_blocks_read = (size_t)total;
+        if (staged) p->ranges.push_back(stage_range);
+        acc.ranges_written = p->ranges.data();
+        acc.n_ranges_written = p->ranges.size();
+    }
+    p->stats.waits_elided += p->tracker.issue(ticket, lane, acc, &p->deps);
     p->next_ticket++;
 
     for (const HazardTracker::Dep& d : p->deps) {
@@ -351,7 +538,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         p->stats.waits_inserted++;
     }
 
-    hipEvent_t up_ev = nullptr;
+    Outstanding rec{ticket, nullptr, {}};
     if (dbytes) {
         std::memcpy(p->ring_host + ring_off, p->plan.data(), dbytes);
         hipError_t e = hipSuccess;
@@ -362,33 +549,33 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                            hipMemcpyHostToDevice, stream);
 #elif AQUA_DESC_MODE == 1
         descs = p->ring_dev + ring_off;
+        hipEvent_t up_ev = nullptr;
         e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
                            hipMemcpyHostToDevice, p->upload);
         if (e == hipSuccess) e = take_event(p, &up_ev);
+        if (e == hipSuccess) rec.aux.push_back(up_ev);
         if (e == hipSuccess) e = hipEventRecord(up_ev, p->upload);
         if (e == hipSuccess) e = hipStreamWaitEvent(stream, up_ev, 0);
 #endif
         if (e != hipSuccess) return latch(p, e);
-        aqua::SwapLaunch L;
-        L.out = !is_in;
-        L.pool = p->base;
-        L.img = dbuf;
-        L.descs = reinterpret_cast<const RunDesc*>(descs);
-        L.ndesc = (uint32_t)p->plan.size();
-        L.num_layers = p->shape.L;
-        L.chunk_bytes = p->shape.C;
-        L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
-        L.max_workgroups = p->max_wg[target];
-        (void)hipGetLastError();
-        e = aqua::launch_swap(L, stream);
-        if (e != hipSuccess) return latch(p, e);
+        if (staged) {
+            st = enqueue_staged(p, is_in, buf, stream, reinterpret_cast<const RunDesc*>(descs),
+                                (uint32_t)p->plan.size(), slot, G, &rec);
+            if (st != AQUA_OK) return st;
+        } else {
+            const aqua::SwapLaunch L =
+                make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
+                            (uint32_t)p->plan.size(), target);
+            (void)hipGetLastError();
+            e = aqua::launch_swap(L, stream);
+            if (e != hipSuccess) return latch(p, e);
+        }
     }
 
-    hipEvent_t ev = nullptr;
-    hipError_t e = take_event(p, &ev);
-    if (e == hipSuccess) e = hipEventRecord(ev, stream);
+    hipError_t e = take_event(p, &rec.ev);
+    if (e == hipSuccess) e = hipEventRecord(rec.ev, stream);
     if (e != hipSuccess) return latch(p, e);
-    p->outstanding[lane].push_back({ticket, ev, up_ev});
+    p->outstanding[lane].push_back(std::move(rec));
     if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
 
     const uint64_t moved = (uint64_t)p->shape.L * total * p->shape.C;
@@ -401,14 +588,19 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     }
     if (target == AQUA_TARGET_HOST) p->stats.bytes_host += moved;
     p->stats.descriptors += p->plan.size();
-    p->stats.host_ns += (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
-                            std::chrono::steady_clock::now() - t0)
-                            .count();
+    const uint64_t total_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                                  std::chrono::steady_clock::now() - t0)
+                                  .count();
+    // Reserving descriptor space blocks only when the ring is full; that
+    // back-pressure is reported apart from the call's own host work.
+    p->stats.wait_ns += waited_ns;
+    p->stats.host_ns += total_ns > waited_ns ? total_ns - waited_ns : 0;
     if (ticket_out) *ticket_out = ticket;
     return AQUA_OK;
 }
 
 }  // namespace
+
 
 extern "C" {
 
@@ -453,6 +645,7 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     p->unit_bytes = env_u64("AQUA_UNIT_BYTES", kDefaultUnitBytes);
     if (!p->unit_bytes) p->unit_bytes = kDefaultUnitBytes;
     if (p->unit_bytes > aqua::kMaxChunkBytes) p->unit_bytes = aqua::kMaxChunkBytes;
+    p->slot_target = env_u64("AQUA_STAGE_SLOT_BYTES", kDefaultSlotBytes);
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
 #if AQUA_DESC_MODE == 1
     if (st == AQUA_OK && hipStreamCreateWithFlags(&p->upload, hipStreamNonBlocking) != hipSuccess) {
@@ -478,10 +671,12 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
         for (auto& q : p->outstanding)
             for (const Outstanding& o : q) {
                 (void)hipEventDestroy(o.ev);
-                if (o.up_ev) (void)hipEventDestroy(o.up_ev);
+                for (hipEvent_t e : o.aux) (void)hipEventDestroy(e);
             }
         for (hipEvent_t ev : p->spare_events) (void)hipEventDestroy(ev);
         free_rings(p);
+        if (p->staging) (void)hipFree(p->staging);
+        if (p->copy) (void)hipStreamDestroy(p->copy);
         if (p->upload) (void)hipStreamDestroy(p->upload);
         if (p->sticky != hipSuccess) st = AQUA_ERR_HIP;
     }
@@ -552,6 +747,12 @@ aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t p, int32_t target,
     if (!p || (target != AQUA_TARGET_DEVICE && target != AQUA_TARGET_HOST))
         return AQUA_ERR_INVALID;
     p->max_wg[target] = max_workgroups;
+    return AQUA_OK;
+}
+
+aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t p, int32_t path) {
+    if (!p || (path != AQUA_HOST_ZERO_COPY && path != AQUA_HOST_STAGED)) return AQUA_ERR_INVALID;
+    p->host_path = path;
     return AQUA_OK;
 }
 

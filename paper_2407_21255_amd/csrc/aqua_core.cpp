@@ -201,10 +201,8 @@ void HazardTracker::need(uint64_t ticket, uint32_t lane, uint64_t* elided) {
     if (ticket > dep_[m]) dep_[m] = ticket;
 }
 
-uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, bool is_in,
-                              const int32_t* blocks, size_t nblocks,
-                              const std::pair<uint64_t, uint64_t>* ranges,
-                              size_t nranges, std::vector<Dep>* deps) {
+uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
+                              std::vector<Dep>* deps) {
     ensure_lane(lane);
     deps->clear();
     std::fill(dep_.begin(), dep_.end(), 0);
@@ -213,61 +211,76 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, bool is_in,
     last_ticket_ = ticket;
     uint64_t elided = 0;
 
-    // Offload ranges: drop finished records, then look for overlaps.
+    // Offload ranges: drop finished records, then look for overlaps.  A
+    // read conflicts with earlier writes; a write with every earlier access.
     size_t w = 0;
     for (size_t k = 0; k < ranges_.size(); ++k)
         if (!done(ranges_[k].ticket)) ranges_[w++] = ranges_[k];
     ranges_.resize(w);
     const size_t old = ranges_.size();
-    for (size_t r = 0; r < nranges; ++r) {
-        const uint64_t lo = ranges[r].first, hi = ranges[r].second;
+    for (size_t r = 0; r < a.n_ranges_read; ++r) {
+        const uint64_t lo = a.ranges_read[r].first, hi = a.ranges_read[r].second;
         for (size_t k = 0; k < old; ++k) {
             const RangeRec& q = ranges_[k];
-            if (q.lo < hi && lo < q.hi && (q.write || !is_in))
-                need(q.ticket, lane, &elided);
+            if (q.write && q.lo < hi && lo < q.hi) need(q.ticket, lane, &elided);
         }
     }
-    if (!is_in) {
+    for (size_t r = 0; r < a.n_ranges_written; ++r) {
+        const uint64_t lo = a.ranges_written[r].first, hi = a.ranges_written[r].second;
+        for (size_t k = 0; k < old; ++k) {
+            const RangeRec& q = ranges_[k];
+            if (q.lo < hi && lo < q.hi) need(q.ticket, lane, &elided);
+        }
+    }
+    if (a.n_ranges_written) {
         // A write that covers an earlier record is ordered after it, and
         // every later access that conflicts with the record conflicts with
         // the write too: the record can go.
         size_t k = 0;
         for (size_t i = 0; i < old; ++i) {
             bool covered = false;
-            for (size_t r = 0; r < nranges && !covered; ++r)
-                covered = ranges[r].first <= ranges_[i].lo && ranges_[i].hi <= ranges[r].second;
+            for (size_t r = 0; r < a.n_ranges_written && !covered; ++r)
+                covered = a.ranges_written[r].first <= ranges_[i].lo &&
+                          ranges_[i].hi <= a.ranges_written[r].second;
             if (!covered) ranges_[k++] = ranges_[i];
         }
         ranges_.resize(k);
     }
-    for (size_t r = 0; r < nranges; ++r)
-        ranges_.push_back({ranges[r].first, ranges[r].second, ticket, lane, !is_in});
+    for (size_t r = 0; r < a.n_ranges_read; ++r)
+        ranges_.push_back({a.ranges_read[r].first, a.ranges_read[r].second, ticket, lane, false});
+    for (size_t r = 0; r < a.n_ranges_written; ++r)
+        ranges_.push_back(
+            {a.ranges_written[r].first, a.ranges_written[r].second, ticket, lane, true});
 
-    // Pool blocks.
-    for (size_t j = 0; j < nblocks; ++j) {
-        const uint32_t b = (uint32_t)blocks[j];
+    // Pool blocks read: after their last writer; join the readers.
+    for (size_t j = 0; j < a.n_blocks_read; ++j) {
+        const uint32_t b = (uint32_t)a.blocks_read[j];
         need(last_writer_[b], lane, &elided);
         std::vector<Reader>& rd = readers_[b];
-        if (is_in) {
-            for (const Reader& q : rd) need(q.ticket, lane, &elided);
-            rd.clear();
-            last_writer_[b] = ticket;
-        } else {
-            bool found = false;
-            for (Reader& q : rd)
-                if (q.lane == lane) {
-                    q.ticket = ticket;
-                    found = true;
-                }
-            if (!found) {
-                // Forget readers that have finished before adding one.
-                size_t k = 0;
-                for (size_t i = 0; i < rd.size(); ++i)
-                    if (!done(rd[i].ticket)) rd[k++] = rd[i];
-                rd.resize(k);
-                rd.push_back({lane, ticket});
+        bool found = false;
+        for (Reader& q : rd)
+            if (q.lane == lane) {
+                q.ticket = ticket;
+                found = true;
             }
+        if (!found) {
+            // Forget readers that have finished before adding one.
+            size_t k = 0;
+            for (size_t i = 0; i < rd.size(); ++i)
+                if (!done(rd[i].ticket)) rd[k++] = rd[i];
+            rd.resize(k);
+            rd.push_back({lane, ticket});
         }
+    }
+    // Pool blocks written: after their last writer and every reader since.
+    for (size_t j = 0; j < a.n_blocks_written; ++j) {
+        const uint32_t b = (uint32_t)a.blocks_written[j];
+        need(last_writer_[b], lane, &elided);
+        std::vector<Reader>& rd = readers_[b];
+        for (const Reader& q : rd)
+            if (q.ticket != ticket) need(q.ticket, lane, &elided);
+        rd.clear();
+        last_writer_[b] = ticket;
     }
 
     for (uint32_t m = 0; m < dep_.size(); ++m)

@@ -98,14 +98,25 @@ public:
     explicit HazardTracker(uint32_t num_blocks = 0) { reset(num_blocks); }
     void reset(uint32_t num_blocks);
 
+    // What one call touches: pool blocks it reads or writes, and byte
+    // ranges [lo, hi) of offload buffers (by address) it reads or writes.
+    struct Access {
+        const int32_t* blocks_read = nullptr;
+        size_t n_blocks_read = 0;
+        const int32_t* blocks_written = nullptr;
+        size_t n_blocks_written = 0;
+        const std::pair<uint64_t, uint64_t>* ranges_read = nullptr;
+        size_t n_ranges_read = 0;
+        const std::pair<uint64_t, uint64_t>* ranges_written = nullptr;
+        size_t n_ranges_written = 0;
+    };
+
     // Registers call `ticket` (must exceed every earlier ticket) on `lane`.
-    // Swap-out (is_in false) reads `blocks` and writes `ranges`; swap-in
-    // reads `ranges` and writes `blocks`.  Writes into *deps, per other
-    // lane, the newest earlier ticket the call must wait for.  Returns the
-    // number of conflicts that were skipped because already complete.
-    uint64_t issue(uint64_t ticket, uint32_t lane, bool is_in,
-                   const int32_t* blocks, size_t nblocks,
-                   const std::pair<uint64_t, uint64_t>* ranges, size_t nranges,
+    // Writes into *deps, per other lane, the newest earlier ticket the call
+    // must wait for.  Returns the number of conflicts that were skipped
+    // because already complete.  Blocks written by one call must be
+    // distinct; a range both read and written is listed as written.
+    uint64_t issue(uint64_t ticket, uint32_t lane, const Access& a,
                    std::vector<Dep>* deps);
 
     // Everything on `lane` up to and including `ticket` has completed.

@@ -55,8 +55,10 @@ void* aqua_core_tracker_new(uint32_t num_blocks) {
 
 void aqua_core_tracker_free(void* t) { delete static_cast<aqua::HazardTracker*>(t); }
 
-// ranges: nranges pairs (lo, hi).  Returns the number of dependencies and
-// writes them to dep_lanes / dep_tickets (at most max_deps).
+// ranges: nranges pairs (lo, hi).  A swap-out (is_in 0) reads `blocks`
+// and writes the ranges; a swap-in reads the ranges and writes `blocks`.
+// Returns the number of dependencies and writes them to dep_lanes /
+// dep_tickets (at most max_deps).
 int64_t aqua_core_tracker_issue(void* t, uint64_t ticket, uint32_t lane,
                                 int32_t is_in, const int32_t* blocks,
                                 uint64_t nblocks, const uint64_t* ranges,
@@ -65,8 +67,50 @@ int64_t aqua_core_tracker_issue(void* t, uint64_t ticket, uint32_t lane,
     auto* tr = static_cast<aqua::HazardTracker*>(t);
     std::vector<std::pair<uint64_t, uint64_t>> r(nranges);
     for (uint64_t k = 0; k < nranges; ++k) r[k] = {ranges[2 * k], ranges[2 * k + 1]};
+    aqua::HazardTracker::Access acc;
+    if (is_in) {
+        acc.blocks_written = blocks;
+        acc.n_blocks_written = nblocks;
+        acc.ranges_read = r.data();
+        acc.n_ranges_read = r.size();
+    } else {
+        acc.blocks_read = blocks;
+        acc.n_blocks_read = nblocks;
+        acc.ranges_written = r.data();
+        acc.n_ranges_written = r.size();
+    }
     std::vector<aqua::HazardTracker::Dep> deps;
-    tr->issue(ticket, lane, is_in != 0, blocks, nblocks, r.data(), r.size(), &deps);
+    tr->issue(ticket, lane, acc, &deps);
+    for (uint64_t k = 0; k < deps.size() && k < max_deps; ++k) {
+        dep_lanes[k] = deps[k].lane;
+        dep_tickets[k] = deps[k].ticket;
+    }
+    return (int64_t)deps.size();
+}
+
+// General form: separate read and write sets (ranges as (lo, hi) pairs).
+int64_t aqua_core_tracker_issue_rw(void* t, uint64_t ticket, uint32_t lane,
+                                   const int32_t* blocks_r, uint64_t nbr,
+                                   const int32_t* blocks_w, uint64_t nbw,
+                                   const uint64_t* ranges_r, uint64_t nrr,
+                                   const uint64_t* ranges_w, uint64_t nrw,
+                                   uint32_t* dep_lanes, uint64_t* dep_tickets,
+                                   uint64_t max_deps) {
+    auto* tr = static_cast<aqua::HazardTracker*>(t);
+    std::vector<std::pair<uint64_t, uint64_t>> rr(nrr), rw(nrw);
+    for (uint64_t k = 0; k < nrr; ++k) rr[k] = {ranges_r[2 * k], ranges_r[2 * k + 1]};
+    for (uint64_t k = 0; k < nrw; ++k) rw[k] = {ranges_w[2 * k], ranges_w[2 * k + 1]};
+    aqua::HazardTracker::Access acc;
+    acc.blocks_read = blocks_r;
+    acc.n_blocks_read = nbr;
+    acc.blocks_written = blocks_w;
+    acc.n_blocks_written = nbw;
+    acc.ranges_read = rr.data();
+    acc.n_ranges_read = rr.size();
+    acc.ranges_written = rw.data();
+    acc.n_ranges_written = rw.size();
+    std::vector<aqua::HazardTracker::Dep> deps;
+    tr->issue(ticket, lane, acc, &deps);
     for (uint64_t k = 0; k < deps.size() && k < max_deps; ++k) {
         dep_lanes[k] = deps[k].lane;
         dep_tickets[k] = deps[k].ticket;

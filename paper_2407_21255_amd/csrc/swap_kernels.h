@@ -13,8 +13,10 @@ struct SwapLaunch {
     bool out;                 // true: pool -> image, false: image -> pool
     uint8_t* pool;            // device pointer of the pool base
     uint8_t* img;             // device-accessible pointer of the buffer base
+    uint32_t img_l0;          // layer l's image data starts at img_off + (l - img_l0) * lstride
     const RunDesc* descs;     // device copy of the run descriptors
     uint32_t ndesc;
+    uint32_t first_layer;     // layers [first_layer, first_layer + num_layers)
     uint32_t num_layers;
     uint64_t chunk_bytes;     // C
     uint64_t pool_lstride;    // N * C

@@ -92,19 +92,21 @@ __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
 
 // OUT: pool -> image (gather).  !OUT: image -> pool (scatter).
 // Work unit u in [0, units) is (layer l0 + u / ndesc, descriptor u % ndesc);
+// layer l of the image side starts img_l0 layers before img_off's origin
+// (0 for whole images, the first staged layer for a staging slot);
 // consecutive workgroups take consecutive runs of one layer, so the image
 // side of a gather is written front to back.
 template <bool OUT, int UNROLL>
 __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
     uint8_t* __restrict__ pool, uint8_t* __restrict__ img,
-    const RunDesc* __restrict__ descs, uint32_t ndesc, uint32_t l0,
+    const RunDesc* __restrict__ descs, uint32_t ndesc, uint32_t l0, uint32_t img_l0,
     uint32_t units, uint64_t chunk_bytes, uint64_t pool_lstride) {
     for (uint32_t u = blockIdx.x; u < units; u += gridDim.x) {
         const uint32_t l = l0 + u / ndesc;
         const uint32_t k = u - (u / ndesc) * ndesc;
         const RunDesc dsc = descs[k];
         uint8_t* p = pool + (uint64_t)l * pool_lstride + (uint64_t)dsc.block * chunk_bytes;
-        uint8_t* m = img + dsc.img_off + (uint64_t)l * dsc.img_lstride;
+        uint8_t* m = img + dsc.img_off + (uint64_t)(l - img_l0) * dsc.img_lstride;
         const uint32_t nvec = (uint32_t)((uint64_t)dsc.nchunks * chunk_bytes / 16);
         if constexpr (OUT)
             copy_span<UNROLL, AQUA_NT_OUT_LD, AQUA_NT_OUT_ST>(
@@ -121,18 +123,19 @@ hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
     if (!a.ndesc || !a.num_layers) return hipSuccess;
     // Split by layers so that every launch has fewer than 2^31 units.
     const uint32_t per = (uint32_t)std::max<uint64_t>(1, (1ull << 31) / a.ndesc);
-    for (uint32_t l0 = 0; l0 < a.num_layers; l0 += per) {
-        const uint32_t nl = std::min<uint32_t>(per, a.num_layers - l0);
+    const uint32_t end = a.first_layer + a.num_layers;
+    for (uint32_t l0 = a.first_layer; l0 < end; l0 += per) {
+        const uint32_t nl = std::min<uint32_t>(per, end - l0);
         const uint32_t units = nl * a.ndesc;
         uint32_t grid = units;
         if (a.max_workgroups && grid > a.max_workgroups) grid = a.max_workgroups;
         if (a.out)
             hipLaunchKernelGGL((swap_runs_kernel<true, kUnroll>), dim3(grid), dim3(kThreads), 0,
-                               stream, a.pool, a.img, a.descs, a.ndesc, l0, units,
+                               stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
                                a.chunk_bytes, a.pool_lstride);
         else
             hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll>), dim3(grid), dim3(kThreads), 0,
-                               stream, a.pool, a.img, a.descs, a.ndesc, l0, units,
+                               stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
                                a.chunk_bytes, a.pool_lstride);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

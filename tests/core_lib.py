@@ -42,6 +42,9 @@ def lib():
         L.aqua_core_tracker_free.argtypes = [P]
         L.aqua_core_tracker_issue.argtypes = [P, u64, u32, i32, P, u64, P, u64, P, P, u64]
         L.aqua_core_tracker_issue.restype = i64
+        L.aqua_core_tracker_issue_rw.argtypes = [P, u64, u32, P, u64, P, u64, P, u64, P, u64,
+                                                 P, P, u64]
+        L.aqua_core_tracker_issue_rw.restype = i64
         L.aqua_core_tracker_complete.argtypes = [P, u32, u64]
         L.aqua_core_tracker_live_ranges.argtypes = [P]
         L.aqua_core_tracker_live_ranges.restype = u64
@@ -87,6 +90,19 @@ class Tracker:
         tickets = np.zeros(64, dtype=np.uint64)
         n = lib().aqua_core_tracker_issue(self.h, ticket, lane, int(is_in), _p(b), b.size,
                                           _p(r), r.size // 2, _p(lanes), _p(tickets), 64)
+        assert 0 <= n <= 64
+        return [(int(lanes[k]), int(tickets[k])) for k in range(n)]
+
+    def issue_rw(self, ticket, lane, blocks_r, blocks_w, ranges_r, ranges_w):
+        br = np.ascontiguousarray(blocks_r, dtype=np.int32)
+        bw = np.ascontiguousarray(blocks_w, dtype=np.int32)
+        rr = np.ascontiguousarray(np.asarray(ranges_r, dtype=np.uint64).reshape(-1))
+        rw = np.ascontiguousarray(np.asarray(ranges_w, dtype=np.uint64).reshape(-1))
+        lanes = np.zeros(64, dtype=np.uint32)
+        tickets = np.zeros(64, dtype=np.uint64)
+        n = lib().aqua_core_tracker_issue_rw(self.h, ticket, lane, _p(br), br.size, _p(bw),
+                                             bw.size, _p(rr), rr.size // 2, _p(rw),
+                                             rw.size // 2, _p(lanes), _p(tickets), 64)
         assert 0 <= n <= 64
         return [(int(lanes[k]), int(tickets[k])) for k in range(n)]
 

@@ -75,6 +75,8 @@ def oracle_replay(sched, pool_np, region_np, first, count):
     """The oracle's run of slices [first, first+count) in issue order."""
     d = odesc(sched.shape)
     for s in range(first, first + count):
+        if (s - first) % 10 == 0:
+            say("oracle replay: slice", s)
         sl = sched.slices[s]
         out_off = [sched.slot_offsets[p] for p in sl.out_prompts]
         in_off = [sched.slot_offsets[p] for p in sl.in_prompts]

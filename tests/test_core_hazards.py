@@ -33,7 +33,21 @@ def _conflict(a, b):
     return False
 
 
-def _run_sequence(rng, n_calls, n_blocks, n_lanes, inform_prob, complete_steps):
+def _overlap(ra, rb):
+    return any(lo < hi2 and lo2 < hi for lo, hi in ra for lo2, hi2 in rb)
+
+
+def _conflict_rw(a, b):
+    """a, b: (blocks_r, blocks_w, ranges_r, ranges_w)."""
+    br, bw, rr, rw = a
+    cr, cw, sr, sw = b
+    if set(bw) & (set(cr) | set(cw)) or set(cw) & set(br):
+        return True
+    return _overlap(rw, sr + sw) or _overlap(sw, rr)
+
+
+def _run_sequence(rng, n_calls, n_blocks, n_lanes, inform_prob, complete_steps,
+                  general=False):
     tr = Tracker(n_blocks)
     calls = []          # (is_in, blocks, ranges, lane)
     waits = {}          # ticket -> list of dep tickets
@@ -64,10 +78,27 @@ def _run_sequence(rng, n_calls, n_blocks, n_lanes, inform_prob, complete_steps):
         if not is_in:  # a swap-out's images never overlap each other
             ranges.sort()
             ranges = [r for i, r in enumerate(ranges) if i == 0 or r[0] >= ranges[i - 1][1]]
-        deps = tr.issue(t, m, is_in, blocks, ranges)
+        if general:
+            # Arbitrary read and write sets: distinct written blocks, read
+            # blocks possibly repeated, ranges read and written (migration).
+            kw = int(rng.integers(0, min(3, n_blocks + 1)))
+            bw = [int(x) for x in rng.choice(n_blocks, size=kw, replace=False)]
+            br = [int(x) for x in rng.integers(0, n_blocks, size=int(rng.integers(0, 3)))]
+            br = [b for b in br if b not in bw]
+            rr, rw = [], []
+            for _ in range(int(rng.integers(0, 3))):
+                lo = int(rng.integers(0, 64)) * 16
+                (rr if rng.random() < 0.5 else rw).append(
+                    (lo, lo + int(rng.integers(1, 8)) * 16))
+            acc = (br, bw, rr, rw)
+            deps = tr.issue_rw(t, m, br, bw, rr, rw)
+        else:
+            acc = (([] if is_in else blocks), (blocks if is_in else []),
+                   (ranges if is_in else []), ([] if is_in else ranges))
+            deps = tr.issue(t, m, is_in, blocks, ranges)
         for lane, dt in deps:
             assert lane != m and calls[dt - 1][3] == lane
-        calls.append((is_in, blocks, ranges, m))
+        calls.append((acc, None, None, m))
         waits[t] = [dt for _, dt in deps]
         informed_at_issue[t] = dict(informed)
         lane_tickets[m].append(t)
@@ -112,7 +143,7 @@ def _run_sequence(rng, n_calls, n_blocks, n_lanes, inform_prob, complete_steps):
         reach[t] = r
     for j in range(1, n + 1):
         for i in range(1, j):
-            if _conflict(calls[i - 1][:3], calls[j - 1][:3]):
+            if _conflict_rw(calls[i - 1][0], calls[j - 1][0]):
                 assert i in reach[j], (i, j, calls[i - 1], calls[j - 1], waits[j])
     return calls, waits
 
@@ -123,6 +154,14 @@ def test_random_sequences_are_sequentially_consistent():
         _run_sequence(rng, n_calls=int(rng.integers(5, 40)), n_blocks=int(rng.integers(2, 12)),
                       n_lanes=int(rng.integers(1, 4)), inform_prob=float(rng.random()),
                       complete_steps=int(rng.integers(1, 4)))
+
+
+def test_random_read_write_sets_are_sequentially_consistent():
+    rng = np.random.default_rng(32)
+    for trial in range(300):
+        _run_sequence(rng, n_calls=int(rng.integers(5, 40)), n_blocks=int(rng.integers(2, 12)),
+                      n_lanes=int(rng.integers(1, 4)), inform_prob=float(rng.random()),
+                      complete_steps=int(rng.integers(1, 4)), general=True)
 
 
 def test_waits_only_where_needed():

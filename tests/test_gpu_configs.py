@@ -28,7 +28,8 @@ def _gpu():
     torch.cuda.empty_cache()
 
 
-def _full_round_trip(case: wl.SwapCase, pinned: bool, gemm: bool = False):
+def _full_round_trip(case: wl.SwapCase, pinned: bool, gemm: bool = False,
+                     host_path=None):
     s = case.shape
     d = odesc(s)
     t0 = time.time()
@@ -46,6 +47,8 @@ def _full_round_trip(case: wl.SwapCase, pinned: bool, gemm: bool = False):
     swap = torch.cuda.Stream()
     comp = torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
+    if host_path is not None:
+        kv.set_host_path(host_path)
     try:
         if gemm:  # a compute stream busy with bf16 GEMMs while the swap runs
             a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
@@ -84,10 +87,13 @@ def test_llama8b_hbm_full():
     _full_round_trip(wl.llama8b_hbm_case(), pinned=False)
 
 
-def test_llama8b_pinned_host_full_with_gemm():
+@pytest.mark.parametrize("path", ["zero_copy", "staged"])
+def test_llama8b_pinned_host_full_with_gemm(path):
     """8 x 4096-token prompts out to pinned host memory and back while a
     second stream runs bf16 GEMMs."""
-    _full_round_trip(wl.llama8b_host_case(), pinned=True, gemm=True)
+    _full_round_trip(wl.llama8b_host_case(), pinned=True, gemm=True,
+                     host_path={"staged": aqua.AQUA_HOST_STAGED,
+                                "zero_copy": aqua.AQUA_HOST_ZERO_COPY}[path])
 
 
 def test_llama70b_hbm_full():
@@ -95,8 +101,12 @@ def test_llama70b_hbm_full():
     _full_round_trip(wl.llama70b_case(), pinned=False)
 
 
-def test_llama70b_pinned_host_full():
-    _full_round_trip(wl.llama70b_case(seed=14), pinned=True)
+@pytest.mark.parametrize("path", ["zero_copy", "staged"])
+def test_llama70b_pinned_host_full(path):
+    """The 10 GiB image of one 32768-token prompt in pinned host memory."""
+    _full_round_trip(wl.llama70b_case(seed=14), pinned=True,
+                     host_path={"staged": aqua.AQUA_HOST_STAGED,
+                                "zero_copy": aqua.AQUA_HOST_ZERO_COPY}[path])
 
 
 def test_preemption_cycle_full():

@@ -28,7 +28,7 @@ def _gpu():
 
 
 def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
-               buf_bytes=None, pinned=False, sentinel=True, stream=None):
+               buf_bytes=None, pinned=False, sentinel=True, stream=None, host_path=None):
     """swap_out(out_tables) then swap_in(in_tables) on the GPU and in the
     oracle; compares the image, guards and the whole pool."""
     C = shape.chunk_bytes
@@ -46,6 +46,8 @@ def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
     buf = guarded_buffer(size, G, pinned)
     inner = buf[G:G + size]
     kv = aqua.KVPool(shape.as_tuple(), pool)
+    if host_path is not None:
+        kv.set_host_path(host_path)
     try:
         t1 = kv.swap_out(out_tables, inner, img_offsets, stream=stream)
         kv.sync(t1)
@@ -133,11 +135,38 @@ def test_unit_size_extremes(unit, monkeypatch):
     _roundtrip(shape, 9, out_tables, in_tables, None)
 
 
-def test_pinned_host_target_round_trip():
+def test_pinned_host_zero_copy_round_trip():
     """The offload image in pinned host memory, written and read zero-copy."""
     case = wl.tiny_case(seed=11)
-    say("host target tiny")
+    say("host target zero-copy tiny")
     _roundtrip(case.shape, case.seed, case.out_tables, case.in_tables, case.owner,
+               pinned=True, host_path=aqua.AQUA_HOST_ZERO_COPY)
+
+
+def test_pinned_host_staged_round_trip():
+    """The default (staged) host path: gather into HBM slots, copy engines
+    over the link; same bytes as the oracle."""
+    case = wl.tiny_case(seed=12)
+    say("host target staged tiny")
+    _roundtrip(case.shape, case.seed, case.out_tables, case.in_tables, case.owner,
+               pinned=True)
+
+
+@pytest.mark.parametrize("shape", RAGGED[:2], ids=lambda s: f"C{s.chunk_bytes}")
+def test_pinned_host_staged_placed_images(shape):
+    """Placed images with gaps in a pinned buffer on the staged path: the
+    gaps and guards must stay untouched."""
+    N = shape.num_blocks
+    perm = wl.permutation(N, 43)
+    out_tables = [perm[:5], perm[5:6], [], perm[6:20]]
+    in_tables = [perm[20:25], perm[25:26], [], perm[26:40]]
+    offs, pos = [], 0
+    for t in out_tables:
+        pos = (pos + 4096 + 48 + 15) // 16 * 16
+        offs.append(pos)
+        pos += shape.image_bytes(len(t))
+    say("staged placed", shape)
+    _roundtrip(shape, 8, out_tables, in_tables, None, img_offsets=offs, buf_bytes=pos + 4096,
                pinned=True)
 
 
