@@ -34,8 +34,8 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # were taken on: a changed kernel reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama8b_hbm", "35d08644ad681be3"): {
-        "gather (swap-out)": 4295902800, "scatter (swap-in)": 4295816800},
+    ("llama8b_hbm", "ea082bfbccbff980"): {
+        "gather (swap-out)": 4295912960, "scatter (swap-in)": 4295821414},
 }
 
 
@@ -354,14 +354,19 @@ def run_cycle(args, res_common):
         if timed:
             b1.record(sb)
             evs.append((a0, a1, b0, b1, len(out[0]), len(inn[0])))
-        kv.sync(0)
+        kv.sync(0)  # the slice boundary
 
+    # Each slice ends with aqua_sync, as a scheduler's loop boundary does.
+    # (Issued without it, slices stay correct -- the library orders reused
+    # blocks and slots -- but consecutive slices then contend for HBM.)
     for k in range(args.warmup):
         one(k, False)
+    kv.sync(0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.warmup, n):
         one(k, True)
+    kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = kv.stats()
@@ -382,6 +387,7 @@ def run_cycle(args, res_common):
             "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
             "pool_blocks": s.num_blocks, "chunk_bytes": C, "prompts": len(sched.nblocks),
             "swaps_per_slice": 16, "slices_timed": args.steps,
+            "host_sync_per_slice": True,
             "mean_payload_bytes_per_direction": round(float(out_b.mean())),
             "offload_target": "hbm", "parallelism": "single_gpu",
         },

@@ -27,9 +27,11 @@ constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 
 // How run descriptors reach the kernels.  2 (shipped): the kernels read
 // them straight from the pinned, coherent host ring -- one 32-byte scalar
-// load per workgroup, and no copy on the call's stream.  0 and 1 exist for
-// measurement: 0 copies them to a device ring on the call's stream, 1 on
-// the library's upload stream, which the call's stream then waits for.
+// load per workgroup, and no copy on the call's stream; staged host calls
+// copy them to the device ring instead (the link is busy with their data).
+// 0 and 1 exist for measurement: 0 copies them to the device ring on the
+// call's stream, 1 on the library's upload stream, which the call's stream
+// then waits for.
 #ifndef AQUA_DESC_MODE
 #define AQUA_DESC_MODE 2
 #endif
@@ -215,10 +217,10 @@ void free_rings(aqua_kv_pool* p) {
 }
 
 aqua_status alloc_rings(aqua_kv_pool* p, uint64_t bytes) {
-    hipError_t e = hipSuccess;
-#if AQUA_DESC_MODE != 2
-    e = hipMalloc((void**)&p->ring_dev, bytes);
-#endif
+    // The device ring serves the staged host path (and the measurement
+    // modes): there the copy engines keep the host link busy, and
+    // descriptors fetched over it would stall the gathers.
+    hipError_t e = hipMalloc((void**)&p->ring_dev, bytes);
     if (e == hipSuccess)
         e = hipHostMalloc((void**)&p->ring_host, bytes,
                           hipHostMallocMapped | hipHostMallocCoherent);
@@ -543,6 +545,11 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         std::memcpy(p->ring_host + ring_off, p->plan.data(), dbytes);
         hipError_t e = hipSuccess;
         const uint8_t* descs = p->ring_host_dev + ring_off;
+        if (staged) {
+            descs = p->ring_dev + ring_off;
+            e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
+                               hipMemcpyHostToDevice, stream);
+        }
 #if AQUA_DESC_MODE == 0
         descs = p->ring_dev + ring_off;
         e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,

@@ -71,7 +71,7 @@ def apply_mutations_device(sched, s, pool_t, region_t):
         region_t[o:o + n].fill_(wl.CONSUMED_BYTE)
 
 
-def oracle_replay(sched, pool_np, region_np, first, count):
+def oracle_replay(sched, pool_np, region_np, first, count, mutate=True):
     """The oracle's run of slices [first, first+count) in issue order."""
     d = odesc(sched.shape)
     for s in range(first, first + count):
@@ -82,4 +82,5 @@ def oracle_replay(sched, pool_np, region_np, first, count):
         in_off = [sched.slot_offsets[p] for p in sl.in_prompts]
         assert oracle.swap_out(d, pool_np, sl.out_tables, region_np, out_off) == 0
         assert oracle.swap_in(d, pool_np, sl.in_tables, region_np, in_off) == 0
-        apply_mutations_host(sched, s, pool_np, region_np)
+        if mutate:
+            apply_mutations_host(sched, s, pool_np, region_np)

@@ -141,3 +141,35 @@ def test_preemption_cycle_full():
         kv.close()
         del pool, region
         torch.cuda.empty_cache()
+
+
+def test_preemption_cycle_without_host_syncs():
+    """The same schedule issued slice after slice with no host
+    synchronisation (no mutations in between): blocks that one slice frees
+    are reused by later swap-ins while earlier swap-outs may still read
+    them, and only the library's waits keep the result equal to the
+    oracle's sequential replay."""
+    n = 24
+    sched = wl.preemption_schedule(n_slices=n, seed=15)
+    s = sched.shape
+    pool = device_pool(s, sched.seed, schedule_owner(sched))
+    region = region_for(sched)
+    pool_h, region_h = host(pool), host(region)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    try:
+        for k in range(n):
+            out, out_off, inn, in_off = slice_tables(sched, k)
+            kv.swap_out(out, region, out_off, stream=sa)
+            kv.swap_in(inn, region, in_off, stream=sb)
+        kv.sync(0)
+        st = kv.stats()
+        say("unsynchronised cycle", st)
+        oracle_replay(sched, pool_h, region_h, 0, n, mutate=False)
+        assert_bytes_equal(host(region), region_h, "offload region")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["waits_inserted"] > 0
+    finally:
+        kv.close()
+        del pool, region
+        torch.cuda.empty_cache()
