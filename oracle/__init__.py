@@ -69,6 +69,12 @@ def lib() -> ctypes.CDLL:
         L.oracle_swap_out.restype = i32
         L.oracle_swap_in.argtypes = [D, P, u64, u32, P, P, P, u64, P]
         L.oracle_swap_in.restype = i32
+        L.oracle_swap_out_ex.argtypes = [D, P, u64, u32, P, P, P, u64, P, P, u32, u32]
+        L.oracle_swap_out_ex.restype = i32
+        L.oracle_swap_in_ex.argtypes = [D, P, u64, u32, P, P, P, u64, P, P, u32, u32]
+        L.oracle_swap_in_ex.restype = i32
+        L.oracle_migrate.argtypes = [P, u64, P, u64, u32, P, P, P]
+        L.oracle_migrate.restype = i32
         _lib = L
     return _lib
 
@@ -135,3 +141,43 @@ def swap_in(d: KVDesc, pool: np.ndarray, tables, src: np.ndarray,
         ctypes.byref(d), _ptr(pool), pool.nbytes, len(offs) - 1, _ptr(ids),
         _ptr(offs), _ptr(src), src.nbytes if src_bytes is None else src_bytes,
         _ptr(io)))
+
+
+def _u64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.uint64)
+
+
+def swap_out_ex(d: KVDesc, pool: np.ndarray, tables, dst: np.ndarray,
+                img_offsets=None, img_blocks=None, first_layer=0, num_layers=0,
+                *, ids=None, offs=None, dst_bytes=None) -> int:
+    """Swap-out of layers [first_layer, first_layer + num_layers) (all when
+    num_layers is 0) into images of img_blocks[s] blocks per layer."""
+    if ids is None:
+        ids, offs = _tables(tables)
+    io, ib = _u64(img_offsets), _u64(img_blocks)
+    return int(lib().oracle_swap_out_ex(
+        ctypes.byref(d), _ptr(pool), pool.nbytes, len(offs) - 1, _ptr(ids),
+        _ptr(offs), _ptr(dst), dst.nbytes if dst_bytes is None else dst_bytes,
+        _ptr(io), _ptr(ib), first_layer, num_layers))
+
+
+def swap_in_ex(d: KVDesc, pool: np.ndarray, tables, src: np.ndarray,
+               img_offsets=None, img_blocks=None, first_layer=0, num_layers=0,
+               *, ids=None, offs=None, src_bytes=None) -> int:
+    if ids is None:
+        ids, offs = _tables(tables)
+    io, ib = _u64(img_offsets), _u64(img_blocks)
+    return int(lib().oracle_swap_in_ex(
+        ctypes.byref(d), _ptr(pool), pool.nbytes, len(offs) - 1, _ptr(ids),
+        _ptr(offs), _ptr(src), src.nbytes if src_bytes is None else src_bytes,
+        _ptr(io), _ptr(ib), first_layer, num_layers))
+
+
+def migrate(src: np.ndarray, dst: np.ndarray, src_offsets, dst_offsets, lengths,
+            src_bytes=None, dst_bytes=None) -> int:
+    """Copy byte ranges from one offload buffer to another."""
+    so, do, ln = _u64(src_offsets), _u64(dst_offsets), _u64(lengths)
+    return int(lib().oracle_migrate(
+        _ptr(src), src.nbytes if src_bytes is None else src_bytes, _ptr(dst),
+        dst.nbytes if dst_bytes is None else dst_bytes, len(ln), _ptr(so), _ptr(do),
+        _ptr(ln)))
