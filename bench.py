@@ -56,6 +56,15 @@ WORKLOADS = {
                      "pinned host memory and back",
     "tiny": "4 layers, 8 KV heads, head_dim 128, block 16, fp16, 256-block pool: one "
             "512-token prompt out to an HBM buffer and back",
+    "prefix": "prefill caching on a Yi-34B-shaped pool (60 layers, 8 KV heads, head_dim 128, "
+              "bf16, 8192 blocks): the KV of a 100000-token prompt is cached once in an HBM "
+              "region; each step swaps its prefix (all but the last 256 tokens) back in "
+              "from the cached image",
+    "prefix_host": "the same prefix cache held in pinned host memory",
+    "layered": "Llama-3-70B-shaped KV, one 32768-token prompt swapped in from an HBM region "
+               "in 10 layer groups of 8, one ticket each",
+    "migrate": "Llama-3-70B-shaped KV: the 10 GiB image of one 32768-token prompt migrated "
+               "from the HBM region to pinned host memory and back",
     "cycle": "time-sliced preemption on a Llama-3-8B-shaped fp8 e4m3 pool (16384 blocks): "
              "64 prompts of 128..8192 tokens, each slice swaps the 16 longest-resident out "
              "on one stream and the 16 longest-waiting in on another",
@@ -408,6 +417,132 @@ def run_cycle(args, res_common):
     return res, s
 
 
+def run_next(args, res_common):
+    """Prefix swap-in, layer-group swap-in, and image migration."""
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import aqua
+    from paper_2407_21255_amd import workload as wl
+
+    w = args.workload
+    if w.startswith("prefix"):
+        s = wl.YI34B
+        n = ceil_div_tokens(100000, s.block_tokens)          # 6250 blocks
+        m = n - 256 // s.block_tokens                          # prefix: all but 256 tokens
+        perm = wl.permutation(s.num_blocks, 6)
+        prompt, fresh = perm[:n], perm[s.num_blocks - m:]
+        owner = {b: (0, i) for i, b in enumerate(prompt)}
+    else:
+        case = wl.llama70b_case()
+        s, prompt, fresh, owner = case.shape, case.out_tables[0], case.in_tables[0], case.owner
+        n = m = len(prompt)
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, 6, owner)
+    pinned = w == "prefix_host"
+    nbytes = s.image_bytes(n)
+    img = (torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) if pinned
+           else torch.empty(nbytes, dtype=torch.uint8, device="cuda"))
+    img.zero_()
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    kv.swap_out([prompt], img, stream=stream)
+    kv.sync(0)
+    extra = {}
+    tf = aqua._csr([fresh])
+    if w == "migrate":
+        back = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        moved = 2 * nbytes
+        def step(timed_evs):
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(stream)
+            kv.migrate(img, back, [0], [0], [nbytes], stream=stream)
+            e1.record(stream)
+            kv.migrate(back, img, [0], [0], [nbytes], stream=stream)
+            e2.record(stream)
+            timed_evs.append((e0, e1, e2))
+    elif w == "layered":
+        groups = [(l0, 8) for l0 in range(0, s.num_layers, 8)]
+        moved = nbytes
+        def step(timed_evs):
+            evs = [torch.cuda.Event(enable_timing=True)]
+            evs[0].record(stream)
+            for l0, nl in groups:
+                kv.swap_in(tf, img, stream=stream, layers=(l0, nl))
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                evs.append(e)
+            timed_evs.append(tuple(evs))
+    else:
+        moved = s.image_bytes(m)
+        def step(timed_evs):
+            e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
+            e0.record(stream)
+            kv.swap_in(tf, img, stream=stream, img_blocks=[n])
+            e1.record(stream)
+            timed_evs.append((e0, e1))
+    warm = []
+    for _ in range(args.warmup):
+        step(warm)
+    kv.sync(0)
+    torch.cuda.synchronize()
+    evs = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(evs)
+    kv.sync(0)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = kv.stats()
+    kv.close()
+    if w == "migrate":
+        d2h = np.mean([a.elapsed_time(b) for a, b, _ in evs])
+        h2d = np.mean([b.elapsed_time(c) for _, b, c in evs])
+        extra = {"hbm_to_host_ms": round(float(d2h), 3), "host_to_hbm_ms": round(float(h2d), 3),
+                 "hbm_to_host_GBps": round(nbytes / d2h / 1e6, 2),
+                 "host_to_hbm_GBps": round(nbytes / h2d / 1e6, 2)}
+        bound, peak, dom_ms, alg = "host_link", HOST_LINK_PEAK_GBS, max(d2h, h2d), nbytes
+    elif w == "layered":
+        first = np.mean([e[0].elapsed_time(e[1]) for e in evs])
+        total = np.mean([e[0].elapsed_time(e[-1]) for e in evs])
+        extra = {"first_group_ms": round(float(first), 3), "all_groups_ms": round(float(total), 3),
+                 "groups": 10, "layers_per_group": 8}
+        bound, peak, dom_ms, alg = "hbm", HBM_PEAK_GBS, total / 10, 2 * nbytes / 10
+    else:
+        ms = np.mean([a.elapsed_time(b) for a, b in evs])
+        extra = {"prefix_tokens": m * s.block_tokens, "cached_tokens": 100000,
+                 "load_ms": round(float(ms), 3)}
+        if pinned:
+            bound, peak, dom_ms, alg = "host_link", HOST_LINK_PEAK_GBS, ms, moved
+        else:
+            bound, peak, dom_ms, alg = "hbm", HBM_PEAK_GBS, ms, 2 * moved
+    achieved = alg / (dom_ms * 1e-3) / 1e9
+    res = dict(res_common)
+    res.update({
+        "value": round(moved * args.steps / wall / 1e9, 2),
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "dtype": wl.DTYPE_NAME[s.dtype],
+        "config": {"workload": WORKLOADS[w], "layers": s.num_layers, "kv_heads": s.num_kv_heads,
+                   "head_dim": s.head_dim, "block_tokens": s.block_tokens,
+                   "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
+                   "image_blocks": n, "moved_bytes_per_step": moved,
+                   "parallelism": "single_gpu"},
+        "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": alg},
+        "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"] +
+                                                       st["calls_migrate"]) / 1e3, 2),
+        "kernel_source": _kernel_hash(),
+    })
+    res.update(extra)
+    return res, s
+
+
+def ceil_div_tokens(tokens, block_tokens):
+    return -(-tokens // block_tokens)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -445,6 +580,8 @@ def main():
     }
     if args.workload == "cycle":
         res, shape = run_cycle(args, common)
+    elif args.workload in ("prefix", "prefix_host", "layered", "migrate"):
+        res, shape = run_next(args, common)
     else:
         res, shape = run_pair(args, common)
     if not args.no_cpu_baseline:

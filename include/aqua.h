@@ -107,6 +107,8 @@ typedef struct {
     uint64_t descriptors;                 /* run descriptors launched */
     uint64_t waits_inserted;              /* cross-stream waits enqueued */
     uint64_t waits_elided;                /* conflicts already complete */
+    uint64_t calls_migrate;               /* successful migrations */
+    uint64_t bytes_migrated;
     uint64_t host_ns;                     /* host time in swap calls, not
                                              counting wait_ns */
     uint64_t wait_ns;                     /* host time blocked inside swap
@@ -158,6 +160,65 @@ AQUA_API aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs,
                          const uint64_t* seq_offsets, const void* src,
                          uint64_t src_bytes, const uint64_t* img_offsets,
                          int32_t target, void* stream, uint64_t* ticket);
+
+/* Which part of each image a call moves.
+ *   img_blocks  NULL, or per sequence the image's blocks per layer m_s, at
+ *               least its table length n_s: the image is [L][m_s][C] and the
+ *               table covers its first n_s blocks of every layer.  Used to
+ *               swap a cached prefix in from a longer image (the paper's
+ *               prefill caching keeps a long prompt's context in swap space
+ *               and reloads it for later prompts sharing the prefix,
+ *               sections 8 and 9.3).  Packed images are then sum L*m_q*C
+ *               apart and capacity checks use m_s.
+ *   first_layer, num_layers
+ *               move only layers [first_layer, first_layer + num_layers) of
+ *               pool and image; num_layers 0 (with first_layer 0) moves all.
+ *               Used for layer-by-layer offload as in FlexGen (section 9.1)
+ *               and to pipeline a swap-in: one call, and one ticket, per
+ *               layer group.
+ * Ordering is tracked at the granularity of whole blocks and whole image
+ * extents. */
+typedef struct {
+    const uint64_t* img_blocks;
+    uint32_t first_layer;
+    uint32_t num_layers;
+} aqua_swap_range;
+
+/* aqua_swap_out / aqua_swap_in with a range (NULL: the whole images).
+ * AQUA_ERR_INVALID when m_s < n_s or the layer range leaves [0, L). */
+AQUA_API aqua_status aqua_swap_out_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
+                                      const int32_t* block_ids,
+                                      const uint64_t* seq_offsets, void* dst,
+                                      uint64_t dst_bytes, const uint64_t* img_offsets,
+                                      const aqua_swap_range* range, int32_t target,
+                                      void* stream, uint64_t* ticket);
+AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
+                                     const int32_t* block_ids,
+                                     const uint64_t* seq_offsets, const void* src,
+                                     uint64_t src_bytes, const uint64_t* img_offsets,
+                                     const aqua_swap_range* range, int32_t target,
+                                     void* stream, uint64_t* ticket);
+
+/* Image migration.  When the memory holding offloaded images is reclaimed
+ * (section 6, "Reclaiming Aqua Tensors"), the images move elsewhere -- here
+ * between the HBM region and pinned host memory, in either direction, or
+ * within one kind -- and later swap-ins read them from the new place.
+ * Copies n byte ranges: range k from src + src_offsets[k] to
+ * dst + dst_offsets[k], lengths[k] bytes.
+ *   src, dst       device (target DEVICE) or pinned host (target HOST)
+ *                  pointers, 16-byte aligned, with src_bytes / dst_bytes
+ *                  usable.
+ *   offsets, lengths  host arrays of n entries, multiples of 16.
+ * Destination ranges must not overlap each other or any source range
+ * (AQUA_ERR_DUPLICATE); ranges must fit their buffers (AQUA_ERR_CAPACITY).
+ * Ordered with the pool's swaps like any call that reads the source ranges
+ * and writes the destination ranges.  Uses the range-copy kernel (capped
+ * like zero-copy swaps when either side is host memory). */
+AQUA_API aqua_status aqua_migrate(aqua_kv_pool_t pool, const void* src, uint64_t src_bytes,
+                                  int32_t src_target, void* dst, uint64_t dst_bytes,
+                                  int32_t dst_target, uint32_t n,
+                                  const uint64_t* src_offsets, const uint64_t* dst_offsets,
+                                  const uint64_t* lengths, void* stream, uint64_t* ticket);
 
 /* Block the host until `ticket` (0: every outstanding call) has completed.
  * Returns AQUA_ERR_HIP if a HIP failure was latched. */

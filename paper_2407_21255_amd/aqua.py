@@ -35,7 +35,8 @@ AQUA_HOST_ZERO_COPY, AQUA_HOST_STAGED = 0, 1
 
 EXPORTS = (
     "aqua_kv_pool_create", "aqua_kv_pool_destroy", "aqua_swap_out",
-    "aqua_swap_in", "aqua_sync", "aqua_stream_wait", "aqua_query",
+    "aqua_swap_in", "aqua_swap_out_ex", "aqua_swap_in_ex", "aqua_migrate",
+    "aqua_sync", "aqua_stream_wait", "aqua_query",
     "aqua_kv_pool_set_max_workgroups", "aqua_kv_pool_set_host_path",
     "aqua_pool_stats_get", "aqua_status_str",
 )
@@ -52,10 +53,19 @@ class aqua_kv_desc(ctypes.Structure):
     ]
 
 
+class aqua_swap_range(ctypes.Structure):
+    _fields_ = [
+        ("img_blocks", ctypes.c_void_p),
+        ("first_layer", ctypes.c_uint32),
+        ("num_layers", ctypes.c_uint32),
+    ]
+
+
 class aqua_pool_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "calls_out", "calls_in", "bytes_out", "bytes_in", "bytes_host",
-        "descriptors", "waits_inserted", "waits_elided", "host_ns", "wait_ns")] + [
+        "descriptors", "waits_inserted", "waits_elided", "calls_migrate",
+        "bytes_migrated", "host_ns", "wait_ns")] + [
         ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
@@ -84,6 +94,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_kv_pool_destroy.argtypes = [P]
     L.aqua_swap_out.argtypes = [P, u32, P, P, P, u64, P, i32, P, ctypes.POINTER(u64)]
     L.aqua_swap_in.argtypes = [P, u32, P, P, P, u64, P, i32, P, ctypes.POINTER(u64)]
+    R = ctypes.POINTER(aqua_swap_range)
+    L.aqua_swap_out_ex.argtypes = [P, u32, P, P, P, u64, P, R, i32, P, ctypes.POINTER(u64)]
+    L.aqua_swap_in_ex.argtypes = [P, u32, P, P, P, u64, P, R, i32, P, ctypes.POINTER(u64)]
+    L.aqua_migrate.argtypes = [P, P, u64, i32, P, u64, i32, u32, P, P, P, P,
+                               ctypes.POINTER(u64)]
     L.aqua_sync.argtypes = [P, u64]
     L.aqua_stream_wait.argtypes = [P, u64, P]
     L.aqua_query.argtypes = [P, u64]
@@ -125,6 +140,30 @@ def aqua_swap_in(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
     t = ctypes.c_uint64(0)
     st = load().aqua_swap_in(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
                              img_offsets, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_out_ex(pool, num_seqs, block_ids, seq_offsets, dst, dst_bytes,
+                     img_offsets, rng, target, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_out_ex(pool, num_seqs, block_ids, seq_offsets, dst, dst_bytes,
+                                 img_offsets, rng, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_in_ex(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
+                    img_offsets, rng, target, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_in_ex(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
+                                img_offsets, rng, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_migrate(pool, src, src_bytes, src_target, dst, dst_bytes, dst_target, n,
+                 src_offsets, dst_offsets, lengths, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_migrate(pool, src, src_bytes, src_target, dst, dst_bytes, dst_target, n,
+                             src_offsets, dst_offsets, lengths, stream, ctypes.byref(t))
     return st, t.value
 
 
@@ -205,29 +244,52 @@ class KVPool:
             raise AquaError(st, "aqua_kv_pool_create")
         self.handle = h
 
-    def _swap(self, fn, name, tables, buf, img_offsets, stream, target):
+    def _swap(self, is_in, tables, buf, img_offsets, stream, target, img_blocks, layers):
         ids, offs = _csr(tables)
         io = None
         if img_offsets is not None:
             io = np.ascontiguousarray(img_offsets, dtype=np.uint64)
         tgt = _target_of(buf) if target is None else target
-        st, ticket = fn(self.handle, len(offs) - 1, ids.ctypes.data, offs.ctypes.data,
-                        buf.data_ptr(), buf.numel() * buf.element_size(),
-                        None if io is None else io.ctypes.data, tgt,
-                        _stream_handle(stream))
+        args = (self.handle, len(offs) - 1, ids.ctypes.data, offs.ctypes.data,
+                buf.data_ptr(), buf.numel() * buf.element_size(),
+                None if io is None else io.ctypes.data)
+        if img_blocks is None and layers is None:
+            fn, name = (aqua_swap_in, "aqua_swap_in") if is_in else (aqua_swap_out, "aqua_swap_out")
+            st, ticket = fn(*args, tgt, _stream_handle(stream))
+        else:
+            ib = None if img_blocks is None else np.ascontiguousarray(img_blocks, dtype=np.uint64)
+            l0, nl = (0, 0) if layers is None else layers
+            rng = aqua_swap_range(None if ib is None else ib.ctypes.data, l0, nl)
+            fn, name = ((aqua_swap_in_ex, "aqua_swap_in_ex") if is_in
+                        else (aqua_swap_out_ex, "aqua_swap_out_ex"))
+            st, ticket = fn(*args, ctypes.byref(rng), tgt, _stream_handle(stream))
         if st != AQUA_OK:
             raise AquaError(st, name)
         return ticket
 
     def swap_out(self, tables, dst: torch.Tensor, img_offsets=None, stream=None,
-                 target=None) -> int:
-        return self._swap(aqua_swap_out, "aqua_swap_out", tables, dst, img_offsets,
-                          stream, target)
+                 target=None, img_blocks=None, layers=None) -> int:
+        """Gather; ``img_blocks`` (blocks per layer of each image) and
+        ``layers`` = (first, count) select the extended form."""
+        return self._swap(False, tables, dst, img_offsets, stream, target, img_blocks, layers)
 
     def swap_in(self, tables, src: torch.Tensor, img_offsets=None, stream=None,
-                target=None) -> int:
-        return self._swap(aqua_swap_in, "aqua_swap_in", tables, src, img_offsets,
-                          stream, target)
+                target=None, img_blocks=None, layers=None) -> int:
+        return self._swap(True, tables, src, img_offsets, stream, target, img_blocks, layers)
+
+    def migrate(self, src: torch.Tensor, dst: torch.Tensor, src_offsets, dst_offsets,
+                lengths, stream=None) -> int:
+        """Copy byte ranges between offload buffers (device or pinned host)."""
+        so, do, ln = (np.ascontiguousarray(x, dtype=np.uint64)
+                      for x in (src_offsets, dst_offsets, lengths))
+        st, ticket = aqua_migrate(self.handle, src.data_ptr(), src.numel() * src.element_size(),
+                                  _target_of(src), dst.data_ptr(),
+                                  dst.numel() * dst.element_size(), _target_of(dst), len(ln),
+                                  so.ctypes.data, do.ctypes.data, ln.ctypes.data,
+                                  _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_migrate")
+        return ticket
 
     def sync(self, ticket: int = 0) -> None:
         st = aqua_sync(self.handle, ticket)

@@ -55,9 +55,10 @@ struct RingUse {
 };
 
 // One sequence of a staged call: image offset in the caller's buffer, its
-// first entry in the concatenated table, and its table length.
+// first entry in the concatenated table, its table length and its image's
+// blocks per layer.
 struct StagedSeq {
-    uint64_t off, first, n;
+    uint64_t off, first, n, m;
 };
 
 }  // namespace
@@ -352,11 +353,34 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
 // Swap-in: the copy stream fills a slot from the host image, then the
 // scatter drains it on the call's stream.  A slot is refilled only after
 // its previous user has finished with it.
+// Moves sequence q's layers [l0, l0 + nl) between a slot and the host image
+// on the copy stream: one copy when the image holds exactly the table's
+// blocks, else one per layer (only the first n of its m blocks).
+hipError_t stage_copies(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t* slot,
+                        uint32_t G, uint32_t l0, uint32_t nl) {
+    const uint64_t C = p->shape.C;
+    for (const StagedSeq& q : p->sseq) {
+        uint8_t* s = slot + G * q.first * C;
+        uint8_t* h = (uint8_t*)const_cast<void*>(buf) + q.off;
+        const uint32_t pieces = q.m == q.n ? 1 : nl;
+        const uint64_t bytes = q.m == q.n ? nl * q.n * C : q.n * C;
+        for (uint32_t j = 0; j < pieces; ++j) {
+            const uint64_t l = l0 + j;
+            uint8_t* hj = h + l * q.m * C;
+            uint8_t* sj = s + (uint64_t)j * q.n * C;
+            const hipError_t e =
+                to_host ? hipMemcpyAsync(hj, sj, bytes, hipMemcpyDeviceToHost, p->copy)
+                        : hipMemcpyAsync(sj, hj, bytes, hipMemcpyHostToDevice, p->copy);
+            if (e != hipSuccess) return e;
+        }
+    }
+    return hipSuccess;
+}
+
 aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStream_t stream,
                            const RunDesc* descs, uint32_t ndesc, uint64_t slot, uint32_t G,
-                           Outstanding* rec) {
-    const uint64_t C = p->shape.C;
-    const uint32_t L = p->shape.L;
+                           uint32_t l_begin, uint32_t l_end, Outstanding* rec) {
+    const uint32_t L = l_end;
     hipError_t e = hipSuccess;
     auto ev = [&](hipEvent_t* x) -> hipError_t {
         hipError_t r = take_event(p, x);
@@ -372,7 +396,7 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
 
     hipEvent_t slot_free[2] = {nullptr, nullptr};
     hipEvent_t last_copy = nullptr;
-    for (uint32_t l0 = 0, k = 0; l0 < L; l0 += G, ++k) {
+    for (uint32_t l0 = l_begin, k = 0; l0 < L; l0 += G, ++k) {
         const uint32_t nl = std::min<uint32_t>(G, L - l0);
         uint8_t* s = p->staging + (k % 2) * slot;
         // The kernels only touch HBM here: no host-link grid cap.
@@ -387,11 +411,7 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
         if (slot_free[k % 2] && (e = hipStreamWaitEvent(first, slot_free[k % 2], 0)))
             return latch(p, e);
         if (is_in) {
-            for (const StagedSeq& q : p->sseq) {
-                e = hipMemcpyAsync(s + G * q.first * C, (const uint8_t*)buf + q.off + l0 * q.n * C,
-                                   nl * q.n * C, hipMemcpyHostToDevice, p->copy);
-                if (e != hipSuccess) return latch(p, e);
-            }
+            if ((e = stage_copies(p, false, buf, s, G, l0, nl)) != hipSuccess) return latch(p, e);
         } else {
             (void)hipGetLastError();
             if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
@@ -402,12 +422,7 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
             (void)hipGetLastError();
             if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
         } else {
-            for (const StagedSeq& q : p->sseq) {
-                e = hipMemcpyAsync((uint8_t*)const_cast<void*>(buf) + q.off + l0 * q.n * C,
-                                   s + G * q.first * C, nl * q.n * C, hipMemcpyDeviceToHost,
-                                   p->copy);
-                if (e != hipSuccess) return latch(p, e);
-            }
+            if ((e = stage_copies(p, true, buf, s, G, l0, nl)) != hipSuccess) return latch(p, e);
         }
         if ((e = hipEventRecord(e2, second)) != hipSuccess) return latch(p, e);
         slot_free[k % 2] = e2;
@@ -422,7 +437,8 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
 aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                     const int32_t* ids, const uint64_t* offs, const void* buf,
                     uint64_t buf_bytes, const uint64_t* img_offsets,
-                    int32_t target, void* stream_ptr, uint64_t* ticket_out) {
+                    const aqua_swap_range* range, int32_t target, void* stream_ptr,
+                    uint64_t* ticket_out) {
     if (!p) return AQUA_ERR_INVALID;
     if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
     const auto t0 = std::chrono::steady_clock::now();
@@ -435,6 +451,11 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     a.buf = (uintptr_t)buf;
     a.buf_bytes = buf_bytes;
     a.is_in = is_in;
+    if (range) {
+        a.img_blocks = range->img_blocks;
+        a.first_layer = range->first_layer;
+        a.num_layers = range->num_layers;
+    }
     aqua_status st = (target == AQUA_TARGET_DEVICE || target == AQUA_TARGET_HOST)
                          ? aqua::validate_call(p->shape, a, p->marks)
                          : AQUA_ERR_INVALID;
@@ -461,6 +482,8 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     const uint32_t lane = lane_for(p, stream);
     const uint64_t ticket = p->next_ticket;
     const bool staged = target == AQUA_TARGET_HOST && p->host_path == AQUA_HOST_STAGED && total;
+    const uint32_t l_begin = a.first_layer;
+    const uint32_t l_count = a.num_layers ? a.num_layers : p->shape.L;
 
     // Plan.  The staged path plans the concatenated table as one packed
     // sequence (its layout in the HBM slots).
@@ -469,7 +492,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     uint32_t G = 0;
     if (staged) {
         const uint64_t per_layer = total * p->shape.C;
-        G = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(p->shape.L, p->slot_target / per_layer));
+        G = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(l_count, p->slot_target / per_layer));
         slot = (uint64_t)G * per_layer;
         // Descriptors for the slot layout: sequence s at G * first_s * C.
         p->sseq.clear();
@@ -477,10 +500,13 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         for (uint32_t k = 0; k < num_seqs; ++k) {
             p->slot_offsets[k] = (uint64_t)G * offs[k] * p->shape.C;
             if (offs[k + 1] > offs[k])
-                p->sseq.push_back({aqua::image_offset(p->shape, a, k), offs[k], offs[k + 1] - offs[k]});
+                p->sseq.push_back({aqua::image_offset(p->shape, a, k), offs[k],
+                                   offs[k + 1] - offs[k], aqua::image_blocks(a, k)});
         }
+        // Slot images are dense: [G][n_s][C].
         aqua::CallArgs c = a;
         c.img_offsets = p->slot_offsets.data();
+        c.img_blocks = nullptr;
         aqua::plan_runs(p->shape, c, p->unit_bytes, &p->plan);
         st = ensure_staging(p, 2 * slot);
         if (st != AQUA_OK) return st;
@@ -567,12 +593,15 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         if (e != hipSuccess) return latch(p, e);
         if (staged) {
             st = enqueue_staged(p, is_in, buf, stream, reinterpret_cast<const RunDesc*>(descs),
-                                (uint32_t)p->plan.size(), slot, G, &rec);
+                                (uint32_t)p->plan.size(), slot, G, l_begin, l_begin + l_count,
+                                &rec);
             if (st != AQUA_OK) return st;
         } else {
-            const aqua::SwapLaunch L =
+            aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
                             (uint32_t)p->plan.size(), target);
+            L.first_layer = l_begin;
+            L.num_layers = l_count;
             (void)hipGetLastError();
             e = aqua::launch_swap(L, stream);
             if (e != hipSuccess) return latch(p, e);
@@ -585,7 +614,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     p->outstanding[lane].push_back(std::move(rec));
     if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
 
-    const uint64_t moved = (uint64_t)p->shape.L * total * p->shape.C;
+    const uint64_t moved = (uint64_t)l_count * total * p->shape.C;
     if (is_in) {
         p->stats.calls_in++;
         p->stats.bytes_in += moved;
@@ -600,6 +629,112 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                                   .count();
     // Reserving descriptor space blocks only when the ring is full; that
     // back-pressure is reported apart from the call's own host work.
+    p->stats.wait_ns += waited_ns;
+    p->stats.host_ns += total_ns > waited_ns ? total_ns - waited_ns : 0;
+    if (ticket_out) *ticket_out = ticket;
+    return AQUA_OK;
+}
+
+aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int32_t src_target,
+                       void* dst, uint64_t dst_bytes, int32_t dst_target, uint32_t n,
+                       const uint64_t* so, const uint64_t* dof, const uint64_t* len,
+                       void* stream_ptr, uint64_t* ticket_out) {
+    if (!p) return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
+    const auto t0 = std::chrono::steady_clock::now();
+    auto valid_target = [](int32_t t) {
+        return t == AQUA_TARGET_DEVICE || t == AQUA_TARGET_HOST;
+    };
+    aqua_status st = (valid_target(src_target) && valid_target(dst_target))
+                         ? aqua::validate_migrate((uintptr_t)src, src_bytes, (uintptr_t)dst,
+                                                  dst_bytes, n, so, dof, len)
+                         : AQUA_ERR_INVALID;
+    if (st == AQUA_ERR_INVALID) return st;
+    uint64_t moved = 0;
+    for (uint32_t k = 0; k < n; ++k) moved += len[k];
+
+    DeviceGuard dg(p->device);
+    if (!dg.ok) {
+        (void)hipGetLastError();
+        return AQUA_ERR_HIP;
+    }
+    uint8_t* dsrc = nullptr;
+    uint8_t* ddst = nullptr;
+    if (moved) {
+        aqua_status pc = resolve_buffer(p, src, src_bytes, src_target, &dsrc);
+        if (pc == AQUA_OK) pc = resolve_buffer(p, dst, dst_bytes, dst_target, &ddst);
+        if (pc != AQUA_OK) return pc;
+    }
+    if (st != AQUA_OK) return st;
+
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    st = poll(p);
+    if (st != AQUA_OK) return st;
+    const uint32_t lane = lane_for(p, stream);
+    const uint64_t ticket = p->next_ticket;
+
+    std::vector<aqua::CopyDesc> pieces;
+    aqua::plan_copies(n, so, dof, len, kDefaultUnitBytes, &pieces);
+    p->ranges.clear();
+    std::vector<std::pair<uint64_t, uint64_t>> wr;
+    for (uint32_t k = 0; k < n; ++k) {
+        if (!len[k]) continue;
+        p->ranges.emplace_back((uint64_t)(uintptr_t)src + so[k], (uint64_t)(uintptr_t)src + so[k] + len[k]);
+        wr.emplace_back((uint64_t)(uintptr_t)dst + dof[k], (uint64_t)(uintptr_t)dst + dof[k] + len[k]);
+    }
+    uint64_t ring_off = 0;
+    const uint64_t dbytes = pieces.size() * sizeof(aqua::CopyDesc);
+    uint64_t waited_ns = 0;
+    if (dbytes) {
+        const auto w0 = std::chrono::steady_clock::now();
+        st = ring_reserve(p, dbytes, &ring_off);
+        waited_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                        std::chrono::steady_clock::now() - w0)
+                        .count();
+        if (st != AQUA_OK) return st;
+    }
+    HazardTracker::Access acc;
+    acc.ranges_read = p->ranges.data();
+    acc.n_ranges_read = p->ranges.size();
+    acc.ranges_written = wr.data();
+    acc.n_ranges_written = wr.size();
+    p->stats.waits_elided += p->tracker.issue(ticket, lane, acc, &p->deps);
+    p->next_ticket++;
+    for (const HazardTracker::Dep& d : p->deps) {
+        hipEvent_t ev = event_of(p, d.ticket);
+        if (!ev) continue;
+        const hipError_t e = hipStreamWaitEvent(stream, ev, 0);
+        if (e != hipSuccess) return latch(p, e);
+        p->stats.waits_inserted++;
+    }
+    Outstanding rec{ticket, nullptr, {}};
+    if (dbytes) {
+        // Descriptors go to the device ring: a migration touching host
+        // memory keeps the link busy.
+        std::memcpy(p->ring_host + ring_off, pieces.data(), dbytes);
+        hipError_t e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
+                                      hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return latch(p, e);
+        const bool host_side = src_target == AQUA_TARGET_HOST || dst_target == AQUA_TARGET_HOST;
+        (void)hipGetLastError();
+        e = aqua::launch_copy(dsrc, ddst,
+                              reinterpret_cast<const aqua::CopyDesc*>(p->ring_dev + ring_off),
+                              (uint32_t)pieces.size(),
+                              host_side ? p->max_wg[AQUA_TARGET_HOST] : p->max_wg[AQUA_TARGET_DEVICE],
+                              stream);
+        if (e != hipSuccess) return latch(p, e);
+    }
+    hipError_t e = take_event(p, &rec.ev);
+    if (e == hipSuccess) e = hipEventRecord(rec.ev, stream);
+    if (e != hipSuccess) return latch(p, e);
+    p->outstanding[lane].push_back(std::move(rec));
+    if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
+    p->stats.calls_migrate++;
+    p->stats.bytes_migrated += moved;
+    if (src_target == AQUA_TARGET_HOST || dst_target == AQUA_TARGET_HOST) p->stats.bytes_host += moved;
+    const uint64_t total_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                                  std::chrono::steady_clock::now() - t0)
+                                  .count();
     p->stats.wait_ns += waited_ns;
     p->stats.host_ns += total_ns > waited_ns ? total_ns - waited_ns : 0;
     if (ticket_out) *ticket_out = ticket;
@@ -696,7 +831,7 @@ aqua_status aqua_swap_out(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t*
                           const uint64_t* img_offsets, int32_t target, void* stream,
                           uint64_t* ticket) {
     return do_swap(pool, false, num_seqs, block_ids, seq_offsets, dst, dst_bytes, img_offsets,
-                   target, stream, ticket);
+                   nullptr, target, stream, ticket);
 }
 
 aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* block_ids,
@@ -704,7 +839,31 @@ aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* 
                          const uint64_t* img_offsets, int32_t target, void* stream,
                          uint64_t* ticket) {
     return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
-                   target, stream, ticket);
+                   nullptr, target, stream, ticket);
+}
+
+aqua_status aqua_swap_out_ex(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* block_ids,
+                             const uint64_t* seq_offsets, void* dst, uint64_t dst_bytes,
+                             const uint64_t* img_offsets, const aqua_swap_range* range,
+                             int32_t target, void* stream, uint64_t* ticket) {
+    return do_swap(pool, false, num_seqs, block_ids, seq_offsets, dst, dst_bytes, img_offsets,
+                   range, target, stream, ticket);
+}
+
+aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* block_ids,
+                            const uint64_t* seq_offsets, const void* src, uint64_t src_bytes,
+                            const uint64_t* img_offsets, const aqua_swap_range* range,
+                            int32_t target, void* stream, uint64_t* ticket) {
+    return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
+                   range, target, stream, ticket);
+}
+
+aqua_status aqua_migrate(aqua_kv_pool_t pool, const void* src, uint64_t src_bytes,
+                         int32_t src_target, void* dst, uint64_t dst_bytes, int32_t dst_target,
+                         uint32_t n, const uint64_t* src_offsets, const uint64_t* dst_offsets,
+                         const uint64_t* lengths, void* stream, uint64_t* ticket) {
+    return do_migrate(pool, src, src_bytes, src_target, dst, dst_bytes, dst_target, n,
+                      src_offsets, dst_offsets, lengths, stream, ticket);
 }
 
 aqua_status aqua_sync(aqua_kv_pool_t p, uint64_t ticket) {

@@ -51,10 +51,17 @@ aqua_status make_shape(const aqua_kv_desc* d, Shape* out) {
     return AQUA_OK;
 }
 
+uint64_t image_blocks(const CallArgs& a, uint32_t k) {
+    return a.img_blocks ? a.img_blocks[k] : a.offs[k + 1] - a.offs[k];
+}
+
 uint64_t image_offset(const Shape& s, const CallArgs& a, uint32_t k) {
     if (a.img_offsets) return a.img_offsets[k];
     // Packed: images one after another in sequence order.
-    return (uint64_t)s.L * a.offs[k] * s.C;
+    if (!a.img_blocks) return (uint64_t)s.L * a.offs[k] * s.C;
+    uint64_t off = 0;
+    for (uint32_t q = 0; q < k; ++q) off += (uint64_t)s.L * a.img_blocks[q] * s.C;
+    return off;
 }
 
 aqua_status validate_call(const Shape& s, const CallArgs& a, DupMarks& marks) {
@@ -71,6 +78,12 @@ aqua_status validate_call(const Shape& s, const CallArgs& a, DupMarks& marks) {
     if (a.img_offsets)
         for (uint32_t k = 0; k < a.num_seqs; ++k)
             if (a.img_offsets[k] % 16) return AQUA_ERR_INVALID;
+    if (a.img_blocks)
+        for (uint32_t k = 0; k < a.num_seqs; ++k)
+            if (a.img_blocks[k] < a.offs[k + 1] - a.offs[k]) return AQUA_ERR_INVALID;
+    if (a.num_layers == 0 ? a.first_layer != 0
+                          : (uint64_t)a.first_layer + a.num_layers > s.L)
+        return AQUA_ERR_INVALID;
 
     // -- range
     for (uint64_t j = 0; j < total; ++j)
@@ -101,13 +114,14 @@ aqua_status validate_call(const Shape& s, const CallArgs& a, DupMarks& marks) {
     }
 
     // -- capacity (128-bit so that absurd tables cannot wrap around)
+    unsigned __int128 packed = 0;
     for (uint32_t k = 0; k < a.num_seqs; ++k) {
-        const uint64_t n = a.offs[k + 1] - a.offs[k];
-        if (!n) continue;
+        const uint64_t m = image_blocks(a, k);
+        const unsigned __int128 len = (unsigned __int128)s.L * m * s.C;
         const unsigned __int128 off =
-            a.img_offsets ? (unsigned __int128)a.img_offsets[k]
-                          : (unsigned __int128)s.L * a.offs[k] * s.C;
-        const unsigned __int128 len = (unsigned __int128)s.L * n * s.C;
+            a.img_offsets ? (unsigned __int128)a.img_offsets[k] : packed;
+        packed += len;
+        if (a.offs[k + 1] == a.offs[k]) continue;
         if (off + len > a.buf_bytes) return AQUA_ERR_CAPACITY;
     }
     return AQUA_OK;
@@ -117,10 +131,9 @@ void image_ranges(const Shape& s, const CallArgs& a,
                   std::vector<std::pair<uint64_t, uint64_t>>* out) {
     out->clear();
     for (uint32_t k = 0; k < a.num_seqs; ++k) {
-        const uint64_t n = a.offs[k + 1] - a.offs[k];
-        if (!n) continue;
+        if (a.offs[k + 1] == a.offs[k]) continue;
         const uint64_t lo = image_offset(s, a, k);
-        out->emplace_back(lo, lo + (uint64_t)s.L * n * s.C);
+        out->emplace_back(lo, lo + (uint64_t)s.L * image_blocks(a, k) * s.C);
     }
 }
 
@@ -133,7 +146,7 @@ size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
         if (!n) continue;
         const int32_t* bt = a.ids + first;
         const uint64_t base = image_offset(s, a, k);
-        const uint64_t lstride = n * s.C;
+        const uint64_t lstride = image_blocks(a, k) * s.C;
         uint64_t i = 0;
         while (i < n) {
             uint64_t len = 1;
@@ -150,6 +163,51 @@ size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
             i += len;
         }
     }
+    return out->size() - before;
+}
+
+aqua_status validate_migrate(uintptr_t src, uint64_t src_bytes, uintptr_t dst,
+                             uint64_t dst_bytes, uint32_t n, const uint64_t* src_off,
+                             const uint64_t* dst_off, const uint64_t* len) {
+    if (n && (!src || !dst || !src_off || !dst_off || !len)) return AQUA_ERR_INVALID;
+    if (src % 16 || dst % 16) return AQUA_ERR_INVALID;
+    for (uint32_t k = 0; k < n; ++k)
+        if (src_off[k] % 16 || dst_off[k] % 16 || len[k] % 16) return AQUA_ERR_INVALID;
+    // Overlaps, as address intervals (sorted sweep would do; n is small).
+    for (uint32_t k = 0; k < n; ++k) {
+        if (!len[k]) continue;
+        const unsigned __int128 d0 = (unsigned __int128)dst + dst_off[k], d1 = d0 + len[k];
+        for (uint32_t q = 0; q < n; ++q) {
+            if (!len[q]) continue;
+            const unsigned __int128 s0 = (unsigned __int128)src + src_off[q], s1 = s0 + len[q];
+            if (d0 < s1 && s0 < d1) return AQUA_ERR_DUPLICATE;
+            if (q > k) {
+                const unsigned __int128 e0 = (unsigned __int128)dst + dst_off[q],
+                                        e1 = e0 + len[q];
+                if (d0 < e1 && e0 < d1) return AQUA_ERR_DUPLICATE;
+            }
+        }
+    }
+    for (uint32_t k = 0; k < n; ++k) {
+        if ((unsigned __int128)src_off[k] + len[k] > src_bytes) return AQUA_ERR_CAPACITY;
+        if ((unsigned __int128)dst_off[k] + len[k] > dst_bytes) return AQUA_ERR_CAPACITY;
+    }
+    return AQUA_OK;
+}
+
+size_t plan_copies(uint32_t n, const uint64_t* src_off, const uint64_t* dst_off,
+                   const uint64_t* len, uint64_t unit, std::vector<CopyDesc>* out) {
+    const size_t before = out->size();
+    unit = std::max<uint64_t>(16, unit & ~15ull);
+    for (uint32_t k = 0; k < n; ++k)
+        for (uint64_t o = 0; o < len[k]; o += unit) {
+            CopyDesc d;
+            d.src_off = src_off[k] + o;
+            d.dst_off = dst_off[k] + o;
+            d.len = std::min<uint64_t>(unit, len[k] - o);
+            d.reserved = 0;
+            out->push_back(d);
+        }
     return out->size() - before;
 }
 

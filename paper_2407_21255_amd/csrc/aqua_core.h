@@ -38,7 +38,42 @@ struct CallArgs {
     uintptr_t buf = 0;                     // offload buffer address
     uint64_t buf_bytes = 0;
     bool is_in = false;                    // swap-in: destinations are blocks
+    // Blocks per layer of each image (>= its table length; the table covers
+    // the first blocks of every layer).  nullptr: the table lengths.
+    const uint64_t* img_blocks = nullptr;
+    // Layers moved: [first_layer, first_layer + num_layers); 0 layers with
+    // first_layer 0 means every layer.
+    uint32_t first_layer = 0;
+    uint32_t num_layers = 0;
 };
+
+// Blocks per layer of sequence k's image.
+uint64_t image_blocks(const CallArgs& a, uint32_t k);
+
+// One range of a migration: len bytes from src_off to dst_off.
+struct CopyRange {
+    uint64_t src_off, dst_off, len;
+};
+
+// Migration validation: offsets and lengths multiples of 16, ranges inside
+// their buffers, destination ranges disjoint from each other and from every
+// source range (as addresses).  Same codes and precedence as the oracle.
+aqua_status validate_migrate(uintptr_t src, uint64_t src_bytes, uintptr_t dst,
+                             uint64_t dst_bytes, uint32_t n, const uint64_t* src_off,
+                             const uint64_t* dst_off, const uint64_t* len);
+
+// Work item of the range-copy kernel: at most `unit` bytes each.
+struct alignas(16) CopyDesc {
+    uint64_t src_off;
+    uint64_t dst_off;
+    uint64_t len;
+    uint64_t reserved;
+};
+static_assert(sizeof(CopyDesc) == 32, "descriptor layout is shared with the kernels");
+
+// Splits the ranges into pieces of at most `unit` bytes.
+size_t plan_copies(uint32_t n, const uint64_t* src_off, const uint64_t* dst_off,
+                   const uint64_t* len, uint64_t unit, std::vector<CopyDesc>* out);
 
 // Work item of the copy kernels: a run of `nchunks` consecutive pool blocks
 // starting at `block` whose image chunks are also consecutive.  In layer l

@@ -28,8 +28,58 @@ aqua_status aqua_core_validate(const aqua_kv_desc* desc, uint32_t num_seqs,
     return aqua::validate_call(s, a, marks);
 }
 
+aqua_status aqua_core_validate_ex(const aqua_kv_desc* desc, uint32_t num_seqs,
+                                  const int32_t* ids, const uint64_t* offs,
+                                  uint64_t buf_addr, uint64_t buf_bytes,
+                                  const uint64_t* img_offsets, const uint64_t* img_blocks,
+                                  uint32_t first_layer, uint32_t num_layers, int32_t is_in) {
+    aqua::Shape s;
+    aqua_status st = aqua::make_shape(desc, &s);
+    if (st != AQUA_OK) return st;
+    aqua::CallArgs a;
+    a.num_seqs = num_seqs;
+    a.ids = ids;
+    a.offs = offs;
+    a.img_offsets = img_offsets;
+    a.img_blocks = img_blocks;
+    a.first_layer = first_layer;
+    a.num_layers = num_layers;
+    a.buf = (uintptr_t)buf_addr;
+    a.buf_bytes = buf_bytes;
+    a.is_in = is_in != 0;
+    aqua::DupMarks marks;
+    return aqua::validate_call(s, a, marks);
+}
+
+aqua_status aqua_core_validate_migrate(uint64_t src, uint64_t src_bytes, uint64_t dst,
+                                       uint64_t dst_bytes, uint32_t n, const uint64_t* so,
+                                       const uint64_t* dof, const uint64_t* len) {
+    return aqua::validate_migrate((uintptr_t)src, src_bytes, (uintptr_t)dst, dst_bytes, n, so,
+                                  dof, len);
+}
+
 // Writes up to max_out descriptors (32 bytes each) and returns how many the
 // plan has; negative status for an invalid shape.
+int64_t aqua_core_plan_ex(const aqua_kv_desc* desc, uint32_t num_seqs,
+                          const int32_t* ids, const uint64_t* offs,
+                          const uint64_t* img_offsets, const uint64_t* img_blocks,
+                          uint64_t unit_bytes, void* out, uint64_t max_out) {
+    aqua::Shape s;
+    aqua_status st = aqua::make_shape(desc, &s);
+    if (st != AQUA_OK) return st;
+    aqua::CallArgs a;
+    a.num_seqs = num_seqs;
+    a.ids = ids;
+    a.offs = offs;
+    a.img_offsets = img_offsets;
+    a.img_blocks = img_blocks;
+    std::vector<aqua::RunDesc> plan;
+    aqua::plan_runs(s, a, unit_bytes, &plan);
+    const uint64_t n = plan.size() < max_out ? plan.size() : max_out;
+    if (n) std::memcpy(out, plan.data(), n * sizeof(aqua::RunDesc));
+    return (int64_t)plan.size();
+}
+
 int64_t aqua_core_plan(const aqua_kv_desc* desc, uint32_t num_seqs,
                        const int32_t* ids, const uint64_t* offs,
                        const uint64_t* img_offsets, uint64_t unit_bytes,

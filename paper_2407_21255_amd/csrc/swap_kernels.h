@@ -26,4 +26,9 @@ struct SwapLaunch {
 // Enqueues the copy on `stream`; returns the first launch error.
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream);
 
+// Enqueues the range copy of `n` pieces (each at most 64 KiB, 16-byte
+// multiples) from `src` to `dst`, both device-accessible addresses.
+hipError_t launch_copy(const uint8_t* src, uint8_t* dst, const CopyDesc* descs, uint32_t n,
+                       uint32_t max_workgroups, hipStream_t stream);
+
 }  // namespace aqua

@@ -117,7 +117,31 @@ __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
     }
 }
 
+// Range copy between two offload buffers (image migration): work unit u
+// copies descs[u].len bytes from src + src_off to dst + dst_off.
+template <int UNROLL>
+__global__ __launch_bounds__(kThreads) void copy_ranges_kernel(
+    const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+    const CopyDesc* __restrict__ descs, uint32_t n) {
+    for (uint32_t u = blockIdx.x; u < n; u += gridDim.x) {
+        const CopyDesc dsc = descs[u];
+        copy_span<UNROLL, true, true>(reinterpret_cast<const v4u*>(src + dsc.src_off),
+                                      reinterpret_cast<v4u*>(dst + dsc.dst_off),
+                                      (uint32_t)(dsc.len / 16));
+    }
+}
+
 }  // namespace
+
+hipError_t launch_copy(const uint8_t* src, uint8_t* dst, const CopyDesc* descs, uint32_t n,
+                       uint32_t max_workgroups, hipStream_t stream) {
+    if (!n) return hipSuccess;
+    uint32_t grid = n;
+    if (max_workgroups && grid > max_workgroups) grid = max_workgroups;
+    hipLaunchKernelGGL((copy_ranges_kernel<kUnroll>), dim3(grid), dim3(kThreads), 0, stream,
+                       src, dst, descs, n);
+    return hipGetLastError();
+}
 
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
     if (!a.ndesc || !a.num_layers) return hipSuccess;

@@ -37,6 +37,13 @@ def lib():
         L.aqua_core_validate.restype = i32
         L.aqua_core_plan.argtypes = [ctypes.POINTER(Desc), u32, P, P, P, u64, P, u64]
         L.aqua_core_plan.restype = i64
+        L.aqua_core_plan_ex.argtypes = [ctypes.POINTER(Desc), u32, P, P, P, P, u64, P, u64]
+        L.aqua_core_plan_ex.restype = i64
+        L.aqua_core_validate_ex.argtypes = [ctypes.POINTER(Desc), u32, P, P, u64, u64, P, P,
+                                            u32, u32, i32]
+        L.aqua_core_validate_ex.restype = i32
+        L.aqua_core_validate_migrate.argtypes = [u64, u64, u64, u64, u32, P, P, P]
+        L.aqua_core_validate_migrate.restype = i32
         L.aqua_core_tracker_new.argtypes = [u32]
         L.aqua_core_tracker_new.restype = P
         L.aqua_core_tracker_free.argtypes = [P]
@@ -64,6 +71,36 @@ def validate(desc: Desc, ids, offs, buf_addr, buf_bytes, img_offsets=None, is_in
     ns = len(offs) - 1 if num_seqs is None else num_seqs
     return lib().aqua_core_validate(ctypes.byref(desc), ns, _p(ids), _p(offs), buf_addr,
                                     buf_bytes, _p(io), int(is_in))
+
+
+def validate_ex(desc: Desc, ids, offs, buf_addr, buf_bytes, img_offsets=None,
+                img_blocks=None, first_layer=0, num_layers=0, is_in=False):
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    offs = np.ascontiguousarray(offs, dtype=np.uint64)
+    io = None if img_offsets is None else np.ascontiguousarray(img_offsets, dtype=np.uint64)
+    ib = None if img_blocks is None else np.ascontiguousarray(img_blocks, dtype=np.uint64)
+    return lib().aqua_core_validate_ex(ctypes.byref(desc), len(offs) - 1, _p(ids), _p(offs),
+                                       buf_addr, buf_bytes, _p(io), _p(ib), first_layer,
+                                       num_layers, int(is_in))
+
+
+def validate_migrate(src, src_bytes, dst, dst_bytes, so, do, ln):
+    so, do, ln = (np.ascontiguousarray(x, dtype=np.uint64) for x in (so, do, ln))
+    return lib().aqua_core_validate_migrate(src, src_bytes, dst, dst_bytes, len(ln), _p(so),
+                                            _p(do), _p(ln))
+
+
+def plan_ex(desc: Desc, ids, offs, img_offsets=None, img_blocks=None, unit_bytes=64 << 10):
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    offs = np.ascontiguousarray(offs, dtype=np.uint64)
+    io = None if img_offsets is None else np.ascontiguousarray(img_offsets, dtype=np.uint64)
+    ib = None if img_blocks is None else np.ascontiguousarray(img_blocks, dtype=np.uint64)
+    n = lib().aqua_core_plan_ex(ctypes.byref(desc), len(offs) - 1, _p(ids), _p(offs), _p(io),
+                                _p(ib), unit_bytes, None, 0)
+    out = np.zeros(n, dtype=RUN_DESC)
+    lib().aqua_core_plan_ex(ctypes.byref(desc), len(offs) - 1, _p(ids), _p(offs), _p(io),
+                            _p(ib), unit_bytes, _p(out), n)
+    return out
 
 
 def plan(desc: Desc, ids, offs, img_offsets=None, unit_bytes=64 << 10):

@@ -131,3 +131,67 @@ def test_plan_coalesces_contiguous_tables():
     runs = _check_plan((2, 100, 8, 16, 128, oracle.BF16), [list(range(10, 20))], None,
                        64 << 10)
     assert len(runs) == 10
+
+
+def test_ex_validation_matches_oracle_on_random_calls():
+    """Layer ranges and per-sequence image lengths: same status as the oracle."""
+    rng = np.random.default_rng(23)
+    for case in range(3000):
+        L = int(rng.integers(1, 4))
+        N = int(rng.integers(1, 9))
+        d = (L, N, 1, 2, 8, oracle.F16)
+        C = 64
+        S = int(rng.integers(0, 4))
+        lens = rng.integers(0, 4, size=S)
+        ids = rng.integers(0, N, size=int(lens.sum())).astype(np.int32)
+        if rng.random() < 0.2:
+            ids = rng.integers(-1, N + 1, size=int(lens.sum())).astype(np.int32)
+        offs = np.zeros(S + 1, dtype=np.uint64)
+        offs[1:] = np.cumsum(lens)
+        img_blocks = None
+        if rng.random() < 0.7:
+            img_blocks = (lens + rng.integers(-1 if rng.random() < 0.1 else 0, 3, size=S)).clip(0)
+        img_offsets = None
+        if rng.random() < 0.5:
+            img_offsets = (rng.integers(0, 8, size=S) * (L * C)).astype(np.uint64)
+        l0, nl = 0, 0
+        if rng.random() < 0.6:
+            l0 = int(rng.integers(0, L + 1))
+            nl = int(rng.integers(0, L + 1))
+        buf = np.zeros(int(rng.integers(0, 12)) * L * C + 16, dtype=np.uint8)
+        pool = np.zeros(L * N * C, dtype=np.uint8)
+        is_in = bool(rng.random() < 0.5)
+        od = oracle.desc(*d)
+        fn = oracle.swap_in_ex if is_in else oracle.swap_out_ex
+        kw = {"src_bytes" if is_in else "dst_bytes": buf.nbytes - 16}
+        want = fn(od, pool, None, buf, img_offsets, img_blocks, l0, nl, ids=ids, offs=offs, **kw)
+        got = core_lib.validate_ex(_desc(*d), ids, offs, buf.ctypes.data, buf.nbytes - 16,
+                                   img_offsets, img_blocks, l0, nl, is_in)
+        assert got == want, (case, ids, offs, img_offsets, img_blocks, l0, nl, is_in)
+
+
+def test_plan_with_longer_images_strides_by_image_length():
+    d = _desc(3, 64, 1, 4, 8, oracle.BF16)
+    C = 2 * 4 * 8 * 2
+    runs = core_lib.plan_ex(d, [5, 9, 10, 11, 40], [0, 2, 5], None, [4, 7], unit_bytes=1 << 20)
+    # Sequence 0: image of 4 blocks per layer at 0; sequence 1: 7 blocks at 3*4*C.
+    assert list(runs["block"]) == [5, 9, 10, 40]
+    assert list(runs["nchunks"]) == [1, 1, 2, 1]
+    assert list(runs["img_lstride"]) == [4 * C, 4 * C, 7 * C, 7 * C]
+    assert list(runs["img_off"]) == [0, C, 3 * 4 * C, 3 * 4 * C + 2 * C]
+
+
+def test_migrate_validation_matches_oracle():
+    rng = np.random.default_rng(24)
+    for case in range(2000):
+        src = np.zeros(4096, dtype=np.uint8)
+        dst = src if rng.random() < 0.3 else np.zeros(4096, dtype=np.uint8)
+        n = int(rng.integers(0, 4))
+        g = 16 if rng.random() < 0.9 else 8
+        so = rng.integers(0, 300, size=n) * g
+        do = rng.integers(0, 300, size=n) * g
+        ln = rng.integers(0, 40, size=n) * g
+        want = oracle.migrate(src, dst, so, do, ln)
+        got = core_lib.validate_migrate(src.ctypes.data, src.nbytes, dst.ctypes.data,
+                                        dst.nbytes, so, do, ln)
+        assert got == want, (case, so, do, ln, src is dst)

@@ -1,0 +1,228 @@
+"""GPU parity for the extended operations: prefix swap-in from a cached
+image, layer-group (pipelined / layer-by-layer) swaps, and image migration
+between the HBM region and pinned host memory -- each against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_21255_amd import aqua
+from paper_2407_21255_amd import workload as wl
+from tests.checkers import assert_bytes_equal
+from tests.gpu_util import device_pool, host, odesc, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    aqua.load()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+HOST_PATHS = {"hbm": None, "staged": aqua.AQUA_HOST_STAGED, "zero_copy": aqua.AQUA_HOST_ZERO_COPY}
+
+
+def _buf(nbytes, where):
+    if where == "hbm":
+        return torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    return torch.zeros(nbytes, dtype=torch.uint8, pin_memory=True)
+
+
+@pytest.mark.parametrize("where", ["hbm", "staged", "zero_copy"])
+def test_prefix_swap_in_from_cached_image(where):
+    """A long prompt's image is cached once; prefixes of it are swapped back
+    in, several times, into fresh blocks (the table covers the first m of
+    the image's n blocks per layer)."""
+    shape = wl.KVShape(8, 2048, 4, 16, 64, wl.BF16)     # 16 KiB chunks
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 51)
+    n = 700
+    prompt = perm[:n]
+    pool = device_pool(shape, 21, {b: (0, i) for i, b in enumerate(prompt)})
+    pool_h = host(pool)
+    img = _buf(shape.image_bytes(n), where)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    if HOST_PATHS[where] is not None:
+        kv.set_host_path(HOST_PATHS[where])
+    try:
+        kv.swap_out([prompt], img)
+        kv.sync()
+        img_h = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [prompt], img_h) == 0
+        assert_bytes_equal(host(img), img_h, "cached image")
+        free = perm[n:]
+        for rep, m in enumerate([n - 16, 1, 333]):
+            fresh = free[rep * 400: rep * 400 + m]
+            assert len(fresh) == m
+            kv.swap_in([fresh], img, img_blocks=[n])
+            kv.sync()
+            assert oracle.swap_in_ex(d, pool_h, [fresh], img_h, None, [n]) == 0
+            assert_bytes_equal(host(pool), pool_h, f"pool after prefix {m}")
+            say("prefix", where, m, "ok")
+    finally:
+        kv.close()
+
+
+@pytest.mark.parametrize("where", ["hbm", "staged"])
+def test_layer_groups_pipelined_swap_in(where):
+    """Swap-in issued as one call per layer group; a consumer stream waits
+    on each group's ticket and snapshots that group's layers, which must
+    already hold the swapped-in bytes."""
+    shape = wl.KVShape(12, 1024, 8, 16, 128, wl.F16)
+    d = odesc(shape)
+    C = shape.chunk_bytes
+    perm = wl.permutation(shape.num_blocks, 52)
+    bt, bt2 = perm[:200], perm[200:400]
+    pool = device_pool(shape, 22, {b: (0, i) for i, b in enumerate(bt)})
+    pool_h = host(pool)
+    img = _buf(shape.image_bytes(200), where)
+    swap_s, use_s = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        kv.swap_out([bt], img)
+        kv.sync()
+        img_h = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [bt], img_h) == 0
+        P = pool.view(shape.num_layers, shape.num_blocks, C)
+        idx = torch.tensor(bt2, dtype=torch.long, device="cuda")
+        snaps, groups = [], [(0, 3), (3, 3), (6, 4), (10, 2)]
+        for l0, nl in groups:
+            t = kv.swap_in([bt2], img, stream=swap_s, layers=(l0, nl))
+            kv.stream_wait(t, use_s)
+            with torch.cuda.stream(use_s):
+                snaps.append(P[l0:l0 + nl].index_select(1, idx))
+        torch.cuda.synchronize()
+        assert oracle.swap_in(d, pool_h, [bt2], img_h) == 0
+        PH = pool_h.reshape(shape.num_layers, shape.num_blocks, C)
+        for (l0, nl), snap in zip(groups, snaps):
+            assert_bytes_equal(host(snap), PH[l0:l0 + nl][:, bt2], f"layers {l0}..{l0 + nl}")
+        assert_bytes_equal(host(pool), pool_h, "pool after all groups")
+        assert kv.stats()["calls_in"] == len(groups)
+    finally:
+        kv.close()
+
+
+def test_layer_by_layer_offload_and_reload():
+    """FlexGen-style: while layer l of one prompt goes out, layer l of
+    another comes in, one layer per call on two streams."""
+    shape = wl.KVShape(6, 512, 2, 16, 64, wl.BF16)
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 53)
+    a, b = perm[:100], perm[100:180]
+    pool = device_pool(shape, 23, None)
+    pool_h = host(pool)
+    img_a = _buf(shape.image_bytes(100), "hbm")
+    img_b = torch.empty(shape.image_bytes(80), dtype=torch.uint8, device="cuda")
+    wl.fill_chunks(img_b.view(-1, shape.chunk_bytes),
+                   torch.arange(shape.num_layers * 80, dtype=torch.int64) * 31 + 7,
+                   shape.chunk_bytes, shape.dtype)
+    imgb_h = host(img_b)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        for l in range(shape.num_layers):
+            kv.swap_out([a], img_a, stream=s1, layers=(l, 1))
+            kv.swap_in([a[:80]], img_b, stream=s2, layers=(l, 1))   # reuses a's blocks
+        kv.sync()
+        want_a = np.zeros(img_a.numel(), dtype=np.uint8)
+        for l in range(shape.num_layers):
+            assert oracle.swap_out_ex(d, pool_h, [a], want_a, None, None, l, 1) == 0
+            assert oracle.swap_in_ex(d, pool_h, [a[:80]], imgb_h, None, None, l, 1) == 0
+        assert_bytes_equal(host(img_a), want_a, "layer-wise swap-out")
+        assert_bytes_equal(host(pool), pool_h, "layer-wise swap-in")
+        assert kv.stats()["waits_inserted"] > 0
+    finally:
+        kv.close()
+
+
+@pytest.mark.parametrize("back", ["staged", "zero_copy"])
+def test_migration_between_hbm_and_host_then_swap_in(back):
+    """Reclaim: images swapped out to the HBM region move to pinned host
+    memory (and one back), on other streams with no host sync; a swap-in
+    from the new place equals the oracle's."""
+    shape = wl.KVShape(8, 2048, 8, 16, 128, wl.BF16)
+    d = odesc(shape)
+    case = wl.fragmented_case("mig", shape, 31, 8, 96, 4)
+    pool = device_pool(shape, case.seed, case.owner)
+    pool_h = host(pool)
+    size = case.payload_bytes
+    region = torch.zeros(size + 8192, dtype=torch.uint8, device="cuda")
+    host_buf = torch.zeros(size + 8192, dtype=torch.uint8, pin_memory=True)
+    region2 = torch.zeros(size, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    kv.set_host_path(HOST_PATHS[back])
+    try:
+        # Images at offset 4096 in the region; moved to offset 8192 - 4096 + 0
+        # of the host buffer as two ranges, then one image back to HBM.
+        L, C = shape.num_layers, shape.chunk_bytes
+        lens = [L * len(t) * C for t in case.out_tables]
+        offs = list(np.cumsum([0] + lens[:-1]) + 4096)
+        # Stream sa is held back by real work queued ahead of the swap-out,
+        # so the migration on sb must wait for it, and the second migration
+        # on sc for the first.
+        g = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(sa):
+            for _ in range(200):
+                g = (g @ g).clamp_(-1, 1)
+        kv.swap_out(case.out_tables, region, offs, stream=sa)
+        half = sum(lens[:2])
+        kv.migrate(region, host_buf, [4096, 4096 + half], [16, 16 + half],
+                   [half, size - half], stream=sb)
+        kv.migrate(host_buf, region2, [16], [0], [lens[0]], stream=sc)
+        host_offs = [16 + o - 4096 for o in offs]
+        kv.swap_in(case.in_tables[1:], host_buf, host_offs[1:], stream=sc)
+        kv.swap_in(case.in_tables[:1], region2, [0], stream=sa)
+        kv.sync()
+        st = kv.stats()
+        say("migration", back, st)
+        reg_h = np.zeros(region.numel(), dtype=np.uint8)
+        hb_h = np.zeros(host_buf.numel(), dtype=np.uint8)
+        r2_h = np.zeros(region2.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, case.out_tables, reg_h, offs) == 0
+        assert oracle.migrate(reg_h, hb_h, [4096, 4096 + half], [16, 16 + half],
+                              [half, size - half]) == 0
+        assert oracle.migrate(hb_h, r2_h, [16], [0], [lens[0]]) == 0
+        assert oracle.swap_in(d, pool_h, case.in_tables[1:], hb_h, host_offs[1:]) == 0
+        assert oracle.swap_in(d, pool_h, case.in_tables[:1], r2_h, [0]) == 0
+        assert_bytes_equal(host(region), reg_h, "region")
+        assert_bytes_equal(host(host_buf), hb_h, "host image")
+        assert_bytes_equal(host(region2), r2_h, "migrated back")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["calls_migrate"] == 2 and st["waits_inserted"] >= 2
+    finally:
+        kv.close()
+
+
+def test_migrate_errors_leave_no_trace():
+    shape = wl.KVShape(2, 16, 1, 2, 8, wl.BF16)
+    pool = device_pool(shape, 5)
+    a = torch.arange(4096, dtype=torch.int32, device="cuda").view(torch.uint8)
+    b = torch.zeros(16384, dtype=torch.uint8, device="cuda")
+    a_h, b_h = host(a), host(b)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        for so, do, ln, code in [([0], [8], [16], aqua.AQUA_ERR_INVALID),
+                                 ([0, 32], [0, 16], [32, 16], aqua.AQUA_ERR_DUPLICATE),
+                                 ([16368], [8192], [32], aqua.AQUA_ERR_CAPACITY)]:
+            with pytest.raises(aqua.AquaError) as ei:
+                kv.migrate(a, b, so, do, ln)
+            assert ei.value.status == code
+        with pytest.raises(aqua.AquaError) as ei:
+            kv.migrate(b, b, [0], [16], [32])
+        assert ei.value.status == aqua.AQUA_ERR_DUPLICATE
+        torch.cuda.synchronize()
+        assert_bytes_equal(host(a), a_h, "source")
+        assert_bytes_equal(host(b), b_h, "destination")
+        t = kv.migrate(a, b, [0], [1024], [4096])
+        kv.sync(t)
+        assert_bytes_equal(host(b)[1024:1024 + 4096], a_h[:4096], "migrated bytes")
+    finally:
+        kv.close()
