@@ -65,6 +65,10 @@ WORKLOADS = {
                "in 10 layer groups of 8, one ticket each",
     "migrate": "Llama-3-70B-shaped KV: the 10 GiB image of one 32768-token prompt migrated "
                "from the HBM region to pinned host memory and back",
+    "cfs": "fair scheduling (least-served first, rescheduled every 16 iterations or on a "
+           "completion) of a 192-request burst on a Llama-3-8B-shaped bf16 pool (16384 "
+           "blocks, 2x oversubscribed): each reschedule swaps the prompts leaving the batch "
+           "out and those rejoining it in",
     "cycle": "time-sliced preemption on a Llama-3-8B-shaped fp8 e4m3 pool (16384 blocks): "
              "64 prompts of 128..8192 tokens, each slice swaps the 16 longest-resident out "
              "on one stream and the 16 longest-waiting in on another",
@@ -327,28 +331,23 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
     return out
 
 
-def run_cycle(args, res_common):
-    """Slices of the preemption schedule: out on one stream, in on another."""
+def _time_slices(sched, pool, region, ids, warmup):
+    """Issues slices ``ids`` of a swap schedule (the first ``warmup`` of them
+    untimed): out on one stream, in on another, ``aqua_sync`` at the end of
+    each, as a scheduler's loop boundary does.  (Issued without it, slices
+    stay correct -- the library orders reused blocks and slots -- but
+    consecutive slices then contend for HBM.)"""
     import numpy as np
     import torch
 
     from paper_2407_21255_amd import aqua
-    from paper_2407_21255_amd import workload as wl
     from paper_2407_21255_amd.cycle import slice_tables
 
-    n = args.warmup + args.steps
-    sched = wl.preemption_schedule(n_slices=n)
     s = sched.shape
-    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
-    wl.fill_pool(pool, s, sched.seed, wl.schedule_owner(sched))
-    region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
-    wl.fill_region(region, sched)
-    torch.cuda.synchronize()
-    prepared = [slice_tables(sched, k) for k in range(n)]
+    prepared = {k: slice_tables(sched, k) for k in ids}
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
-    evs, moved = [], 0
-    C = s.chunk_bytes
+    evs = []
 
     def one(k, timed):
         out, out_off, inn, in_off = prepared[k]
@@ -363,57 +362,132 @@ def run_cycle(args, res_common):
         if timed:
             b1.record(sb)
             evs.append((a0, a1, b0, b1, len(out[0]), len(inn[0])))
-        kv.sync(0)  # the slice boundary
+        kv.sync(0)
 
-    # Each slice ends with aqua_sync, as a scheduler's loop boundary does.
-    # (Issued without it, slices stay correct -- the library orders reused
-    # blocks and slots -- but consecutive slices then contend for HBM.)
-    for k in range(args.warmup):
+    for k in ids[:warmup]:
         one(k, False)
     kv.sync(0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.warmup, n):
+    for k in ids[warmup:]:
         one(k, True)
     kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = kv.stats()
     kv.close()
-    out_b = np.array([e[4] for e in evs]) * s.num_layers * C
-    in_b = np.array([e[5] for e in evs]) * s.num_layers * C
+    unit = s.num_layers * s.chunk_bytes
+    out_b = np.array([e[4] for e in evs], dtype=np.float64) * unit
+    in_b = np.array([e[5] for e in evs], dtype=np.float64) * unit
     out_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     in_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    return wall, st, out_b, in_b, out_ms, in_ms
+
+
+def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, config):
+    import numpy as np
+    from paper_2407_21255_amd import workload as wl
+
     moved = float(out_b.sum() + in_b.sum())
-    achieved = float((2 * out_b / (out_ms * 1e-3)).mean()) / 1e9
+    ok = out_b > 0
+    # Gather rate of each slice (its bytes are read and written once).
+    achieved = float((2 * out_b[ok] / (out_ms[ok] * 1e-3)).mean()) / 1e9 if ok.any() else 0.0
     res = dict(res_common)
     res.update({
         "value": round(moved / wall / 1e9, 2),
-        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "ms_per_step": round(wall * 1e3 / max(1, steps), 4),
         "dtype": wl.DTYPE_NAME[s.dtype],
-        "config": {
-            "workload": WORKLOADS["cycle"], "layers": s.num_layers,
-            "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
-            "pool_blocks": s.num_blocks, "chunk_bytes": C, "prompts": len(sched.nblocks),
-            "swaps_per_slice": 16, "slices_timed": args.steps,
-            "host_sync_per_slice": True,
-            "mean_payload_bytes_per_direction": round(float(out_b.mean())),
-            "offload_target": "hbm", "parallelism": "single_gpu",
-        },
+        "config": config,
         "roofline": {
             "bound": "hbm", "kernel": "gather (swap-out), concurrent with the scatter",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-            "algorithmic_bytes_per_launch": round(float(2 * out_b.mean())),
+            "algorithmic_bytes_per_launch": round(float(2 * out_b[ok].mean())) if ok.any()
+            else 0,
         },
-        "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
-                      "swap_in_mean": round(float(in_ms.mean()), 4)},
+        "kernel_ms": {"swap_out_mean": round(float(out_ms[ok].mean()), 4) if ok.any() else 0,
+                      "swap_in_mean": round(float(in_ms[in_b > 0].mean()), 4)
+                      if (in_b > 0).any() else 0},
         "slice_hbm_GBps": round(2 * moved / wall / 1e9, 1),
         "waits_inserted": st["waits_inserted"],
         "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
                                   2),
         "kernel_source": _kernel_hash(),
     })
+    return res
+
+
+def run_cycle(args, res_common):
+    """Slices of the preemption schedule: out on one stream, in on another."""
+    import torch
+
+    from paper_2407_21255_amd import workload as wl
+
+    n = args.warmup + args.steps
+    sched = wl.preemption_schedule(n_slices=n)
+    s = sched.shape
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, sched.seed, wl.schedule_owner(sched))
+    region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_region(region, sched)
+    torch.cuda.synchronize()
+    timed = _time_slices(sched, pool, region, list(range(n)), args.warmup)
+    out_b = timed[2]
+    config = {
+        "workload": WORKLOADS["cycle"], "layers": s.num_layers,
+        "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
+        "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
+        "prompts": len(sched.nblocks), "swaps_per_slice": 16, "slices_timed": args.steps,
+        "host_sync_per_slice": True,
+        "mean_payload_bytes_per_direction": round(float(out_b.mean())),
+        "offload_target": "hbm", "parallelism": "single_gpu",
+    }
+    return _slice_result(res_common, s, *timed, args.steps, config), s
+
+
+def run_cfs(args, res_common):
+    """Fair scheduling of a burst on the 8B-shaped pool: the rescheduler's
+    page-outs and page-ins, slice by slice, for the slices that swap."""
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import cfs
+    from paper_2407_21255_amd import workload as wl
+
+    cfg = wl.CFS_LLAMA8B
+    s = cfg.shape
+    tr = cfg.trace()
+    d = cfg.decode_slots(tr)
+    t0 = time.perf_counter()
+    log, sch = cfs.run_trace(tr, s.num_blocks, s.block_tokens, cfg.batch_tokens, d, cfg.k)
+    sched_s = time.perf_counter() - t0
+    sched = wl.cfs_swap_schedule(s, cfg.seed, tr, log)
+    ids = [k for k, sl in enumerate(sched.slices) if sl.out_tables or sl.in_tables]
+    ids = ids[:args.warmup + args.steps]
+    steps = len(ids) - min(args.warmup, len(ids))
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, cfg.seed)
+    region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_region(region, sched)
+    torch.cuda.synchronize()
+    timed = _time_slices(sched, pool, region, ids, args.warmup)
+    out_b, in_b = timed[2], timed[3]
+    config = {
+        "workload": WORKLOADS["cfs"], "layers": s.num_layers, "kv_heads": s.num_kv_heads,
+        "head_dim": s.head_dim, "block_tokens": s.block_tokens, "pool_blocks": s.num_blocks,
+        "chunk_bytes": s.chunk_bytes, "requests": len(tr), "batch_tokens": cfg.batch_tokens,
+        "decode_slots": d, "k": cfg.k, "iterations": len(log), "reschedules": len(sched.slices),
+        "swapping_slices": len([1 for sl in sched.slices if sl.out_tables or sl.in_tables]),
+        "slices_timed": steps, "host_sync_per_slice": True,
+        "mean_payload_bytes_per_direction": round(float(out_b.mean())) if len(out_b) else 0,
+        "offload_target": "hbm", "parallelism": "single_gpu",
+    }
+    res = _slice_result(res_common, s, *timed, steps, config)
+    res["scheduler"] = {
+        "partition_calls": sch.partition_calls,
+        "host_us_per_iteration": round(sched_s * 1e6 / len(log), 2),
+        "swap_ms_per_swapping_slice": round(float(timed[0] * 1e3 / max(1, steps)), 3),
+    }
     return res, s
 
 
@@ -580,6 +654,8 @@ def main():
     }
     if args.workload == "cycle":
         res, shape = run_cycle(args, common)
+    elif args.workload == "cfs":
+        res, shape = run_cfs(args, common)
     elif args.workload in ("prefix", "prefix_host", "layered", "migrate"):
         res, shape = run_next(args, common)
     else:

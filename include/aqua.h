@@ -262,6 +262,58 @@ AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* o
 /* Static text for a status code. */
 AQUA_API const char* aqua_status_str(aqua_status s);
 
+/* ---- Fair batch partitioning (section 7, "Aqua's batch partitioning
+ * algorithm").  Host code: no pool, no GPU.
+ *
+ * A time-sliced scheduler that pages prompts out and in keeps chunked
+ * prefill by splitting each iteration's token budget b into a prefill
+ * share p and a decode share d, with d at its upper bound, the number of
+ * prompts that fit in GPU memory:
+ *   1. d = min(decode_slots, b), p = b - d;
+ *   2. prefill prompts (prefill_done < prompt_tokens), fewest prompt tokens
+ *      computed first, take chunks of their remaining prompt tokens until p
+ *      is spent;
+ *   3. decode prompts (prefill_done == prompt_tokens), fewest tokens
+ *      generated first, take one token each, at most d of them;
+ *   4. decode slots left unused go to prefill, continuing the order of step
+ *      2 (first the chunk that step 2 cut short);
+ *   5. the whole batch is closed at the first prompt whose KV blocks do not
+ *      fit in what is left of capacity_blocks.
+ * Equal service is broken by the lower request index.  A prompt with
+ * ctx = prefill_done + generated cached tokens that computes x tokens needs
+ * ceil((ctx + x) / block_tokens) blocks; held_blocks of them are already its
+ * own and not counted in capacity_blocks.  At a reschedule pass held 0 and
+ * the whole pool (prompts left out are paged out); within a time slice pass
+ * the residents' current blocks as held and the pool's free blocks as
+ * capacity. */
+typedef struct {
+    uint32_t prompt_tokens; /* >= 1 */
+    uint32_t prefill_done;  /* prompt tokens with KV computed, <= prompt_tokens */
+    uint32_t generated;     /* output tokens so far; 0 while prefill is unfinished */
+    uint32_t held_blocks;   /* pool blocks already owned outside capacity_blocks */
+} aqua_cfs_request;
+
+typedef struct {
+    uint32_t batch_tokens;    /* b, >= 1 */
+    uint32_t decode_slots;    /* upper bound of d: prompts that fit, >= 1 */
+    uint32_t block_tokens;    /* tokens per KV block, >= 1 */
+    uint32_t reserved;        /* must be 0 */
+    uint64_t capacity_blocks; /* pool blocks the batch may take */
+} aqua_cfs_params;
+
+/* requests: host array of num_requests entries.  On AQUA_OK the batch is
+ * written in admission order: batch_index[j] (a request index) computes
+ * batch_tokens[j] tokens, j < *batch_size; each request appears at most
+ * once, so both arrays need num_requests entries.  *blocks_taken (may be
+ * NULL) is the capacity the batch uses.  AQUA_ERR_INVALID for null
+ * pointers, zero batch_tokens / decode_slots / block_tokens, nonzero
+ * reserved, an empty prompt, prefill_done > prompt_tokens or tokens
+ * generated before the prefill is complete; nothing is written then. */
+AQUA_API aqua_status aqua_cfs_partition(const aqua_cfs_request* requests,
+                                        uint32_t num_requests, const aqua_cfs_params* params,
+                                        uint32_t* batch_index, uint32_t* batch_tokens,
+                                        uint32_t* batch_size, uint64_t* blocks_taken);
+
 #ifdef __cplusplus
 }
 #endif

@@ -38,7 +38,7 @@ EXPORTS = (
     "aqua_swap_in", "aqua_swap_out_ex", "aqua_swap_in_ex", "aqua_migrate",
     "aqua_sync", "aqua_stream_wait", "aqua_query",
     "aqua_kv_pool_set_max_workgroups", "aqua_kv_pool_set_host_path",
-    "aqua_pool_stats_get", "aqua_status_str",
+    "aqua_pool_stats_get", "aqua_status_str", "aqua_cfs_partition",
 )
 
 
@@ -67,6 +67,17 @@ class aqua_pool_stats(ctypes.Structure):
         "descriptors", "waits_inserted", "waits_elided", "calls_migrate",
         "bytes_migrated", "host_ns", "wait_ns")] + [
         ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class aqua_cfs_request(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint32) for n in (
+        "prompt_tokens", "prefill_done", "generated", "held_blocks")]
+
+
+class aqua_cfs_params(ctypes.Structure):
+    _fields_ = [("batch_tokens", ctypes.c_uint32), ("decode_slots", ctypes.c_uint32),
+                ("block_tokens", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("capacity_blocks", ctypes.c_uint64)]
 
 
 class AquaError(RuntimeError):
@@ -105,6 +116,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_kv_pool_set_max_workgroups.argtypes = [P, i32, u32]
     L.aqua_kv_pool_set_host_path.argtypes = [P, i32]
     L.aqua_pool_stats_get.argtypes = [P, ctypes.POINTER(aqua_pool_stats)]
+    L.aqua_cfs_partition.argtypes = [P, u32, ctypes.POINTER(aqua_cfs_params), P, P,
+                                     ctypes.POINTER(u32), ctypes.POINTER(u64)]
     L.aqua_status_str.argtypes = [i32]
     L.aqua_status_str.restype = ctypes.c_char_p
     for n in EXPORTS:
@@ -198,6 +211,36 @@ def aqua_status_str(status: int) -> str:
         return load().aqua_status_str(status).decode()
     except FileNotFoundError:
         return f"status {status}"
+
+
+def aqua_cfs_partition(requests: np.ndarray, params: aqua_cfs_params,
+                       batch_index: np.ndarray, batch_tokens: np.ndarray):
+    """requests: uint32 array [n, 4] (the fields of aqua_cfs_request);
+    batch_index / batch_tokens: uint32 arrays of n entries.  Returns
+    (status, batch size, blocks taken)."""
+    n = len(requests)
+    size, taken = ctypes.c_uint32(0), ctypes.c_uint64(0)
+    st = load().aqua_cfs_partition(
+        requests.ctypes.data if n else None, n, ctypes.byref(params),
+        batch_index.ctypes.data if n else None, batch_tokens.ctypes.data if n else None,
+        ctypes.byref(size), ctypes.byref(taken))
+    return st, size.value, taken.value
+
+
+def cfs_partition(requests, batch_tokens: int, decode_slots: int, capacity_blocks: int,
+                  block_tokens: int):
+    """One iteration's fair batch (section 7): ``requests`` rows are
+    (prompt_tokens, prefill_done, generated, held_blocks).  Returns
+    (index array, token array, blocks taken), admission order."""
+    req = np.ascontiguousarray(np.asarray(requests, dtype=np.uint32).reshape(-1, 4))
+    n = len(req)
+    idx = np.zeros(n, dtype=np.uint32)
+    tok = np.zeros(n, dtype=np.uint32)
+    prm = aqua_cfs_params(batch_tokens, decode_slots, block_tokens, 0, capacity_blocks)
+    st, size, taken = aqua_cfs_partition(req, prm, idx, tok)
+    if st != AQUA_OK:
+        raise AquaError(st, "aqua_cfs_partition")
+    return idx[:size], tok[:size], taken
 
 
 # -- torch-facing wrapper ------------------------------------------------------

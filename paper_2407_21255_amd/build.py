@@ -23,7 +23,7 @@ CORE_LIB = os.path.join(PKG, "libaqua_core.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["aqua_core.cpp", "swap_kernels.hip", "aqua_capi.hip"]
+HIP_SOURCES = ["aqua_core.cpp", "cfs.cpp", "swap_kernels.hip", "aqua_capi.hip"]
 CORE_SOURCES = ["aqua_core.cpp", "core_testapi.cpp"]
 
 # Packed fp32 instructions are switched off for every device compile.

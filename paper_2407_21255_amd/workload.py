@@ -354,6 +354,10 @@ class Slice:
     in_tables: List[List[int]]
     resident_after: List[int]       # resident prompts after the slice (FIFO order)
     tables_after: dict              # prompt -> table, for residents
+    # Written by the compute of the slice's iterations, after its swaps:
+    # (prompt, first logical block, new physical blocks), in order.
+    grow: List[tuple] = field(default_factory=list)
+    finished: List[int] = field(default_factory=list)   # blocks freed, no swap
 
 
 @dataclass
@@ -367,6 +371,9 @@ class Schedule:
     initial_resident: List[int]
     initial_tables: dict            # prompt -> table
     slices: List[Slice]
+    # Prompts whose generated image is in the region at the start (None:
+    # every prompt that is not initially resident).
+    initial_swapped: Optional[List[int]] = None
 
     def mutation(self, s: int, p: int) -> int:
         """64-bit word written twice at the start of the last logical block
@@ -429,14 +436,35 @@ def mutation_writes(sched: Schedule, s: int):
     sl = sched.slices[s]
     offs, words = [], []
     for p in sl.resident_after:
+        if not sl.tables_after[p]:
+            continue
         b = sl.tables_after[p][-1]
         offs.append((l * sh.num_blocks + b) * C)
         w = sched.mutation(s, p)
         words.append(np.frombuffer(w.to_bytes(8, "little") * 2, dtype=np.uint8))
-    slots = [(sched.slot_offsets[p], sh.image_bytes(sched.nblocks[p]))
-             for p in sl.in_prompts]
+    slots = [(sched.slot_offsets[p], sh.image_bytes(len(t)))
+             for p, t in zip(sl.in_prompts, sl.in_tables)]
     return (np.asarray(offs, dtype=np.int64),
             np.stack(words) if words else np.zeros((0, 16), np.uint8), slots)
+
+
+def apply_growth(pool: torch.Tensor, sched: Schedule, s: int) -> None:
+    """The KV that slice s's iterations compute: every new block of a
+    resident prompt, all layers, keyed as live chunk (prompt, layer,
+    logical block).  ``pool`` is the flat uint8 pool (host or device)."""
+    sh = sched.shape
+    L, N, C = sh.num_layers, sh.num_blocks, sh.chunk_bytes
+    P = pool[:sh.pool_bytes].view(L, N, C)
+    lay = np.arange(L, dtype=np.uint64).reshape(L, 1)
+    step = max(1, (64 << 20) // (L * C))          # bounds the temporaries
+    for p, first, blocks in sched.slices[s].grow:
+        for j in range(0, len(blocks), step):
+            part = blocks[j:j + step]
+            i = np.arange(first + j, first + j + len(part), dtype=np.uint64).reshape(1, -1)
+            keys = torch.from_numpy(np.ascontiguousarray(
+                chunk_keys_np(sched.seed, TAG_LIVE, p, lay, i)).reshape(-1).view(np.int64))
+            vals = chunk_values(keys.to(pool.device), C, sh.dtype).view(L, len(part), C)
+            P[:, torch.as_tensor(part, dtype=torch.long, device=pool.device)] = vals
 
 
 def fill_region(region: torch.Tensor, sched: Schedule) -> None:
@@ -445,9 +473,10 @@ def fill_region(region: torch.Tensor, sched: Schedule) -> None:
     region.fill_(GUARD_BYTE)
     sh = sched.shape
     C = sh.chunk_bytes
-    for p in range(len(sched.nblocks)):
-        if p in sched.initial_resident:
-            continue
+    swapped = sched.initial_swapped
+    if swapped is None:
+        swapped = [p for p in range(len(sched.nblocks)) if p not in sched.initial_resident]
+    for p in swapped:
         o, n = sched.slot_offsets[p], sched.nblocks[p]
         fill_chunks(region[o:o + sh.image_bytes(n)].view(-1, C),
                     image_keys(sh, sched.seed, p, n), C, sh.dtype)
@@ -456,3 +485,112 @@ def fill_region(region: torch.Tensor, sched: Schedule) -> None:
 def schedule_owner(sched: Schedule) -> dict:
     """Physical block -> (prompt, logical block) of the initial residents."""
     return {b: (p, i) for p, t in sched.initial_tables.items() for i, b in enumerate(t)}
+
+
+# --------------------------------------------------------------------------
+# Fair-scheduling traces and the swap schedules they produce
+
+def burst_trace(seed: int, n: int, burst: int, gap: int, prompt_range, output_range):
+    """Synthetic serving burst: ``burst`` requests at iteration 0, then one
+    every ``gap`` iterations; prompt and output lengths uniform in the
+    closed ranges.  Returns [(arrival, prompt tokens, output tokens)]."""
+    rng = Rng(mix(seed ^ 0xC0F5))
+    out = []
+    for r in range(n):
+        a = 0 if r < burst else (r - burst + 1) * gap
+        p = prompt_range[0] + rng.below(prompt_range[1] - prompt_range[0] + 1)
+        o = output_range[0] + rng.below(output_range[1] - output_range[0] + 1)
+        out.append((a, p, o))
+    return out
+
+
+def cfs_swap_schedule(shape: KVShape, seed: int, trace, log, guard: int = 4096) -> Schedule:
+    """Block-level swap schedule of a rescheduler run.
+
+    ``log`` has one entry per iteration (``resched``, ``out``, ``in``,
+    ``batch``, ``done``).  Each reschedule opens a slice: the prompts paged
+    out are swapped out from their tables into their slots and their blocks
+    go to the tail of the free list (a seeded permutation at the start);
+    the prompts paged in that have an image get fresh blocks from its head,
+    round-robin.  The slice's iterations then grow the residents' tables as
+    their tokens need blocks, and completed prompts free theirs.  Slot p
+    holds prompt p's largest image (prompt plus output tokens)."""
+    T = shape.block_tokens
+    lengths = [p + o for _, p, o in trace]
+    nblocks = [ceil_div(x, T) for x in lengths]
+    slot_offsets, region = image_offsets(nblocks, shape, guard)
+    free = permutation(shape.num_blocks, seed)
+    ctx = [0] * len(trace)
+    tables: dict = {}
+    image = {}                       # prompt -> blocks in its offload image
+    slices: List[Slice] = []
+    for e in log:
+        if e["resched"]:
+            outs, out_t = [], []
+            for p in e["out"]:
+                t = tables.pop(p)
+                if t:
+                    outs.append(p)
+                    out_t.append(t)
+                    free.extend(t)
+                image[p] = len(t)
+            ins = [p for p in e["in"] if image.get(p, 0) > 0]
+            in_t = alloc_round_robin(free, [image[p] for p in ins])
+            for p in e["in"]:
+                tables[p] = []
+            for p, t in zip(ins, in_t):
+                tables[p] = t
+            slices.append(Slice(len(slices), outs, out_t, ins, in_t, [], {}))
+        sl = slices[-1]
+        for p, x in e["batch"]:
+            ctx[p] += x if ctx[p] < trace[p][1] else 1
+            need = ceil_div(ctx[p], T) - len(tables[p])
+            if need > 0:
+                new = free[:need]
+                del free[:need]
+                sl.grow.append((p, len(tables[p]), new))
+                tables[p] = tables[p] + new
+        for p in e["done"]:
+            free.extend(tables.pop(p))
+            sl.finished.append(p)
+        sl.resident_after = sorted(tables)
+        sl.tables_after = {p: list(t) for p, t in tables.items()}
+    return Schedule(shape, seed, lengths, nblocks, slot_offsets, region, [], {}, slices, [])
+
+
+@dataclass
+class CfsConfig:
+    """A fair-scheduling workload: pool shape, burst trace and scheduler
+    settings.  ``decode_slots`` -- the number of prompts that fit in the
+    pool -- is the pool's blocks over the blocks of a mean-length request."""
+    name: str
+    shape: KVShape
+    seed: int
+    n: int
+    burst: int
+    gap: int
+    prompt_range: tuple
+    output_range: tuple
+    batch_tokens: int
+    k: int
+
+    def trace(self):
+        return burst_trace(self.seed, self.n, self.burst, self.gap, self.prompt_range,
+                           self.output_range)
+
+    def decode_slots(self, trace=None) -> int:
+        tr = self.trace() if trace is None else trace
+        total = sum(p + o for _, p, o in tr)
+        mean_blocks = ceil_div(total, len(tr) * self.shape.block_tokens)
+        return max(1, self.shape.num_blocks // mean_blocks)
+
+
+# Small enough for a whole-schedule oracle replay: 48 requests on a
+# 1024-block pool of 8 KiB chunks, about 4x oversubscribed.
+CFS_SMALL = CfsConfig("small", KVShape(4, 1024, 2, 16, 64, BF16), 11, 48, 24, 2,
+                      (64, 1024), (64, 512), 1024, 8)
+# Llama-3-8B-shaped pool (32 GiB); 192 requests, 96 at once then one every
+# second iteration, prompts 512-4096 and outputs 512-2048 tokens, 8192-token
+# iterations, rescheduled every 16 iterations: the pool is about 2x
+# oversubscribed at the peak.
+CFS_LLAMA8B = CfsConfig("llama8b", LLAMA8B, 7, 192, 96, 2, (512, 4096), (512, 2048), 8192, 16)

@@ -82,5 +82,7 @@ def oracle_replay(sched, pool_np, region_np, first, count, mutate=True):
         in_off = [sched.slot_offsets[p] for p in sl.in_prompts]
         assert oracle.swap_out(d, pool_np, sl.out_tables, region_np, out_off) == 0
         assert oracle.swap_in(d, pool_np, sl.in_tables, region_np, in_off) == 0
+        if sl.grow:
+            wl.apply_growth(torch.from_numpy(pool_np), sched, s)
         if mutate:
             apply_mutations_host(sched, s, pool_np, region_np)

@@ -1,0 +1,144 @@
+"""GPU parity of the swaps that fair scheduling issues (Aqua, section 7):
+the rescheduler's page-outs and page-ins become block-level swap calls,
+the slice's compute stand-in grows the residents' KV between them.
+
+* small pool: the whole run, then the pool and offload region bit for bit
+  against the oracle's replay of the same schedule;
+* Llama-3-8B-shaped pool at full size: the first slices of the run, then a
+  sample of resident chunks and swapped-out image chunks against the values
+  the generator defines for them (no other write touches them).
+"""
+import os
+import time
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import cfs as ocfs
+from paper_2407_21255_amd import aqua
+from paper_2407_21255_amd import cfs
+from paper_2407_21255_amd import workload as wl
+from paper_2407_21255_amd.cycle import run_slices, slice_tables
+from tests.checkers import assert_bytes_equal
+from tests.gpu_util import apply_mutations_device, device_pool, host, oracle_replay, \
+    region_for, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    aqua.load()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _schedule(cfg):
+    tr = cfg.trace()
+    sh = cfg.shape
+    args = (sh.num_blocks, sh.block_tokens, cfg.batch_tokens, cfg.decode_slots(tr), cfg.k)
+    log, _ = cfs.run_trace(tr, *args)
+    assert log == ocfs.simulate(tr, *args), "rescheduler differs from the oracle's"
+    return tr, wl.cfs_swap_schedule(sh, cfg.seed, tr, log)
+
+
+def test_cfs_schedule_small_whole_run():
+    cfg = wl.CFS_SMALL
+    sh = cfg.shape
+    tr, sched = _schedule(cfg)
+    n = len(sched.slices)
+    say("cfs small:", n, "slices")
+    pool = device_pool(sh, cfg.seed)
+    region = region_for(sched)
+    pool_h, region_h = host(pool), host(region)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(sh.as_tuple(), pool)
+
+    def between(k):
+        wl.apply_growth(pool, sched, k)
+        apply_mutations_device(sched, k, pool, region)
+
+    try:
+        run_slices(kv, region, sched, 0, n, sa, sb, between=between)
+        torch.cuda.synchronize()
+        st = kv.stats()
+        say("cfs small on GPU", st)
+        oracle_replay(sched, pool_h, region_h, 0, n)
+        assert_bytes_equal(host(region), region_h, "offload region")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["calls_out"] == n and st["calls_in"] == n
+        assert st["bytes_out"] == sum(len(t) for sl in sched.slices for t in sl.out_tables) * \
+            sh.num_layers * sh.chunk_bytes
+    finally:
+        kv.close()
+
+
+def _expected(sh, seed, keys):
+    k = torch.from_numpy(np.ascontiguousarray(keys, dtype=np.uint64).view(np.int64))
+    return wl.chunk_values(k, sh.chunk_bytes, sh.dtype).numpy()
+
+
+def test_cfs_schedule_llama8b_sampled():
+    cfg = wl.CFS_LLAMA8B
+    sh = cfg.shape
+    L, N, C = sh.num_layers, sh.num_blocks, sh.chunk_bytes
+    tr, sched = _schedule(cfg)
+    n = int(os.environ.get("AQUA_TEST_CFS_SLICES", "60"))
+    t0 = time.time()
+    pool = device_pool(sh, cfg.seed)
+    region = region_for(sched)
+    torch.cuda.synchronize()
+    say("cfs llama8b inputs ready", round(time.time() - t0, 1), "s; running", n, "of",
+        len(sched.slices), "slices")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(sh.as_tuple(), pool)
+    try:
+        prepared = [slice_tables(sched, k) for k in range(n)]
+        run_slices(kv, region, sched, 0, n, sa, sb,
+                   between=lambda k: wl.apply_growth(pool, sched, k), prepared=prepared)
+        torch.cuda.synchronize()
+        st = kv.stats()
+        say("cfs llama8b on GPU", round(time.time() - t0, 1), "s", st)
+        assert st["bytes_out"] > 100 * 2 ** 30, "the sampled slices must page real volume"
+        rng = np.random.default_rng(720)
+        last = sched.slices[n - 1]
+        # Resident chunks: live key (prompt, layer, logical block).
+        res = [(p, i) for p in last.resident_after for i in range(len(last.tables_after[p]))]
+        pick = rng.choice(len(res), size=min(384, len(res)), replace=False)
+        lay = rng.integers(0, L, size=len(pick))
+        pi = np.asarray([res[j] for j in pick], dtype=np.int64)
+        blocks = np.asarray([last.tables_after[p][i] for p, i in pi], dtype=np.int64)
+        want = _expected(sh, cfg.seed, wl.chunk_keys_np(cfg.seed, wl.TAG_LIVE, pi[:, 0], lay,
+                                                        pi[:, 1]))
+        P = pool.view(L, N, C)
+        got = P[torch.from_numpy(lay).cuda(), torch.from_numpy(blocks).cuda()].cpu().numpy()
+        assert_bytes_equal(got, want, "resident chunks")
+        # Swapped-out images: the last image each such prompt wrote.
+        image = {}
+        for sl in sched.slices[:n]:
+            for p, t in zip(sl.out_prompts, sl.out_tables):
+                image[p] = len(t)
+            for p in sl.in_prompts:
+                image.pop(p)
+        finished = {p for sl in sched.slices[:n] for p in sl.finished}
+        out = [(p, i) for p, m in image.items() if p not in finished and p not in
+               last.tables_after for i in range(m)]
+        assert out, "some prompts are swapped out at this point"
+        pick = rng.choice(len(out), size=min(384, len(out)), replace=False)
+        po = np.asarray([out[j] for j in pick], dtype=np.int64)
+        lay = rng.integers(0, L, size=len(pick))
+        offs = np.asarray([sched.slot_offsets[p] + (l * image[p] + i) * C
+                           for (p, i), l in zip(po, lay)], dtype=np.int64)
+        idx = torch.from_numpy(offs).cuda().reshape(-1, 1) + torch.arange(C, device="cuda")
+        got = region[idx.reshape(-1)].view(-1, C).cpu().numpy()
+        want = _expected(sh, cfg.seed, wl.chunk_keys_np(cfg.seed, wl.TAG_LIVE, po[:, 0], lay,
+                                                        po[:, 1]))
+        assert_bytes_equal(got, want, "swapped-out image chunks")
+        say("cfs llama8b sampled check ok", len(res), "resident chunks,", len(out), "image chunks")
+    finally:
+        kv.close()
+        del pool, region
+        torch.cuda.empty_cache()
