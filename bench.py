@@ -54,6 +54,15 @@ WORKLOADS = {
                     "32768-token prompt swapped out to an HBM offload region and back",
     "llama70b_host": "Llama-3-70B-shaped KV, bf16: one 32768-token prompt swapped out to "
                      "pinned host memory and back",
+    "llama70b_tp2_hbm": "one tensor-parallel rank of a TP2 Llama-3-70B (80 layers, 4 KV heads, "
+                        "bf16, 32 KiB chunks, 4096-block pool): one 32768-token prompt "
+                        "swapped out to an HBM offload region and back",
+    "llama70b_tp4_hbm": "one tensor-parallel rank of a TP4 Llama-3-70B (80 layers, 2 KV heads, "
+                        "bf16, 16 KiB chunks, 4096-block pool): one 32768-token prompt "
+                        "swapped out to an HBM offload region and back",
+    "llama8b_fp8_hbm": "Llama-3-8B-shaped fp8 e4m3 KV (32 KiB chunks, 16384-block pool): 8 of "
+                       "16 fragmented 2048-token prompts swapped out to an HBM offload region "
+                       "and back into fresh blocks",
     "tiny": "4 layers, 8 KV heads, head_dim 128, block 16, fp16, 256-block pool: one "
             "512-token prompt out to an HBM buffer and back",
     "prefix": "prefill caching on a Yi-34B-shaped pool (60 layers, 8 KV heads, head_dim 128, "
@@ -82,6 +91,9 @@ def _case(name):
         "llama8b_host": lambda: (wl.llama8b_host_case(), True),
         "llama70b_hbm": lambda: (wl.llama70b_case(), False),
         "llama70b_host": lambda: (wl.llama70b_case(), True),
+        "llama70b_tp2_hbm": lambda: (wl.llama70b_case(shape=wl.LLAMA70B_TP2), False),
+        "llama70b_tp4_hbm": lambda: (wl.llama70b_case(shape=wl.LLAMA70B_TP4), False),
+        "llama8b_fp8_hbm": lambda: (wl.llama8b_hbm_case(shape=wl.LLAMA8B_FP8), False),
         "tiny": lambda: (wl.tiny_case(), False),
     }[name]()
 

@@ -278,6 +278,9 @@ TINY = KVShape(4, 256, 8, 16, 128, F16)
 LLAMA8B = KVShape(32, 16384, 8, 16, 128, BF16)
 LLAMA70B = KVShape(80, 4096, 8, 16, 128, BF16)
 LLAMA8B_FP8 = KVShape(32, 16384, 8, 16, 128, FP8_E4M3)
+# One tensor-parallel rank's share of the 70B pool: H/TP KV heads per rank.
+LLAMA70B_TP2 = KVShape(80, 4096, 4, 16, 128, BF16)
+LLAMA70B_TP4 = KVShape(80, 4096, 2, 16, 128, BF16)
 # Yi-34B (public configuration: 60 layers, 8 KV heads, head_dim 128), bf16:
 # 240 KiB of KV per token; an 8192-block pool holds 131072 tokens.
 YI34B = KVShape(60, 8192, 8, 16, 128, BF16)

@@ -71,8 +71,9 @@ def apply_mutations_device(sched, s, pool_t, region_t):
         region_t[o:o + n].fill_(wl.CONSUMED_BYTE)
 
 
-def oracle_replay(sched, pool_np, region_np, first, count, mutate=True):
-    """The oracle's run of slices [first, first+count) in issue order."""
+def oracle_replay(sched, pool_np, region_np, first, count, mutate=True, grow=True):
+    """The oracle's run of slices [first, first+count) in issue order; the
+    compute stand-in (KV growth, mutations) between slices where asked."""
     d = odesc(sched.shape)
     for s in range(first, first + count):
         if (s - first) % 10 == 0:
@@ -82,7 +83,7 @@ def oracle_replay(sched, pool_np, region_np, first, count, mutate=True):
         in_off = [sched.slot_offsets[p] for p in sl.in_prompts]
         assert oracle.swap_out(d, pool_np, sl.out_tables, region_np, out_off) == 0
         assert oracle.swap_in(d, pool_np, sl.in_tables, region_np, in_off) == 0
-        if sl.grow:
+        if grow and sl.grow:
             wl.apply_growth(torch.from_numpy(pool_np), sched, s)
         if mutate:
             apply_mutations_host(sched, s, pool_np, region_np)

@@ -45,17 +45,24 @@ def _schedule(cfg):
     return tr, wl.cfs_swap_schedule(sh, cfg.seed, tr, log)
 
 
-def test_cfs_schedule_small_whole_run():
+@pytest.mark.parametrize("where", ["hbm", "staged", "zero_copy"])
+def test_cfs_schedule_small_whole_run(where):
     cfg = wl.CFS_SMALL
     sh = cfg.shape
     tr, sched = _schedule(cfg)
     n = len(sched.slices)
-    say("cfs small:", n, "slices")
+    say("cfs small:", n, "slices,", where)
     pool = device_pool(sh, cfg.seed)
     region = region_for(sched)
+    if where != "hbm":
+        pinned = torch.empty(region.numel(), dtype=torch.uint8, pin_memory=True)
+        pinned.copy_(region.cpu())
+        region = pinned
     pool_h, region_h = host(pool), host(region)
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     kv = aqua.KVPool(sh.as_tuple(), pool)
+    if where != "hbm":
+        kv.set_host_path(aqua.AQUA_HOST_STAGED if where == "staged" else aqua.AQUA_HOST_ZERO_COPY)
 
     def between(k):
         wl.apply_growth(pool, sched, k)
@@ -72,6 +79,37 @@ def test_cfs_schedule_small_whole_run():
         assert st["calls_out"] == n and st["calls_in"] == n
         assert st["bytes_out"] == sum(len(t) for sl in sched.slices for t in sl.out_tables) * \
             sh.num_layers * sh.chunk_bytes
+    finally:
+        kv.close()
+
+
+def test_cfs_schedule_small_without_host_syncs():
+    """Every reschedule's swaps issued back to back on two streams with no
+    host synchronisation and no compute in between: the swap-ins of one
+    reschedule reuse blocks that its own and earlier swap-outs still read,
+    and only the library's waits keep the end state equal to the oracle's
+    sequential replay."""
+    cfg = wl.CFS_SMALL
+    sh = cfg.shape
+    tr, sched = _schedule(cfg)
+    n = len(sched.slices)
+    pool = device_pool(sh, cfg.seed)
+    region = region_for(sched)
+    pool_h, region_h = host(pool), host(region)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(sh.as_tuple(), pool)
+    try:
+        for k in range(n):
+            out, out_off, inn, in_off = slice_tables(sched, k)
+            kv.swap_out(out, region, out_off, stream=sa)
+            kv.swap_in(inn, region, in_off, stream=sb)
+        kv.sync(0)
+        st = kv.stats()
+        say("cfs small unsynchronised", st)
+        oracle_replay(sched, pool_h, region_h, 0, n, mutate=False, grow=False)
+        assert_bytes_equal(host(region), region_h, "offload region")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["waits_inserted"] > 0
     finally:
         kv.close()
 

@@ -101,6 +101,19 @@ def test_llama70b_hbm_full():
     _full_round_trip(wl.llama70b_case(), pinned=False)
 
 
+@pytest.mark.parametrize("shape", [wl.LLAMA70B_TP2, wl.LLAMA70B_TP4, wl.LLAMA8B_FP8],
+                         ids=["70b_tp2", "70b_tp4", "8b_fp8"])
+def test_smaller_chunks_hbm_full(shape):
+    """One tensor-parallel rank's share of the 70B pool (32 and 16 KiB
+    chunks) and the fp8 8B pool (32 KiB chunks): a workgroup's 64 KiB pass
+    covers one chunk partly, so the ragged tail path carries the copy."""
+    if shape.num_layers == 80:
+        case = wl.llama70b_case(shape=shape)
+    else:
+        case = wl.llama8b_hbm_case(shape=shape)
+    _full_round_trip(case, pinned=False)
+
+
 @pytest.mark.parametrize("path", ["zero_copy", "staged"])
 def test_llama70b_pinned_host_full(path):
     """The 10 GiB image of one 32768-token prompt in pinned host memory."""
