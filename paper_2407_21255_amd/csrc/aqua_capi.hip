@@ -341,6 +341,7 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     L.chunk_bytes = p->shape.C;
     L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
     L.max_workgroups = p->max_wg[target];
+    L.nt_pool_store = p->shape.C >= aqua::kNtPoolStoreMinChunk;
     return L;
 }
 

@@ -21,7 +21,13 @@ struct SwapLaunch {
     uint64_t chunk_bytes;     // C
     uint64_t pool_lstride;    // N * C
     uint32_t max_workgroups;  // 0: one workgroup per (layer, run)
+    bool nt_pool_store;       // scatter: nontemporal stores into the pool
 };
+
+// Scatter store hint for a pool of chunk_bytes-sized chunks: measured on
+// MI355X, nontemporal pool stores shorten the scatter by up to 5 % for 64 KiB
+// chunks and lengthen it by 10 % for the 32 KiB chunks of an fp8 pool.
+constexpr uint64_t kNtPoolStoreMinChunk = 64ull << 10;
 
 // Enqueues the copy on `stream`; returns the first launch error.
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream);

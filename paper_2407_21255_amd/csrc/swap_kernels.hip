@@ -9,7 +9,9 @@
 // The run descriptor is uniform across the workgroup and is fetched with
 // scalar loads.  The offload side is written (swap-out) or read (swap-in) with
 // nontemporal hints: it is touched once and should not displace the pool's
-// working set in L2 and MALL.
+// working set in L2 and MALL.  The gather's pool loads are nontemporal too;
+// the scatter's pool stores are nontemporal for chunks of 64 KiB and more,
+// where that measured faster, and ordinary stores below.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -42,9 +44,8 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #ifndef AQUA_NT_IN_LD    // swap-in: image loads
 #define AQUA_NT_IN_LD 1
 #endif
-#ifndef AQUA_NT_IN_ST    // swap-in: pool stores
-#define AQUA_NT_IN_ST 0
-#endif
+// Swap-in pool stores: nontemporal or not is chosen per launch
+// (SwapLaunch::nt_pool_store).
 
 constexpr int kThreads = AQUA_THREADS;
 constexpr int kUnroll = AQUA_UNROLL;
@@ -90,13 +91,14 @@ __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
     }
 }
 
-// OUT: pool -> image (gather).  !OUT: image -> pool (scatter).
+// OUT: pool -> image (gather).  !OUT: image -> pool (scatter), with
+// nontemporal pool stores when NT_POOL_ST.
 // Work unit u in [0, units) is (layer l0 + u / ndesc, descriptor u % ndesc);
 // layer l of the image side starts img_l0 layers before img_off's origin
 // (0 for whole images, the first staged layer for a staging slot);
 // consecutive workgroups take consecutive runs of one layer, so the image
 // side of a gather is written front to back.
-template <bool OUT, int UNROLL>
+template <bool OUT, int UNROLL, bool NT_POOL_ST>
 __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
     uint8_t* __restrict__ pool, uint8_t* __restrict__ img,
     const RunDesc* __restrict__ descs, uint32_t ndesc, uint32_t l0, uint32_t img_l0,
@@ -112,7 +114,7 @@ __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
             copy_span<UNROLL, AQUA_NT_OUT_LD, AQUA_NT_OUT_ST>(
                 reinterpret_cast<const v4u*>(p), reinterpret_cast<v4u*>(m), nvec);
         else
-            copy_span<UNROLL, AQUA_NT_IN_LD, AQUA_NT_IN_ST>(
+            copy_span<UNROLL, AQUA_NT_IN_LD, NT_POOL_ST>(
                 reinterpret_cast<const v4u*>(m), reinterpret_cast<v4u*>(p), nvec);
     }
 }
@@ -154,13 +156,17 @@ hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
         uint32_t grid = units;
         if (a.max_workgroups && grid > a.max_workgroups) grid = a.max_workgroups;
         if (a.out)
-            hipLaunchKernelGGL((swap_runs_kernel<true, kUnroll>), dim3(grid), dim3(kThreads), 0,
-                               stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
-                               a.chunk_bytes, a.pool_lstride);
+            hipLaunchKernelGGL((swap_runs_kernel<true, kUnroll, false>), dim3(grid),
+                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
+                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
+        else if (a.nt_pool_store)
+            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll, true>), dim3(grid),
+                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
+                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
         else
-            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll>), dim3(grid), dim3(kThreads), 0,
-                               stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
-                               a.chunk_bytes, a.pool_lstride);
+            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll, false>), dim3(grid),
+                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
+                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
