@@ -114,6 +114,10 @@ class CfsScheduler:
             self.pending = True          # no resident can grow: re-form now
         idx, tok = self._partition(cands, np.zeros(len(cands), dtype=np.int64),
                                    self.pool_blocks)
+        if len(idx) == 0:
+            # Only a prompt whose context no longer fits the whole pool can
+            # block every admission; the engine must bound context lengths.
+            raise RuntimeError("no request fits the pool: a context has outgrown it")
         members = np.sort(idx)
         out = np.setdiff1d(self.resident, members, assume_unique=True)
         inn = np.setdiff1d(members, self.resident, assume_unique=True)

@@ -160,3 +160,29 @@ def test_swap_schedule_conserves_blocks(cfg):
         tables = {p: list(t) for p, t in sl.tables_after.items()}
     assert e is None
     assert all(c == p + o for c, (_, p, o) in zip(ctx, tr))
+
+
+def test_rescheduler_fails_loudly_when_a_context_outgrows_the_pool():
+    """A request that keeps generating past what the pool holds can never be
+    admitted again; the scheduler raises instead of spinning."""
+    s = cfs.CfsScheduler(pool_blocks=4, block_tokens=4, batch_tokens=8, decode_slots=2, k=4)
+    s.add(8)
+    now = 0
+    with pytest.raises(RuntimeError, match="outgrown"):
+        for _ in range(100):
+            st = s.step(now)
+            s.advance(st, [])
+            now += 1
+    assert s.generated[0] >= 8       # it ran until its context filled the pool
+
+
+def test_scheduler_rejects_bad_settings_and_prompts():
+    with pytest.raises(ValueError):
+        cfs.CfsScheduler(0, 16, 64, 2, 4)
+    s = cfs.CfsScheduler(4, 4, 8, 2, 4)
+    with pytest.raises(ValueError):
+        s.add(0)
+    with pytest.raises(ValueError):
+        s.add(17)                     # 5 blocks > 4
+    with pytest.raises(ValueError):
+        cfs.run_trace([(0, 4, 13)], 4, 4, 8, 2, 4)    # prompt + output > pool
