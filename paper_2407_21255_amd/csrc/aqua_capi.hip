@@ -25,17 +25,6 @@ constexpr uint64_t kDefaultUnitBytes = 64ull << 10;
 constexpr uint64_t kDefaultSlotBytes = 256ull << 20;  // staged path, per slot
 constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 
-// How run descriptors reach the kernels.  2 (shipped): the kernels read
-// them straight from the pinned, coherent host ring -- one 32-byte scalar
-// load per workgroup, and no copy on the call's stream; staged host calls
-// copy them to the device ring instead (the link is busy with their data).
-// 0 and 1 exist for measurement: 0 copies them to the device ring on the
-// call's stream, 1 on the library's upload stream, which the call's stream
-// then waits for.
-#ifndef AQUA_DESC_MODE
-#define AQUA_DESC_MODE 2
-#endif
-
 uint64_t env_u64(const char* name, uint64_t dflt) {
     const char* v = std::getenv(name);
     if (!v || !*v) return dflt;
@@ -47,7 +36,7 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
 struct Outstanding {
     uint64_t ticket;
     hipEvent_t ev;                 // recorded on the call's stream, last
-    std::vector<hipEvent_t> aux;   // events inside the call (staging, uploads)
+    std::vector<hipEvent_t> aux;   // events inside the call (staging slots)
 };
 
 struct RingUse {
@@ -79,9 +68,11 @@ struct aqua_kv_pool {
     std::vector<std::deque<Outstanding>> outstanding;   // per lane, in order
     std::vector<hipEvent_t> spare_events;
 
-    // Run descriptors: a pinned host ring (read by the kernels directly, or
-    // copied to a device ring in the measurement modes).
-    hipStream_t upload = nullptr;
+    // Run descriptors reach the kernels through a pinned, coherent host ring:
+    // the kernels read them in place (one 32-byte scalar load per workgroup,
+    // no copy on the call's stream), except for calls that keep the host
+    // link busy with their data (staged host swaps, migrations), whose
+    // descriptors are copied to the device ring first.
     uint8_t* ring_host_dev = nullptr;  // device address of ring_host
     uint8_t* ring_host = nullptr;
     uint8_t* ring_dev = nullptr;
@@ -218,9 +209,9 @@ void free_rings(aqua_kv_pool* p) {
 }
 
 aqua_status alloc_rings(aqua_kv_pool* p, uint64_t bytes) {
-    // The device ring serves the staged host path (and the measurement
-    // modes): there the copy engines keep the host link busy, and
-    // descriptors fetched over it would stall the gathers.
+    // The device ring serves calls that keep the host link busy (staged
+    // host swaps, migrations): descriptors fetched over it would stall
+    // their kernels.
     hipError_t e = hipMalloc((void**)&p->ring_dev, bytes);
     if (e == hipSuccess)
         e = hipHostMalloc((void**)&p->ring_host, bytes,
@@ -577,20 +568,6 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
             e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
                                hipMemcpyHostToDevice, stream);
         }
-#if AQUA_DESC_MODE == 0
-        descs = p->ring_dev + ring_off;
-        e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
-                           hipMemcpyHostToDevice, stream);
-#elif AQUA_DESC_MODE == 1
-        descs = p->ring_dev + ring_off;
-        hipEvent_t up_ev = nullptr;
-        e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
-                           hipMemcpyHostToDevice, p->upload);
-        if (e == hipSuccess) e = take_event(p, &up_ev);
-        if (e == hipSuccess) rec.aux.push_back(up_ev);
-        if (e == hipSuccess) e = hipEventRecord(up_ev, p->upload);
-        if (e == hipSuccess) e = hipStreamWaitEvent(stream, up_ev, 0);
-#endif
         if (e != hipSuccess) return latch(p, e);
         if (staged) {
             st = enqueue_staged(p, is_in, buf, stream, reinterpret_cast<const RunDesc*>(descs),
@@ -790,13 +767,6 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     if (p->unit_bytes > aqua::kMaxChunkBytes) p->unit_bytes = aqua::kMaxChunkBytes;
     p->slot_target = env_u64("AQUA_STAGE_SLOT_BYTES", kDefaultSlotBytes);
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
-#if AQUA_DESC_MODE == 1
-    if (st == AQUA_OK && hipStreamCreateWithFlags(&p->upload, hipStreamNonBlocking) != hipSuccess) {
-        (void)hipGetLastError();
-        free_rings(p);
-        st = AQUA_ERR_HIP;
-    }
-#endif
     if (st != AQUA_OK) {
         delete p;
         return st;
@@ -820,7 +790,6 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
         free_rings(p);
         if (p->staging) (void)hipFree(p->staging);
         if (p->copy) (void)hipStreamDestroy(p->copy);
-        if (p->upload) (void)hipStreamDestroy(p->upload);
         if (p->sticky != hipSuccess) st = AQUA_ERR_HIP;
     }
     delete p;
