@@ -397,7 +397,6 @@ def _time_slices(sched, pool, region, ids, warmup):
 
 
 def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, config):
-    import numpy as np
     from paper_2407_21255_amd import workload as wl
 
     moved = float(out_b.sum() + in_b.sum())
@@ -460,7 +459,6 @@ def run_cycle(args, res_common):
 def run_cfs(args, res_common):
     """Fair scheduling of a burst on the 8B-shaped pool: the rescheduler's
     page-outs and page-ins, slice by slice, for the slices that swap."""
-    import numpy as np
     import torch
 
     from paper_2407_21255_amd import cfs

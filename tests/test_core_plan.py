@@ -1,6 +1,5 @@
 """Host core on the CPU: validation parity with the oracle, and the run plan."""
 import numpy as np
-import pytest
 
 import oracle
 from tests import core_lib

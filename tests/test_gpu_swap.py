@@ -1,7 +1,6 @@
 """GPU parity: the HIP gather/scatter path against the CPU oracle, byte for
 byte, through the C ABI.  Every input comes from the seeded generator; every
 expected value from the oracle run on a host copy of the same input."""
-import os
 
 import numpy as np
 import pytest
