@@ -119,32 +119,15 @@ def _expected(sh, seed, keys):
     return wl.chunk_values(k, sh.chunk_bytes, sh.dtype).numpy()
 
 
-def test_cfs_schedule_llama8b_sampled():
-    cfg = wl.CFS_LLAMA8B
+def _sample_check(sched, cfg, pool, region, k, rng):
+    """Resident chunks and swapped-out image chunks after reschedule k hold
+    the generator's values for their (prompt, layer, logical block).
+    Returns the number of chunks each sample could draw from."""
     sh = cfg.shape
     L, N, C = sh.num_layers, sh.num_blocks, sh.chunk_bytes
-    tr, sched = _schedule(cfg)
-    n = int(os.environ.get("AQUA_TEST_CFS_SLICES", "60"))
-    t0 = time.time()
-    pool = device_pool(sh, cfg.seed)
-    region = region_for(sched)
-    torch.cuda.synchronize()
-    say("cfs llama8b inputs ready", round(time.time() - t0, 1), "s; running", n, "of",
-        len(sched.slices), "slices")
-    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
-    kv = aqua.KVPool(sh.as_tuple(), pool)
-    try:
-        prepared = [slice_tables(sched, k) for k in range(n)]
-        run_slices(kv, region, sched, 0, n, sa, sb,
-                   between=lambda k: wl.apply_growth(pool, sched, k), prepared=prepared)
-        torch.cuda.synchronize()
-        st = kv.stats()
-        say("cfs llama8b on GPU", round(time.time() - t0, 1), "s", st)
-        assert st["bytes_out"] > 100 * 2 ** 30, "the sampled slices must page real volume"
-        rng = np.random.default_rng(720)
-        last = sched.slices[n - 1]
-        # Resident chunks: live key (prompt, layer, logical block).
-        res = [(p, i) for p in last.resident_after for i in range(len(last.tables_after[p]))]
+    last = sched.slices[k]
+    res = [(p, i) for p in last.resident_after for i in range(len(last.tables_after[p]))]
+    if res:
         pick = rng.choice(len(res), size=min(384, len(res)), replace=False)
         lay = rng.integers(0, L, size=len(pick))
         pi = np.asarray([res[j] for j in pick], dtype=np.int64)
@@ -153,18 +136,18 @@ def test_cfs_schedule_llama8b_sampled():
                                                         pi[:, 1]))
         P = pool.view(L, N, C)
         got = P[torch.from_numpy(lay).cuda(), torch.from_numpy(blocks).cuda()].cpu().numpy()
-        assert_bytes_equal(got, want, "resident chunks")
-        # Swapped-out images: the last image each such prompt wrote.
-        image = {}
-        for sl in sched.slices[:n]:
-            for p, t in zip(sl.out_prompts, sl.out_tables):
-                image[p] = len(t)
-            for p in sl.in_prompts:
-                image.pop(p)
-        finished = {p for sl in sched.slices[:n] for p in sl.finished}
-        out = [(p, i) for p, m in image.items() if p not in finished and p not in
-               last.tables_after for i in range(m)]
-        assert out, "some prompts are swapped out at this point"
+        assert_bytes_equal(got, want, f"resident chunks after reschedule {k}")
+    # Swapped-out images: the last image each such prompt wrote.
+    image = {}
+    for sl in sched.slices[:k + 1]:
+        for p, t in zip(sl.out_prompts, sl.out_tables):
+            image[p] = len(t)
+        for p in sl.in_prompts:
+            image.pop(p)
+    finished = {p for sl in sched.slices[:k + 1] for p in sl.finished}
+    out = [(p, i) for p, m in image.items() if p not in finished and p not in
+           last.tables_after for i in range(m)]
+    if out:
         pick = rng.choice(len(out), size=min(384, len(out)), replace=False)
         po = np.asarray([out[j] for j in pick], dtype=np.int64)
         lay = rng.integers(0, L, size=len(pick))
@@ -174,8 +157,44 @@ def test_cfs_schedule_llama8b_sampled():
         got = region[idx.reshape(-1)].view(-1, C).cpu().numpy()
         want = _expected(sh, cfg.seed, wl.chunk_keys_np(cfg.seed, wl.TAG_LIVE, po[:, 0], lay,
                                                         po[:, 1]))
-        assert_bytes_equal(got, want, "swapped-out image chunks")
-        say("cfs llama8b sampled check ok", len(res), "resident chunks,", len(out), "image chunks")
+        assert_bytes_equal(got, want, f"swapped-out image chunks after reschedule {k}")
+    return len(res), len(out)
+
+
+def test_cfs_schedule_llama8b_sampled():
+    """The 8B burst at full size, in segments of 60 reschedules (60 by
+    default, the whole run of 349 with AQUA_TEST_CFS_SLICES=349), with a
+    sampled check after each segment."""
+    cfg = wl.CFS_LLAMA8B
+    sh = cfg.shape
+    tr, sched = _schedule(cfg)
+    n = min(len(sched.slices), int(os.environ.get("AQUA_TEST_CFS_SLICES", "60")))
+    t0 = time.time()
+    pool = device_pool(sh, cfg.seed)
+    region = region_for(sched)
+    torch.cuda.synchronize()
+    say("cfs llama8b inputs ready", round(time.time() - t0, 1), "s; running", n, "of",
+        len(sched.slices), "slices")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(sh.as_tuple(), pool)
+    rng = np.random.default_rng(720)
+    try:
+        checked = 0
+        for a in range(0, n, 60):
+            b = min(n, a + 60)
+            prepared = {k: slice_tables(sched, k) for k in range(a, b)}
+            run_slices(kv, region, sched, a, b - a, sa, sb,
+                       between=lambda k: wl.apply_growth(pool, sched, k),
+                       prepared=[prepared.get(k) for k in range(b)])
+            torch.cuda.synchronize()
+            nres, nout = _sample_check(sched, cfg, pool, region, b - 1, rng)
+            checked += bool(nres) + bool(nout)
+            say("cfs llama8b after reschedule", b - 1, round(time.time() - t0, 1), "s:",
+                nres, "resident chunks,", nout, "image chunks sampled from")
+        st = kv.stats()
+        say("cfs llama8b on GPU", st)
+        assert st["bytes_out"] > 100 * 2 ** 30, "the sampled slices must page real volume"
+        assert checked >= 2
     finally:
         kv.close()
         del pool, region
