@@ -78,6 +78,8 @@ WORKLOADS = {
            "completion) of a 192-request burst on a Llama-3-8B-shaped bf16 pool (16384 "
            "blocks, 2x oversubscribed): each reschedule swaps the prompts leaving the batch "
            "out and those rejoining it in",
+    "cycle_host": "the preemption cycle with pinned host memory as swap space: each slice "
+                  "swaps 16 prompts out to host memory on one stream and 16 in on another",
     "cycle": "time-sliced preemption on a Llama-3-8B-shaped fp8 e4m3 pool (16384 blocks): "
              "64 prompts of 128..8192 tokens, each slice swaps the 16 longest-resident out "
              "on one stream and the 16 longest-waiting in on another",
@@ -343,7 +345,7 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
     return out
 
 
-def _time_slices(sched, pool, region, ids, warmup):
+def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     """Issues slices ``ids`` of a swap schedule (the first ``warmup`` of them
     untimed): out on one stream, in on another, ``aqua_sync`` at the end of
     each, as a scheduler's loop boundary does.  (Issued without it, slices
@@ -359,6 +361,9 @@ def _time_slices(sched, pool, region, ids, warmup):
     prepared = {k: slice_tables(sched, k) for k in ids}
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
+    if host_path is not None:
+        kv.set_host_path(aqua.AQUA_HOST_STAGED if host_path == "staged"
+                         else aqua.AQUA_HOST_ZERO_COPY)
     evs = []
 
     def one(k, timed):
@@ -396,13 +401,17 @@ def _time_slices(sched, pool, region, ids, warmup):
     return wall, st, out_b, in_b, out_ms, in_ms
 
 
-def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, config):
+def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, config,
+                  host=False):
     from paper_2407_21255_amd import workload as wl
 
     moved = float(out_b.sum() + in_b.sum())
     ok = out_b > 0
-    # Gather rate of each slice (its bytes are read and written once).
-    achieved = float((2 * out_b[ok] / (out_ms[ok] * 1e-3)).mean()) / 1e9 if ok.any() else 0.0
+    # Gather rate of each slice: its bytes are read and written once in HBM,
+    # or cross the host link once.
+    per = 1 if host else 2
+    achieved = float((per * out_b[ok] / (out_ms[ok] * 1e-3)).mean()) / 1e9 if ok.any() else 0.0
+    peak = HOST_LINK_PEAK_GBS if host else HBM_PEAK_GBS
     res = dict(res_common)
     res.update({
         "value": round(moved / wall / 1e9, 2),
@@ -410,16 +419,17 @@ def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, co
         "dtype": wl.DTYPE_NAME[s.dtype],
         "config": config,
         "roofline": {
-            "bound": "hbm", "kernel": "gather (swap-out), concurrent with the scatter",
-            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-            "algorithmic_bytes_per_launch": round(float(2 * out_b[ok].mean())) if ok.any()
+            "bound": "host_link" if host else "hbm",
+            "kernel": "gather (swap-out), concurrent with the scatter",
+            "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": round(float(per * out_b[ok].mean())) if ok.any()
             else 0,
         },
         "kernel_ms": {"swap_out_mean": round(float(out_ms[ok].mean()), 4) if ok.any() else 0,
                       "swap_in_mean": round(float(in_ms[in_b > 0].mean()), 4)
                       if (in_b > 0).any() else 0},
-        "slice_hbm_GBps": round(2 * moved / wall / 1e9, 1),
+        "slice_hbm_GBps": None if host else round(2 * moved / wall / 1e9, 1),
         "waits_inserted": st["waits_inserted"],
         "host_us_per_call": round(st["host_ns"] / max(1, st["calls_out"] + st["calls_in"]) / 1e3,
                                   2),
@@ -439,21 +449,28 @@ def run_cycle(args, res_common):
     s = sched.shape
     pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
     wl.fill_pool(pool, s, sched.seed, wl.schedule_owner(sched))
-    region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
-    wl.fill_region(region, sched)
+    on_host = args.workload == "cycle_host"
+    if on_host:
+        # Pinned host swap space; its contents do not change the timing.
+        region = torch.empty(sched.region_bytes, dtype=torch.uint8, pin_memory=True)
+    else:
+        region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
+        wl.fill_region(region, sched)
     torch.cuda.synchronize()
-    timed = _time_slices(sched, pool, region, list(range(n)), args.warmup)
+    timed = _time_slices(sched, pool, region, list(range(n)), args.warmup,
+                         host_path=args.host_path if on_host else None)
     out_b = timed[2]
     config = {
-        "workload": WORKLOADS["cycle"], "layers": s.num_layers,
+        "workload": WORKLOADS[args.workload], "layers": s.num_layers,
         "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
         "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
         "prompts": len(sched.nblocks), "swaps_per_slice": 16, "slices_timed": args.steps,
         "host_sync_per_slice": True,
         "mean_payload_bytes_per_direction": round(float(out_b.mean())),
-        "offload_target": "hbm", "parallelism": "single_gpu",
+        "offload_target": "pinned_host" if on_host else "hbm",
+        "host_path": args.host_path if on_host else None, "parallelism": "single_gpu",
     }
-    return _slice_result(res_common, s, *timed, args.steps, config), s
+    return _slice_result(res_common, s, *timed, args.steps, config, host=on_host), s
 
 
 def run_cfs(args, res_common):
@@ -662,7 +679,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "data": "synthetic",
     }
-    if args.workload == "cycle":
+    if args.workload in ("cycle", "cycle_host"):
         res, shape = run_cycle(args, common)
     elif args.workload == "cfs":
         res, shape = run_cfs(args, common)

@@ -243,11 +243,13 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
  *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
  *     (section 7, "Efficient context switching").  Layers pass through two
  *     HBM slots owned by the library (256 MiB each by default, allocated on
- *     the first staged call, after waiting for every outstanding call):
- *     the gather kernel fills a slot and the copy engines move it over the
- *     link while the next slot is filled, and the reverse on swap-in.  The
- *     compute units are busy only for the short gathers, so concurrent
- *     kernels keep running.
+ *     a direction's first staged call, after waiting for every outstanding
+ *     call): the gather kernel fills a slot and the runtime's copies move it
+ *     over the link while the next slot is filled, and the reverse on
+ *     swap-in.  Swap-outs and swap-ins have their own slots and copy stream,
+ *     so a swap-out and a swap-in on different streams use both directions
+ *     of the link at once.  The compute units are busy only for the short
+ *     gathers and scatters, so concurrent kernels keep running.
  *   AQUA_HOST_ZERO_COPY: the gather and scatter kernels read and write the
  *     host image directly over the link, with no HBM staging.  Their
  *     workgroups stay resident for the whole transfer, so the library caps

@@ -80,11 +80,13 @@ struct aqua_kv_pool {
     uint64_t ring_head = 0;
     std::deque<RingUse> ring_uses;
 
-    // Staged host path: two HBM slots and a copy stream for the copy engines.
+    // Staged host path, per direction (0: swap-out, device to host; 1:
+    // swap-in, host to device): two HBM slots and a copy stream, so that a
+    // swap-out and a swap-in use both directions of the link at once.
     int32_t host_path = AQUA_HOST_STAGED;
-    hipStream_t copy = nullptr;
-    uint8_t* staging = nullptr;
-    uint64_t staging_bytes = 0;
+    hipStream_t copy[2] = {nullptr, nullptr};
+    uint8_t* staging[2] = {nullptr, nullptr};
+    uint64_t staging_bytes[2] = {0, 0};
     uint64_t slot_target = kDefaultSlotBytes;
     std::vector<StagedSeq> sseq;
     std::vector<uint64_t> slot_offsets;  // per sequence, in a slot
@@ -261,26 +263,27 @@ aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off) {
     return AQUA_OK;
 }
 
-// Makes the staging buffer hold at least `bytes`, waiting for every
-// outstanding call before it is replaced.
-aqua_status ensure_staging(aqua_kv_pool* p, uint64_t bytes) {
-    if (bytes <= p->staging_bytes) return AQUA_OK;
+// Makes direction dir's staging buffer hold at least `bytes`, waiting for
+// every outstanding call before it is replaced.
+aqua_status ensure_staging(aqua_kv_pool* p, int dir, uint64_t bytes) {
+    if (bytes <= p->staging_bytes[dir]) return AQUA_OK;
     aqua_status st = wait_all(p);
     if (st != AQUA_OK) return st;
-    if (p->staging) (void)hipFree(p->staging);
-    p->staging = nullptr;
-    p->staging_bytes = 0;
-    if (!p->copy && hipStreamCreateWithFlags(&p->copy, hipStreamNonBlocking) != hipSuccess) {
+    if (p->staging[dir]) (void)hipFree(p->staging[dir]);
+    p->staging[dir] = nullptr;
+    p->staging_bytes[dir] = 0;
+    if (!p->copy[dir] &&
+        hipStreamCreateWithFlags(&p->copy[dir], hipStreamNonBlocking) != hipSuccess) {
         (void)hipGetLastError();
-        p->copy = nullptr;
+        p->copy[dir] = nullptr;
         return AQUA_ERR_HIP;
     }
-    if (hipMalloc((void**)&p->staging, bytes) != hipSuccess) {
+    if (hipMalloc((void**)&p->staging[dir], bytes) != hipSuccess) {
         (void)hipGetLastError();
-        p->staging = nullptr;
+        p->staging[dir] = nullptr;
         return AQUA_ERR_HIP;
     }
-    p->staging_bytes = bytes;
+    p->staging_bytes[dir] = bytes;
     return AQUA_OK;
 }
 
@@ -336,8 +339,10 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     return L;
 }
 
-// Staged host path.  Layers go through two HBM slots of G layers each.  A
-// slot holds, sequence after sequence, the sequence's G layers in image
+// Staged host path.  Layers go through two HBM slots of G layers each
+// (per direction: swap-outs and swap-ins have their own slots and copy
+// stream, so one of each can run at once on the two directions of the
+// link).  A slot holds, sequence after sequence, the sequence's G layers in image
 // order ([G][n_s][C] at G * first_s * C), so each sequence's piece of a
 // layer group is contiguous both in the slot and in the host image: one
 // copy per sequence per group.  Swap-out: the gather fills a slot on the
@@ -361,8 +366,8 @@ hipError_t stage_copies(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t*
             uint8_t* hj = h + l * q.m * C;
             uint8_t* sj = s + (uint64_t)j * q.n * C;
             const hipError_t e =
-                to_host ? hipMemcpyAsync(hj, sj, bytes, hipMemcpyDeviceToHost, p->copy)
-                        : hipMemcpyAsync(sj, hj, bytes, hipMemcpyHostToDevice, p->copy);
+                to_host ? hipMemcpyAsync(hj, sj, bytes, hipMemcpyDeviceToHost, p->copy[0])
+                        : hipMemcpyAsync(sj, hj, bytes, hipMemcpyHostToDevice, p->copy[1]);
             if (e != hipSuccess) return e;
         }
     }
@@ -384,13 +389,14 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
     hipEvent_t start = nullptr;
     if ((e = ev(&start)) != hipSuccess) return latch(p, e);
     if ((e = hipEventRecord(start, stream)) != hipSuccess) return latch(p, e);
-    if ((e = hipStreamWaitEvent(p->copy, start, 0)) != hipSuccess) return latch(p, e);
+    hipStream_t copy = p->copy[is_in];
+    if ((e = hipStreamWaitEvent(copy, start, 0)) != hipSuccess) return latch(p, e);
 
     hipEvent_t slot_free[2] = {nullptr, nullptr};
     hipEvent_t last_copy = nullptr;
     for (uint32_t l0 = l_begin, k = 0; l0 < L; l0 += G, ++k) {
         const uint32_t nl = std::min<uint32_t>(G, L - l0);
-        uint8_t* s = p->staging + (k % 2) * slot;
+        uint8_t* s = p->staging[is_in] + (k % 2) * slot;
         // The kernels only touch HBM here: no host-link grid cap.
         aqua::SwapLaunch Lk = make_launch(p, is_in, s, descs, ndesc, AQUA_TARGET_DEVICE);
         Lk.first_layer = l0;
@@ -398,8 +404,8 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
         Lk.img_l0 = l0;
         hipEvent_t e1 = nullptr, e2 = nullptr;
         if ((e = ev(&e1)) != hipSuccess || (e = ev(&e2)) != hipSuccess) return latch(p, e);
-        hipStream_t first = is_in ? p->copy : stream;   // fills the slot
-        hipStream_t second = is_in ? stream : p->copy;  // drains it
+        hipStream_t first = is_in ? copy : stream;   // fills the slot
+        hipStream_t second = is_in ? stream : copy;  // drains it
         if (slot_free[k % 2] && (e = hipStreamWaitEvent(first, slot_free[k % 2], 0)))
             return latch(p, e);
         if (is_in) {
@@ -500,7 +506,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         c.img_offsets = p->slot_offsets.data();
         c.img_blocks = nullptr;
         aqua::plan_runs(p->shape, c, p->unit_bytes, &p->plan);
-        st = ensure_staging(p, 2 * slot);
+        st = ensure_staging(p, is_in, 2 * slot);
         if (st != AQUA_OK) return st;
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
@@ -511,7 +517,8 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         r.second += a.buf;
     }
     const std::pair<uint64_t, uint64_t> stage_range{
-        (uint64_t)(uintptr_t)p->staging, (uint64_t)(uintptr_t)p->staging + 2 * slot};
+        (uint64_t)(uintptr_t)p->staging[is_in],
+        (uint64_t)(uintptr_t)p->staging[is_in] + 2 * slot};
 
     // Reserve descriptor space before registering the ticket: a reservation
     // may wait on earlier tickets.
@@ -788,8 +795,10 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
             }
         for (hipEvent_t ev : p->spare_events) (void)hipEventDestroy(ev);
         free_rings(p);
-        if (p->staging) (void)hipFree(p->staging);
-        if (p->copy) (void)hipStreamDestroy(p->copy);
+        for (int dir = 0; dir < 2; ++dir) {
+            if (p->staging[dir]) (void)hipFree(p->staging[dir]);
+            if (p->copy[dir]) (void)hipStreamDestroy(p->copy[dir]);
+        }
         if (p->sticky != hipSuccess) st = AQUA_ERR_HIP;
     }
     delete p;
