@@ -264,6 +264,67 @@ AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* o
 /* Static text for a status code. */
 AQUA_API const char* aqua_status_str(aqua_status s);
 
+/* ---- Swap space: offload tensors with a device region and a host fallback
+ * (section 6, "Aqua Tensors", "Allocating Aqua Tensors", "Reclaiming Aqua
+ * Tensors").
+ *
+ * Offload tensors are named by handles.  A tensor's bytes live in a device
+ * region lent for offloading (the stand-in for a producer GPU's HBM) while a
+ * range of it fits, else in pinned host memory (the DRAM fallback).  Reclaim
+ * moves device tensors to host memory to hand device memory back; restore
+ * moves host tensors back into the device region while they fit.  A handle
+ * keeps its identity when its tensor moves; aqua_swap_locate gives the
+ * current pointer and target, which the swap calls take.  Moves are
+ * migrations on the space's pool (aqua_migrate), so calls on that pool issued
+ * after a move, on any stream, are ordered after it, and a freed or vacated
+ * range is reused only after the calls that still read or write it.  A
+ * pointer from aqua_swap_locate is valid until its tensor is freed or moved.
+ * Ranges are 256-byte aligned; tensor sizes are multiples of 16 bytes. */
+typedef struct aqua_swap_space* aqua_swap_space_t;
+
+/* Allocates device_bytes of device memory on the pool's GPU and host_bytes
+ * of pinned, device-mapped host memory (either may be 0).  The space must be
+ * destroyed before its pool.  AQUA_ERR_HIP if an allocation fails. */
+AQUA_API aqua_status aqua_swap_space_create(aqua_kv_pool_t pool, uint64_t device_bytes,
+                                            uint64_t host_bytes, aqua_swap_space_t* out);
+
+/* Waits for every outstanding call on the pool, then frees both regions. */
+AQUA_API aqua_status aqua_swap_space_destroy(aqua_swap_space_t space);
+
+/* A tensor of `bytes`: in the device region if a free range fits, else in
+ * host memory.  AQUA_ERR_INVALID for 0 or a size that is not a multiple of
+ * 16, AQUA_ERR_CAPACITY if neither region has room. */
+AQUA_API aqua_status aqua_swap_alloc(aqua_swap_space_t space, uint64_t bytes,
+                                     uint64_t* handle);
+
+/* Releases the tensor's range; later calls that reuse it are ordered after
+ * the calls that still use it.  AQUA_ERR_INVALID for an unknown handle. */
+AQUA_API aqua_status aqua_swap_free(aqua_swap_space_t space, uint64_t handle);
+
+/* Current place of a tensor: *ptr (device pointer for AQUA_TARGET_DEVICE,
+ * host pointer for AQUA_TARGET_HOST), its size and target; NULL outputs are
+ * skipped.  The engine uses the target to tell whether a prompt's state is
+ * on the device side or in host memory. */
+AQUA_API aqua_status aqua_swap_locate(aqua_swap_space_t space, uint64_t handle, void** ptr,
+                                      uint64_t* bytes, int32_t* target);
+
+/* Reclaim: moves device tensors (oldest handles first) to host memory until
+ * at least `bytes` of the device region is free (UINT64_MAX: every device
+ * tensor), as one migration on `stream`; *ticket (may be NULL) is its
+ * ticket, 0 if nothing had to move.  AQUA_ERR_CAPACITY, with nothing moved,
+ * if host memory cannot take the tensors that would have to move. */
+AQUA_API aqua_status aqua_swap_reclaim(aqua_swap_space_t space, uint64_t bytes, void* stream,
+                                       uint64_t* ticket);
+
+/* Restore: moves host tensors (oldest handles first) into the device region
+ * while they fit, as one migration on `stream`; *ticket as for reclaim. */
+AQUA_API aqua_status aqua_swap_restore(aqua_swap_space_t space, void* stream, uint64_t* ticket);
+
+/* Free bytes of each region and the number of live tensors in each. */
+AQUA_API aqua_status aqua_swap_usage(aqua_swap_space_t space, uint64_t* device_free,
+                                     uint64_t* host_free, uint64_t* device_tensors,
+                                     uint64_t* host_tensors);
+
 /* ---- Fair batch partitioning (section 7, "Aqua's batch partitioning
  * algorithm").  Host code: no pool, no GPU.
  *

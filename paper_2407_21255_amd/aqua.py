@@ -39,6 +39,8 @@ EXPORTS = (
     "aqua_sync", "aqua_stream_wait", "aqua_query",
     "aqua_kv_pool_set_max_workgroups", "aqua_kv_pool_set_host_path",
     "aqua_pool_stats_get", "aqua_status_str", "aqua_cfs_partition",
+    "aqua_swap_space_create", "aqua_swap_space_destroy", "aqua_swap_alloc", "aqua_swap_free",
+    "aqua_swap_locate", "aqua_swap_reclaim", "aqua_swap_restore", "aqua_swap_usage",
 )
 
 
@@ -118,6 +120,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_pool_stats_get.argtypes = [P, ctypes.POINTER(aqua_pool_stats)]
     L.aqua_cfs_partition.argtypes = [P, u32, ctypes.POINTER(aqua_cfs_params), P, P,
                                      ctypes.POINTER(u32), ctypes.POINTER(u64)]
+    L.aqua_swap_space_create.argtypes = [P, u64, u64, ctypes.POINTER(P)]
+    L.aqua_swap_space_destroy.argtypes = [P]
+    L.aqua_swap_alloc.argtypes = [P, u64, ctypes.POINTER(u64)]
+    L.aqua_swap_free.argtypes = [P, u64]
+    L.aqua_swap_locate.argtypes = [P, u64, ctypes.POINTER(P), ctypes.POINTER(u64),
+                                   ctypes.POINTER(i32)]
+    L.aqua_swap_reclaim.argtypes = [P, u64, P, ctypes.POINTER(u64)]
+    L.aqua_swap_restore.argtypes = [P, P, ctypes.POINTER(u64)]
+    L.aqua_swap_usage.argtypes = [P] + [ctypes.POINTER(u64)] * 4
     L.aqua_status_str.argtypes = [i32]
     L.aqua_status_str.restype = ctypes.c_char_p
     for n in EXPORTS:
@@ -243,7 +254,70 @@ def cfs_partition(requests, batch_tokens: int, decode_slots: int, capacity_block
     return idx[:size], tok[:size], taken
 
 
+def aqua_swap_space_create(pool, device_bytes: int, host_bytes: int):
+    h = ctypes.c_void_p()
+    st = load().aqua_swap_space_create(pool, device_bytes, host_bytes, ctypes.byref(h))
+    return st, h.value
+
+
+def aqua_swap_space_destroy(space) -> int:
+    return load().aqua_swap_space_destroy(space)
+
+
+def aqua_swap_alloc(space, nbytes: int):
+    h = ctypes.c_uint64(0)
+    st = load().aqua_swap_alloc(space, nbytes, ctypes.byref(h))
+    return st, h.value
+
+
+def aqua_swap_free(space, handle: int) -> int:
+    return load().aqua_swap_free(space, handle)
+
+
+def aqua_swap_locate(space, handle: int):
+    """(status, pointer, bytes, target)."""
+    ptr, nb, tg = ctypes.c_void_p(), ctypes.c_uint64(0), ctypes.c_int32(0)
+    st = load().aqua_swap_locate(space, handle, ctypes.byref(ptr), ctypes.byref(nb),
+                                 ctypes.byref(tg))
+    return st, ptr.value, nb.value, tg.value
+
+
+def aqua_swap_reclaim(space, nbytes: int, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_reclaim(space, nbytes, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_restore(space, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_restore(space, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_usage(space):
+    """(status, device free bytes, host free bytes, device tensors, host tensors)."""
+    v = [ctypes.c_uint64(0) for _ in range(4)]
+    st = load().aqua_swap_usage(space, *[ctypes.byref(x) for x in v])
+    return (st, *[x.value for x in v])
+
+
 # -- torch-facing wrapper ------------------------------------------------------
+
+class RawBuffer:
+    """A byte buffer the library placed (a swap-space tensor), usable where
+    the swap calls take a tensor."""
+
+    def __init__(self, ptr: int, nbytes: int, target: int):
+        self.ptr, self.nbytes, self.aqua_target = ptr, nbytes, target
+
+    def data_ptr(self) -> int:
+        return self.ptr
+
+    def numel(self) -> int:
+        return self.nbytes
+
+    def element_size(self) -> int:
+        return 1
 
 def _csr(tables):
     """(int32 ids, uint64 offsets) from a list of tables or an (ids, offs) pair."""
@@ -266,7 +340,9 @@ def _stream_handle(stream) -> Optional[int]:
     return stream.cuda_stream or None
 
 
-def _target_of(t: torch.Tensor) -> int:
+def _target_of(t) -> int:
+    if isinstance(t, RawBuffer):
+        return t.aqua_target
     if t.is_cuda:
         return AQUA_TARGET_DEVICE
     if t.is_pinned():
@@ -372,6 +448,71 @@ class KVPool:
             self.handle = None
             if st != AQUA_OK:
                 raise AquaError(st, "aqua_kv_pool_destroy")
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+class SwapSpace:
+    """Offload tensors with a device region and a pinned-host fallback, on a
+    pool (see aqua_swap_space_create)."""
+
+    def __init__(self, pool: "KVPool", device_bytes: int, host_bytes: int):
+        st, h = aqua_swap_space_create(pool.handle, device_bytes, host_bytes)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_space_create")
+        self.handle = h
+
+    def alloc(self, nbytes: int) -> int:
+        st, h = aqua_swap_alloc(self.handle, nbytes)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_alloc")
+        return h
+
+    def free(self, tensor: int) -> None:
+        st = aqua_swap_free(self.handle, tensor)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_free")
+
+    def locate(self, tensor: int):
+        """(pointer, bytes, target) of a tensor now."""
+        st, ptr, nb, tg = aqua_swap_locate(self.handle, tensor)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_locate")
+        return ptr, nb, tg
+
+    def buffer(self, tensor: int) -> RawBuffer:
+        """The tensor's current bytes, for KVPool.swap_out / swap_in."""
+        return RawBuffer(*self.locate(tensor))
+
+    def reclaim(self, nbytes: Optional[int] = None, stream=None) -> int:
+        st, t = aqua_swap_reclaim(self.handle, (1 << 64) - 1 if nbytes is None else nbytes,
+                                  _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_reclaim")
+        return t
+
+    def restore(self, stream=None) -> int:
+        st, t = aqua_swap_restore(self.handle, _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_restore")
+        return t
+
+    def usage(self) -> dict:
+        st, df, hf, dn, hn = aqua_swap_usage(self.handle)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_usage")
+        return {"device_free": df, "host_free": hf, "device_tensors": dn, "host_tensors": hn}
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            st = aqua_swap_space_destroy(self.handle)
+            self.handle = None
+            if st != AQUA_OK:
+                raise AquaError(st, "aqua_swap_space_destroy")
 
     def __enter__(self):
         return self

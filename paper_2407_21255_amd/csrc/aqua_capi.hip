@@ -8,6 +8,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <deque>
+#include <map>
 #include <new>
 #include <vector>
 
@@ -100,7 +101,25 @@ struct aqua_kv_pool {
     hipError_t sticky = hipSuccess;
 };
 
+// Swap space: a device region and a host region, each handed out by a range
+// allocator, and the tensors placed in them, by handle.
+struct aqua_swap_space {
+    aqua_kv_pool* pool = nullptr;
+    uint8_t* region[2] = {nullptr, nullptr};  // index: AQUA_TARGET_DEVICE / _HOST
+    uint64_t region_bytes[2] = {0, 0};
+    aqua::RangeAllocator ranges[2];
+    struct Tensor {
+        uint64_t bytes;
+        int32_t target;
+        uint64_t off;
+    };
+    std::map<uint64_t, Tensor> tensors;  // by handle, oldest first
+    uint64_t next_handle = 1;
+};
+
 namespace {
+
+constexpr uint64_t kSwapAlign = 256;
 
 // Switches to the pool's device for the duration of a call.
 struct DeviceGuard {
@@ -726,6 +745,39 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
     return AQUA_OK;
 }
 
+// Moves the tensors in `moves` (handle, destination offset) from region
+// `from` to the other one as one migration on the pool; on success the
+// tensors point at their new ranges and their old ranges are released.
+aqua_status swap_move(aqua_swap_space* s, int from,
+                      const std::vector<std::pair<uint64_t, uint64_t>>& moves, void* stream,
+                      uint64_t* ticket) {
+    const int to = 1 - from;
+    std::vector<uint64_t> so, dof, len;
+    for (const auto& m : moves) {
+        const auto& t = s->tensors.at(m.first);
+        so.push_back(t.off);
+        dof.push_back(m.second);
+        len.push_back(t.bytes);
+    }
+    uint64_t tk = 0;
+    const aqua_status st =
+        do_migrate(s->pool, s->region[from], s->region_bytes[from], from, s->region[to],
+                   s->region_bytes[to], to, (uint32_t)moves.size(), so.data(), dof.data(),
+                   len.data(), stream, &tk);
+    if (st != AQUA_OK) {
+        for (const auto& m : moves) s->ranges[to].free(m.second);
+        return st;
+    }
+    for (const auto& m : moves) {
+        auto& t = s->tensors.at(m.first);
+        s->ranges[from].free(t.off);
+        t.target = to;
+        t.off = m.second;
+    }
+    if (ticket) *ticket = tk;
+    return AQUA_OK;
+}
+
 }  // namespace
 
 
@@ -904,6 +956,134 @@ aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t p, int32_t path) {
 aqua_status aqua_pool_stats_get(aqua_kv_pool_t p, aqua_pool_stats* out) {
     if (!p || !out) return AQUA_ERR_INVALID;
     *out = p->stats;
+    return AQUA_OK;
+}
+
+aqua_status aqua_swap_space_create(aqua_kv_pool_t pool, uint64_t device_bytes,
+                                   uint64_t host_bytes, aqua_swap_space_t* out) {
+    if (!pool || !out) return AQUA_ERR_INVALID;
+    if (pool->sticky != hipSuccess) return AQUA_ERR_STATE;
+    DeviceGuard dg(pool->device);
+    if (!dg.ok) {
+        (void)hipGetLastError();
+        return AQUA_ERR_HIP;
+    }
+    aqua_swap_space* s = new (std::nothrow) aqua_swap_space();
+    if (!s) return AQUA_ERR_HIP;
+    s->pool = pool;
+    hipError_t e = hipSuccess;
+    if (device_bytes) e = hipMalloc((void**)&s->region[AQUA_TARGET_DEVICE], device_bytes);
+    if (e == hipSuccess && host_bytes)
+        e = hipHostMalloc((void**)&s->region[AQUA_TARGET_HOST], host_bytes, hipHostMallocMapped);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        if (s->region[AQUA_TARGET_DEVICE]) (void)hipFree(s->region[AQUA_TARGET_DEVICE]);
+        delete s;
+        return AQUA_ERR_HIP;
+    }
+    s->region_bytes[AQUA_TARGET_DEVICE] = device_bytes;
+    s->region_bytes[AQUA_TARGET_HOST] = host_bytes;
+    s->ranges[AQUA_TARGET_DEVICE].reset(device_bytes, kSwapAlign);
+    s->ranges[AQUA_TARGET_HOST].reset(host_bytes, kSwapAlign);
+    *out = s;
+    return AQUA_OK;
+}
+
+aqua_status aqua_swap_space_destroy(aqua_swap_space_t s) {
+    if (!s) return AQUA_ERR_INVALID;
+    aqua_status st = AQUA_OK;
+    {
+        DeviceGuard dg(s->pool->device);
+        if (s->pool->sticky == hipSuccess) st = wait_all(s->pool);
+        if (s->region[AQUA_TARGET_DEVICE]) (void)hipFree(s->region[AQUA_TARGET_DEVICE]);
+        if (s->region[AQUA_TARGET_HOST]) (void)hipHostFree(s->region[AQUA_TARGET_HOST]);
+    }
+    delete s;
+    return st;
+}
+
+aqua_status aqua_swap_alloc(aqua_swap_space_t s, uint64_t bytes, uint64_t* handle) {
+    if (!s || !handle || !bytes || bytes % 16) return AQUA_ERR_INVALID;
+    uint64_t off = 0;
+    int32_t target = AQUA_TARGET_DEVICE;
+    if (!s->ranges[target].alloc(bytes, &off)) {
+        target = AQUA_TARGET_HOST;
+        if (!s->ranges[target].alloc(bytes, &off)) return AQUA_ERR_CAPACITY;
+    }
+    const uint64_t h = s->next_handle++;
+    s->tensors[h] = {bytes, target, off};
+    *handle = h;
+    return AQUA_OK;
+}
+
+aqua_status aqua_swap_free(aqua_swap_space_t s, uint64_t handle) {
+    if (!s) return AQUA_ERR_INVALID;
+    auto it = s->tensors.find(handle);
+    if (it == s->tensors.end()) return AQUA_ERR_INVALID;
+    s->ranges[it->second.target].free(it->second.off);
+    s->tensors.erase(it);
+    return AQUA_OK;
+}
+
+aqua_status aqua_swap_locate(aqua_swap_space_t s, uint64_t handle, void** ptr, uint64_t* bytes,
+                             int32_t* target) {
+    if (!s) return AQUA_ERR_INVALID;
+    auto it = s->tensors.find(handle);
+    if (it == s->tensors.end()) return AQUA_ERR_INVALID;
+    const auto& t = it->second;
+    if (ptr) *ptr = s->region[t.target] + t.off;
+    if (bytes) *bytes = t.bytes;
+    if (target) *target = t.target;
+    return AQUA_OK;
+}
+
+aqua_status aqua_swap_reclaim(aqua_swap_space_t s, uint64_t bytes, void* stream,
+                              uint64_t* ticket) {
+    if (!s) return AQUA_ERR_INVALID;
+    if (ticket) *ticket = 0;
+    auto& dev = s->ranges[AQUA_TARGET_DEVICE];
+    auto& host = s->ranges[AQUA_TARGET_HOST];
+    const bool all = bytes == UINT64_MAX;
+    uint64_t freed = dev.free_bytes();
+    std::vector<std::pair<uint64_t, uint64_t>> moves;
+    for (const auto& kv : s->tensors) {
+        if (!all && freed >= bytes) break;
+        if (kv.second.target != AQUA_TARGET_DEVICE) continue;
+        uint64_t off = 0;
+        if (!host.alloc(kv.second.bytes, &off)) {
+            for (const auto& m : moves) host.free(m.second);
+            return AQUA_ERR_CAPACITY;
+        }
+        moves.emplace_back(kv.first, off);
+        freed += dev.granted(kv.second.off);
+    }
+    if (moves.empty()) return AQUA_OK;
+    return swap_move(s, AQUA_TARGET_DEVICE, moves, stream, ticket);
+}
+
+aqua_status aqua_swap_restore(aqua_swap_space_t s, void* stream, uint64_t* ticket) {
+    if (!s) return AQUA_ERR_INVALID;
+    if (ticket) *ticket = 0;
+    auto& dev = s->ranges[AQUA_TARGET_DEVICE];
+    std::vector<std::pair<uint64_t, uint64_t>> moves;
+    for (const auto& kv : s->tensors) {
+        if (kv.second.target != AQUA_TARGET_HOST) continue;
+        uint64_t off = 0;
+        if (dev.alloc(kv.second.bytes, &off)) moves.emplace_back(kv.first, off);
+    }
+    if (moves.empty()) return AQUA_OK;
+    return swap_move(s, AQUA_TARGET_HOST, moves, stream, ticket);
+}
+
+aqua_status aqua_swap_usage(aqua_swap_space_t s, uint64_t* device_free, uint64_t* host_free,
+                            uint64_t* device_tensors, uint64_t* host_tensors) {
+    if (!s) return AQUA_ERR_INVALID;
+    uint64_t n[2] = {0, 0};
+    for (const auto& kv : s->tensors) n[kv.second.target]++;
+    if (device_free) *device_free = s->ranges[AQUA_TARGET_DEVICE].free_bytes();
+    if (host_free) *host_free = s->ranges[AQUA_TARGET_HOST].free_bytes();
+    if (device_tensors) *device_tensors = n[AQUA_TARGET_DEVICE];
+    if (host_tensors) *host_tensors = n[AQUA_TARGET_HOST];
     return AQUA_OK;
 }
 

@@ -346,4 +346,67 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
     return elided;
 }
 
+// ---------------------------------------------------------------------------
+// RangeAllocator
+
+void RangeAllocator::reset(uint64_t size, uint64_t align) {
+    align_ = align ? align : 1;
+    size_ = size - size % align_;
+    free_.clear();
+    used_.clear();
+    if (size_) free_[0] = size_;
+    free_total_ = size_;
+}
+
+bool RangeAllocator::alloc(uint64_t bytes, uint64_t* off) {
+    if (!bytes) return false;
+    if (bytes > UINT64_MAX - align_) return false;
+    const uint64_t need = (bytes + align_ - 1) / align_ * align_;
+    for (auto it = free_.begin(); it != free_.end(); ++it) {
+        if (it->second < need) continue;
+        const uint64_t o = it->first, len = it->second;
+        free_.erase(it);
+        if (len > need) free_[o + need] = len - need;
+        used_[o] = need;
+        free_total_ -= need;
+        *off = o;
+        return true;
+    }
+    return false;
+}
+
+bool RangeAllocator::free(uint64_t off) {
+    auto u = used_.find(off);
+    if (u == used_.end()) return false;
+    uint64_t lo = off, len = u->second;
+    used_.erase(u);
+    free_total_ += len;
+    auto next = free_.lower_bound(lo);
+    if (next != free_.end() && next->first == lo + len) {  // merge the right neighbour
+        len += next->second;
+        next = free_.erase(next);
+    }
+    if (next != free_.begin()) {                            // merge the left neighbour
+        auto prev = std::prev(next);
+        if (prev->first + prev->second == lo) {
+            lo = prev->first;
+            len += prev->second;
+            free_.erase(prev);
+        }
+    }
+    free_[lo] = len;
+    return true;
+}
+
+uint64_t RangeAllocator::largest_free() const {
+    uint64_t m = 0;
+    for (const auto& f : free_) m = std::max(m, f.second);
+    return m;
+}
+
+uint64_t RangeAllocator::granted(uint64_t off) const {
+    auto u = used_.find(off);
+    return u == used_.end() ? 0 : u->second;
+}
+
 }  // namespace aqua

@@ -1,10 +1,12 @@
 // aqua_core.h -- host-side core of the KV page-swap library: argument
-// validation, run planning and cross-stream hazard tracking.  Pure C++17,
+// validation, run planning, cross-stream hazard tracking and the swap
+// space's range allocator.  Pure C++17,
 // no HIP types, so that it builds and is tested on a machine without a GPU.
 #pragma once
 
 #include <cstddef>
 #include <cstdint>
+#include <map>
 #include <utility>
 #include <vector>
 
@@ -182,6 +184,26 @@ private:
     std::vector<uint64_t> dep_;         // per lane, scratch of one issue()
     std::vector<uint32_t> ticket_lane_; // index: ticket
     uint64_t last_ticket_ = 0;
+};
+
+// First-fit allocator of byte ranges inside one arena [0, size) (the swap
+// space's device region and its host region).  Every range starts on an
+// `align` boundary and is a multiple of it; freeing coalesces neighbours.
+// Host bookkeeping only: whoever reuses a freed range orders the reuse.
+class RangeAllocator {
+public:
+    void reset(uint64_t size, uint64_t align);
+    bool alloc(uint64_t bytes, uint64_t* off);  // false: no free range fits
+    bool free(uint64_t off);                     // false: off is not allocated
+    uint64_t size() const { return size_; }
+    uint64_t free_bytes() const { return free_total_; }
+    uint64_t largest_free() const;
+    uint64_t granted(uint64_t off) const;        // bytes of the range at off (0: none)
+
+private:
+    uint64_t size_ = 0, align_ = 1, free_total_ = 0;
+    std::map<uint64_t, uint64_t> free_;   // offset -> length
+    std::map<uint64_t, uint64_t> used_;   // offset -> length
 };
 
 }  // namespace aqua

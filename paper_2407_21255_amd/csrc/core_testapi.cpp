@@ -176,4 +176,23 @@ uint64_t aqua_core_tracker_live_ranges(void* t) {
     return static_cast<aqua::HazardTracker*>(t)->live_ranges();
 }
 
+void* aqua_core_ranges_new(uint64_t size, uint64_t align) {
+    auto* r = new aqua::RangeAllocator();
+    r->reset(size, align);
+    return r;
+}
+void aqua_core_ranges_free_all(void* r) { delete static_cast<aqua::RangeAllocator*>(r); }
+int aqua_core_ranges_alloc(void* r, uint64_t bytes, uint64_t* off) {
+    return static_cast<aqua::RangeAllocator*>(r)->alloc(bytes, off) ? 1 : 0;
+}
+int aqua_core_ranges_release(void* r, uint64_t off) {
+    return static_cast<aqua::RangeAllocator*>(r)->free(off) ? 1 : 0;
+}
+uint64_t aqua_core_ranges_free_bytes(void* r) {
+    return static_cast<aqua::RangeAllocator*>(r)->free_bytes();
+}
+uint64_t aqua_core_ranges_largest_free(void* r) {
+    return static_cast<aqua::RangeAllocator*>(r)->largest_free();
+}
+
 }  // extern "C"

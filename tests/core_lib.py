@@ -1,5 +1,6 @@
 """ctypes access to libaqua_core.so: the library's host core (validation,
-run planning, hazard tracking) built without HIP for CPU tests."""
+run planning, hazard tracking, the swap space's range allocator) built
+without HIP for CPU tests."""
 from __future__ import annotations
 
 import ctypes
@@ -152,4 +153,43 @@ class Tracker:
     def __del__(self):
         if getattr(self, "h", None):
             lib().aqua_core_tracker_free(self.h)
+            self.h = None
+
+
+class Ranges:
+    """The core's first-fit range allocator."""
+
+    def __init__(self, size: int, align: int):
+        L = lib()
+        u64, P = ctypes.c_uint64, ctypes.c_void_p
+        L.aqua_core_ranges_new.argtypes = [u64, u64]
+        L.aqua_core_ranges_new.restype = P
+        L.aqua_core_ranges_free_all.argtypes = [P]
+        L.aqua_core_ranges_alloc.argtypes = [P, u64, ctypes.POINTER(u64)]
+        L.aqua_core_ranges_alloc.restype = ctypes.c_int
+        L.aqua_core_ranges_release.argtypes = [P, u64]
+        L.aqua_core_ranges_release.restype = ctypes.c_int
+        L.aqua_core_ranges_free_bytes.argtypes = [P]
+        L.aqua_core_ranges_free_bytes.restype = u64
+        L.aqua_core_ranges_largest_free.argtypes = [P]
+        L.aqua_core_ranges_largest_free.restype = u64
+        self.L = L
+        self.h = L.aqua_core_ranges_new(size, align)
+
+    def alloc(self, nbytes: int):
+        off = ctypes.c_uint64(0)
+        return off.value if self.L.aqua_core_ranges_alloc(self.h, nbytes, ctypes.byref(off)) else None
+
+    def free(self, off: int) -> bool:
+        return bool(self.L.aqua_core_ranges_release(self.h, off))
+
+    def free_bytes(self) -> int:
+        return int(self.L.aqua_core_ranges_free_bytes(self.h))
+
+    def largest_free(self) -> int:
+        return int(self.L.aqua_core_ranges_largest_free(self.h))
+
+    def close(self):
+        if self.h:
+            self.L.aqua_core_ranges_free_all(self.h)
             self.h = None

@@ -1,0 +1,160 @@
+"""GPU parity of the swap space: offload tensors placed in a device region or,
+when it is full, in pinned host memory; reclaim moving them to host memory
+and restore moving them back, on the pool's ordering, with no host sync
+between the calls; each tensor's bytes checked against the oracle, read back
+with the HIP runtime's own copy."""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_21255_amd import aqua
+from paper_2407_21255_amd import workload as wl
+from tests.checkers import assert_bytes_equal
+from tests.gpu_util import device_pool, host, odesc, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    aqua.load()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _read(ptr: int, nbytes: int) -> np.ndarray:
+    """Bytes at a device or pinned host address, copied by the runtime."""
+    torch.cuda.synchronize()
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    out = np.empty(nbytes, dtype=np.uint8)
+    assert hip.hipMemcpy(out.ctypes.data, ptr, nbytes, 4) == 0     # hipMemcpyDefault
+    return out
+
+
+def test_swap_space_fallback_reclaim_and_restore():
+    shape = wl.KVShape(8, 2048, 4, 16, 64, wl.BF16)      # 16 KiB chunks
+    d = odesc(shape)
+    case = wl.fragmented_case("space", shape, 41, 12, 40, 8)
+    img = shape.image_bytes(40)                           # 5 MiB per prompt
+    pool = device_pool(shape, case.seed, case.owner)
+    pool_h = host(pool)
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    space = aqua.SwapSpace(kv, 3 * img + (1 << 20), 12 * img)
+    try:
+        hs = [space.alloc(img) for _ in case.out_tables]
+        u = space.usage()
+        assert (u["device_tensors"], u["host_tensors"]) == (3, 5), u
+        assert [space.locate(h)[2] for h in hs] == [aqua.AQUA_TARGET_DEVICE] * 3 + \
+            [aqua.AQUA_TARGET_HOST] * 5
+        # Swap-outs into the tensors, then a reclaim of the device region and
+        # new tensors in the vacated range, all without host syncs.
+        for k, (h, t) in enumerate(zip(hs, case.out_tables)):
+            kv.swap_out([t], space.buffer(h), stream=sa if k % 2 else sb)
+        t_rec = space.reclaim(stream=sc)
+        assert t_rec > 0
+        u = space.usage()
+        assert (u["device_tensors"], u["host_tensors"]) == (0, 8), u
+        # Residents 8 and 9 go out into two new tensors, which reuse the
+        # device range the reclaim is still reading from.
+        extra_tables = [t for p, t in enumerate(_tables_of(case)) if p in (8, 9)]
+        hx = [space.alloc(img) for _ in extra_tables]
+        assert all(space.locate(h)[2] == aqua.AQUA_TARGET_DEVICE for h in hx)
+        for h, t in zip(hx, extra_tables):
+            kv.swap_out([t], space.buffer(h), stream=sa)
+        # Swap the 8 preempted prompts back in from wherever they are now.
+        for h, t in zip(hs, case.in_tables):
+            kv.swap_in([t], space.buffer(h), stream=sb)
+        kv.sync()
+        st = kv.stats()
+        say("swap space", st, space.usage())
+        assert st["waits_inserted"] > 0
+        # Oracle: images of the preempted and the two extra prompts, then
+        # the swap-ins.
+        want = []
+        for t in case.out_tables:
+            a = np.zeros(img, dtype=np.uint8)
+            assert oracle.swap_out(d, pool_h, [t], a) == 0
+            want.append(a)
+        want_x = []
+        for t in extra_tables:
+            a = np.zeros(img, dtype=np.uint8)
+            assert oracle.swap_out(d, pool_h, [t], a) == 0
+            want_x.append(a)
+        for t, a in zip(case.in_tables, want):
+            assert oracle.swap_in(d, pool_h, [t], a) == 0
+        assert_bytes_equal(host(pool), pool_h, "pool after swap-ins from reclaimed tensors")
+        for h, a in zip(hs, want):
+            ptr, nb, tg = space.locate(h)
+            assert tg == aqua.AQUA_TARGET_HOST and nb == img
+            assert_bytes_equal(_read(ptr, nb), a, f"reclaimed tensor {h}")
+        for h, a in zip(hx, want_x):
+            ptr, nb, _ = space.locate(h)
+            assert_bytes_equal(_read(ptr, nb), a, f"new tensor {h} in the vacated range")
+        # Restore: host tensors move back, oldest first, while the device
+        # region has room.  With hx[0] freed, 5 MiB at offset 0 and 6 MiB at
+        # 10 MiB are free: hs[0] and hs[1] move, hs[2] does not fit.
+        space.free(hx[0])
+        t_res = space.restore(stream=sc)
+        assert t_res > 0
+        u = space.usage()
+        assert u["device_tensors"] == 3 and u["host_tensors"] == 6, u
+        assert [space.locate(h)[2] for h in hs[:3]] == [aqua.AQUA_TARGET_DEVICE] * 2 + \
+            [aqua.AQUA_TARGET_HOST]
+        kv.stream_wait(t_res, torch.cuda.current_stream())
+        for h, a in zip(hs, want):
+            ptr, nb, _ = space.locate(h)
+            assert_bytes_equal(_read(ptr, nb), a, f"restored tensor {h}")
+        assert_bytes_equal(_read(*space.locate(hx[1])[:2]), want_x[1], "kept tensor")
+    finally:
+        space.close()
+        kv.close()
+
+
+def _tables_of(case):
+    """Block table of every prompt of a fragmented case, by prompt."""
+    by = {}
+    for b, (p, i) in case.owner.items():
+        by.setdefault(p, {})[i] = b
+    return [[by[p][i] for i in range(len(by[p]))] for p in sorted(by)]
+
+
+def test_swap_space_errors_leave_no_trace():
+    shape = wl.KVShape(2, 64, 1, 2, 8, wl.BF16)
+    pool = device_pool(shape, 3)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    space = aqua.SwapSpace(kv, 4096, 8192)
+    try:
+        for nbytes, code in [(0, aqua.AQUA_ERR_INVALID), (24, aqua.AQUA_ERR_INVALID),
+                             (16384, aqua.AQUA_ERR_CAPACITY)]:
+            with pytest.raises(aqua.AquaError) as ei:
+                space.alloc(nbytes)
+            assert ei.value.status == code
+        for fn in (space.free, space.locate):
+            with pytest.raises(aqua.AquaError) as ei:
+                fn(12345)
+            assert ei.value.status == aqua.AQUA_ERR_INVALID
+        a = space.alloc(4096)           # fills the device region
+        b = space.alloc(8192)           # fills the host region
+        assert space.locate(a)[2] == aqua.AQUA_TARGET_DEVICE
+        assert space.locate(b)[2] == aqua.AQUA_TARGET_HOST
+        before = space.usage()
+        with pytest.raises(aqua.AquaError) as ei:
+            space.reclaim()             # the host region has no room for `a`
+        assert ei.value.status == aqua.AQUA_ERR_CAPACITY
+        assert space.usage() == before and space.locate(a)[2] == aqua.AQUA_TARGET_DEVICE
+        assert space.reclaim(0) == 0    # nothing needs to move
+        assert space.restore() == 0     # the device region is full
+        space.free(a)
+        space.free(b)
+        assert space.usage() == {"device_free": 4096, "host_free": 8192, "device_tensors": 0,
+                                 "host_tensors": 0}
+    finally:
+        space.close()
+        kv.close()
