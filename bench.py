@@ -548,6 +548,9 @@ def run_next(args, res_common):
     torch.cuda.synchronize()
     stream = torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
+    if pinned:
+        kv.set_host_path(aqua.AQUA_HOST_STAGED if args.host_path == "staged"
+                         else aqua.AQUA_HOST_ZERO_COPY)
     kv.swap_out([prompt], img, stream=stream)
     kv.sync(0)
     extra = {}
@@ -628,6 +631,7 @@ def run_next(args, res_common):
                    "head_dim": s.head_dim, "block_tokens": s.block_tokens,
                    "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
                    "image_blocks": n, "moved_bytes_per_step": moved,
+                   "host_path": args.host_path if pinned else None,
                    "parallelism": "single_gpu"},
         "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
                      "frac": round(achieved / peak, 4), "traffic": None,
@@ -656,9 +660,9 @@ def main():
                     help="run 4096^3 bf16 GEMMs on a compute stream during the swaps")
     ap.add_argument("--max-workgroups", type=int, default=0,
                     help="cap the swap kernels' grid (0: library default)")
-    ap.add_argument("--host-path", default="staged", choices=["zero_copy", "staged"],
-                    help="pinned-host workloads: kernels over the link, or HBM staging "
-                         "plus the copy engines")
+    ap.add_argument("--host-path", default="zero_copy", choices=["zero_copy", "staged"],
+                    help="pinned-host workloads: the kernels over the link (the library's "
+                         "default), or HBM staging plus the runtime's copies")
     ap.add_argument("--copy-reference", action="store_true",
                     help="one plain device copy of the payload size before timing")
     args = ap.parse_args()

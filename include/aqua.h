@@ -240,7 +240,13 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
                                             uint32_t max_workgroups);
 
 /* How swaps with a pinned-host target move their bytes.
- *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
+ *   AQUA_HOST_ZERO_COPY (default): the gather and scatter kernels read and
+ *     write the host image directly over the link, with no HBM staging.
+ *     Their workgroups stay resident for the whole transfer, so the library
+ *     caps the grid (16 workgroups unless aqua_kv_pool_set_max_workgroups
+ *     says otherwise), which is enough to saturate the link at a steady
+ *     rate; kernels on other streams lose those compute units meanwhile.
+ *   AQUA_HOST_STAGED: the paper's temporary-tensor scheme
  *     (section 7, "Efficient context switching").  Layers pass through two
  *     HBM slots owned by the library (256 MiB each by default, allocated on
  *     a direction's first staged call, after waiting for every outstanding
@@ -249,12 +255,9 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
  *     swap-in.  Swap-outs and swap-ins have their own slots and copy stream,
  *     so a swap-out and a swap-in on different streams use both directions
  *     of the link at once.  The compute units are busy only for the short
- *     gathers and scatters, so concurrent kernels keep running.
- *   AQUA_HOST_ZERO_COPY: the gather and scatter kernels read and write the
- *     host image directly over the link, with no HBM staging.  Their
- *     workgroups stay resident for the whole transfer, so the library caps
- *     the grid (16 workgroups unless aqua_kv_pool_set_max_workgroups says
- *     otherwise), which is enough to saturate the link. */
+ *     gathers and scatters, so concurrent kernels keep running; the link
+ *     rate then depends on how the runtime carries its device-to-host
+ *     copies. */
 enum { AQUA_HOST_ZERO_COPY = 0, AQUA_HOST_STAGED = 1 };
 AQUA_API aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t pool, int32_t path);
 

@@ -84,7 +84,7 @@ struct aqua_kv_pool {
     // Staged host path, per direction (0: swap-out, device to host; 1:
     // swap-in, host to device): two HBM slots and a copy stream, so that a
     // swap-out and a swap-in use both directions of the link at once.
-    int32_t host_path = AQUA_HOST_STAGED;
+    int32_t host_path = AQUA_HOST_ZERO_COPY;
     hipStream_t copy[2] = {nullptr, nullptr};
     uint8_t* staging[2] = {nullptr, nullptr};
     uint64_t staging_bytes[2] = {0, 0};

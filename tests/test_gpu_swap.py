@@ -143,12 +143,12 @@ def test_pinned_host_zero_copy_round_trip():
 
 
 def test_pinned_host_staged_round_trip():
-    """The default (staged) host path: gather into HBM slots, copy engines
-    over the link; same bytes as the oracle."""
+    """The staged host path: gather into HBM slots, runtime copies over the
+    link; same bytes as the oracle."""
     case = wl.tiny_case(seed=12)
     say("host target staged tiny")
     _roundtrip(case.shape, case.seed, case.out_tables, case.in_tables, case.owner,
-               pinned=True)
+               pinned=True, host_path=aqua.AQUA_HOST_STAGED)
 
 
 @pytest.mark.parametrize("shape", RAGGED[:2], ids=lambda s: f"C{s.chunk_bytes}")
@@ -166,7 +166,7 @@ def test_pinned_host_staged_placed_images(shape):
         pos += shape.image_bytes(len(t))
     say("staged placed", shape)
     _roundtrip(shape, 8, out_tables, in_tables, None, img_offsets=offs, buf_bytes=pos + 4096,
-               pinned=True)
+               pinned=True, host_path=aqua.AQUA_HOST_STAGED)
 
 
 def test_errors_match_oracle_and_leave_no_trace():
