@@ -362,6 +362,7 @@ class KVPool:
         if st != AQUA_OK:
             raise AquaError(st, "aqua_kv_pool_create")
         self.handle = h
+        self._spaces = []      # swap spaces on this pool, closed before it
 
     def _swap(self, is_in, tables, buf, img_offsets, stream, target, img_blocks, layers):
         ids, offs = _csr(tables)
@@ -443,6 +444,8 @@ class KVPool:
         return {n: getattr(s, n) for n, _ in s._fields_ if n != "reserved"}
 
     def close(self) -> None:
+        for sp in list(getattr(self, "_spaces", [])):
+            sp.close()
         if getattr(self, "handle", None):
             st = aqua_kv_pool_destroy(self.handle)
             self.handle = None
@@ -465,6 +468,8 @@ class SwapSpace:
         if st != AQUA_OK:
             raise AquaError(st, "aqua_swap_space_create")
         self.handle = h
+        self.pool = pool
+        pool._spaces.append(self)
 
     def alloc(self, nbytes: int) -> int:
         st, h = aqua_swap_alloc(self.handle, nbytes)
@@ -511,6 +516,7 @@ class SwapSpace:
         if getattr(self, "handle", None):
             st = aqua_swap_space_destroy(self.handle)
             self.handle = None
+            self.pool._spaces.remove(self)
             if st != AQUA_OK:
                 raise AquaError(st, "aqua_swap_space_destroy")
 
