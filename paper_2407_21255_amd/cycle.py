@@ -47,3 +47,24 @@ def run_slices(pool: aqua.KVPool, region: torch.Tensor, sched: Schedule,
             cur = torch.cuda.current_stream()
             out_stream.wait_stream(cur)
             in_stream.wait_stream(cur)
+
+
+def run_slices_in_space(pool: aqua.KVPool, space: aqua.SwapSpace, tensors: dict,
+                        sched: Schedule, first: int, count: int, out_stream, in_stream,
+                        between: Optional[Callable[[int], None]] = None) -> None:
+    """Runs slices [first, first+count) with every prompt's image in its own
+    swap-space tensor (``tensors``: prompt -> handle), wherever the tensor
+    lives now (device region or host fallback).  One call per prompt, since
+    the tensors of one slice may sit in different places."""
+    for s in range(first, first + count):
+        sl = sched.slices[s]
+        for p, t in zip(sl.out_prompts, sl.out_tables):
+            pool.swap_out([t], space.buffer(tensors[p]), stream=out_stream)
+        for p, t in zip(sl.in_prompts, sl.in_tables):
+            pool.swap_in([t], space.buffer(tensors[p]), stream=in_stream)
+        pool.sync(0)
+        if between is not None:
+            between(s)
+            cur = torch.cuda.current_stream()
+            out_stream.wait_stream(cur)
+            in_stream.wait_stream(cur)

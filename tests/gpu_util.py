@@ -61,6 +61,15 @@ def apply_mutations_host(sched, s, pool_np, region_np):
         region_np[o:o + n] = wl.CONSUMED_BYTE
 
 
+def apply_pool_mutations_device(sched, s, pool_t):
+    """The residents' 16-byte stamps of slice s (no offload-slot marks)."""
+    offs, words, _ = wl.mutation_writes(sched, s)
+    if len(offs):
+        idx = torch.from_numpy(offs).to(pool_t.device).reshape(-1, 1) + \
+            torch.arange(16, device=pool_t.device).reshape(1, -1)
+        pool_t[idx.reshape(-1)] = torch.from_numpy(words.reshape(-1)).to(pool_t.device)
+
+
 def apply_mutations_device(sched, s, pool_t, region_t):
     offs, words, slots = wl.mutation_writes(sched, s)
     if len(offs):
@@ -71,7 +80,14 @@ def apply_mutations_device(sched, s, pool_t, region_t):
         region_t[o:o + n].fill_(wl.CONSUMED_BYTE)
 
 
-def oracle_replay(sched, pool_np, region_np, first, count, mutate=True, grow=True):
+def apply_pool_mutations_host(sched, s, pool_np):
+    offs, words, _ = wl.mutation_writes(sched, s)
+    for o, w in zip(offs, words):
+        pool_np[o:o + 16] = w
+
+
+def oracle_replay(sched, pool_np, region_np, first, count, mutate=True, grow=True,
+                  slot_marks=True):
     """The oracle's run of slices [first, first+count) in issue order; the
     compute stand-in (KV growth, mutations) between slices where asked."""
     d = odesc(sched.shape)
@@ -85,5 +101,7 @@ def oracle_replay(sched, pool_np, region_np, first, count, mutate=True, grow=Tru
         assert oracle.swap_in(d, pool_np, sl.in_tables, region_np, in_off) == 0
         if grow and sl.grow:
             wl.apply_growth(torch.from_numpy(pool_np), sched, s)
-        if mutate:
+        if mutate and slot_marks:
             apply_mutations_host(sched, s, pool_np, region_np)
+        elif mutate:
+            apply_pool_mutations_host(sched, s, pool_np)

@@ -54,7 +54,12 @@ def test_swap_space_fallback_reclaim_and_restore():
         assert [space.locate(h)[2] for h in hs] == [aqua.AQUA_TARGET_DEVICE] * 3 + \
             [aqua.AQUA_TARGET_HOST] * 5
         # Swap-outs into the tensors, then a reclaim of the device region and
-        # new tensors in the vacated range, all without host syncs.
+        # new tensors in the vacated range, all without host syncs.  A bounded
+        # spin ahead of them keeps the swap-outs pending while the reclaim is
+        # issued, so the reclaim must wait for them on the device.
+        for s in (sa, sb):
+            with torch.cuda.stream(s):
+                torch.cuda._sleep(20_000_000)
         for k, (h, t) in enumerate(zip(hs, case.out_tables)):
             kv.swap_out([t], space.buffer(h), stream=sa if k % 2 else sb)
         t_rec = space.reclaim(stream=sc)
@@ -155,6 +160,70 @@ def test_swap_space_errors_leave_no_trace():
         space.free(b)
         assert space.usage() == {"device_free": 4096, "host_free": 8192, "device_tensors": 0,
                                  "host_tensors": 0}
+    finally:
+        space.close()
+        kv.close()
+
+
+def test_fair_scheduling_images_in_a_swap_space_with_reclaim_and_restore():
+    """The small fair-scheduling run with every prompt's image in its own
+    swap-space tensor: a third of them fit the device region, the rest fall
+    back to host memory.  After a third of the reschedules the device region
+    is reclaimed (every tensor moves to host memory), after two thirds it is
+    restored, and the swaps go on from wherever the tensors are.  Pool and
+    tensors must equal the oracle's replay with images in fixed slots."""
+    from paper_2407_21255_amd import cfs
+    from paper_2407_21255_amd.cycle import run_slices_in_space
+    from tests.gpu_util import apply_pool_mutations_device, oracle_replay
+    cfg = wl.CFS_SMALL
+    sh = cfg.shape
+    tr = cfg.trace()
+    log, _ = cfs.run_trace(tr, sh.num_blocks, sh.block_tokens, cfg.batch_tokens,
+                           cfg.decode_slots(tr), cfg.k)
+    sched = wl.cfs_swap_schedule(sh, cfg.seed, tr, log)
+    n = len(sched.slices)
+    sizes = [sh.image_bytes(nb) for nb in sched.nblocks]
+    total = sum(sizes)
+    pool = device_pool(sh, cfg.seed)
+    pool_h = host(pool)
+    region_h = np.full(sched.region_bytes, wl.GUARD_BYTE, dtype=np.uint8)
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(sh.as_tuple(), pool)
+    space = aqua.SwapSpace(kv, total // 3 // 256 * 256, total + 256 * len(sizes))
+    try:
+        tensors = {p: space.alloc(sz) for p, sz in enumerate(sizes)}
+        u0 = space.usage()
+        assert u0["device_tensors"] > 0 and u0["host_tensors"] > 0, u0
+
+        def between(k):
+            wl.apply_growth(pool, sched, k)
+            apply_pool_mutations_device(sched, k, pool)
+
+        n1, n2 = n // 3, 2 * n // 3
+        run_slices_in_space(kv, space, tensors, sched, 0, n1, sa, sb, between)
+        assert space.reclaim(stream=sc) > 0
+        assert space.usage()["device_tensors"] == 0
+        run_slices_in_space(kv, space, tensors, sched, n1, n2 - n1, sa, sb, between)
+        assert space.restore(stream=sc) > 0
+        u2 = space.usage()
+        assert u2["device_tensors"] > 0, u2
+        run_slices_in_space(kv, space, tensors, sched, n2, n - n2, sa, sb, between)
+        kv.sync()
+        st = kv.stats()
+        say("cfs in swap space", st, u0, u2)
+        assert st["calls_migrate"] == 2
+        oracle_replay(sched, pool_h, region_h, 0, n, slot_marks=False)
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        last = {}
+        for sl in sched.slices:
+            for p, t in zip(sl.out_prompts, sl.out_tables):
+                last[p] = len(t)
+        assert last
+        for p, m in last.items():
+            ptr, _, _ = space.locate(tensors[p])
+            nb = sh.image_bytes(m)
+            o = sched.slot_offsets[p]
+            assert_bytes_equal(_read(ptr, nb), region_h[o:o + nb], f"image of prompt {p}")
     finally:
         space.close()
         kv.close()
