@@ -202,8 +202,7 @@ def run_pair(args, res_common):
         kv.set_max_workgroups(aqua.AQUA_TARGET_HOST if pinned else aqua.AQUA_TARGET_DEVICE,
                               args.max_workgroups)
     if pinned:
-        kv.set_host_path(aqua.AQUA_HOST_STAGED if args.host_path == "staged"
-                         else aqua.AQUA_HOST_ZERO_COPY)
+        _configure_host(kv, args.host_path)
     evs = []
 
     def step(i, timed):
@@ -256,6 +255,8 @@ def run_pair(args, res_common):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = kv.stats()
+    carrier = ([kv.link_engine(0), kv.link_engine(1)]
+               if pinned and args.host_path == "staged" else None)
     kv.close()
     if args.gemm:
         # Kernel time of each GEMM alone and while the swaps run (gaps in the
@@ -288,6 +289,7 @@ def run_pair(args, res_common):
             "payload_bytes_per_direction": payload,
             "offload_target": "pinned_host" if pinned else "hbm",
             "host_path": args.host_path if pinned else None,
+            "link_carrier": carrier,
             "parallelism": "single_gpu",
         },
         "roofline": {
@@ -345,6 +347,23 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
     return out
 
 
+LINK_ENGINE = {"auto": -2, "runtime": -1}
+_link_request = "auto"
+
+
+def _configure_host(kv, host_path):
+    """Host path of a pool, and for the staged path the carrier of its link
+    copies (``--link-engine``)."""
+    from paper_2407_21255_amd import aqua
+    kv.set_host_path(aqua.AQUA_HOST_STAGED if host_path == "staged"
+                     else aqua.AQUA_HOST_ZERO_COPY)
+    if host_path == "staged":
+        e = LINK_ENGINE.get(_link_request)
+        e = int(_link_request) if e is None else e
+        for direction in (0, 1):
+            kv.set_link_engine(direction, e)
+
+
 def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     """Issues slices ``ids`` of a swap schedule (the first ``warmup`` of them
     untimed): out on one stream, in on another, ``aqua_sync`` at the end of
@@ -362,8 +381,7 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
     if host_path is not None:
-        kv.set_host_path(aqua.AQUA_HOST_STAGED if host_path == "staged"
-                         else aqua.AQUA_HOST_ZERO_COPY)
+        _configure_host(kv, host_path)
     evs = []
 
     def one(k, timed):
@@ -549,8 +567,7 @@ def run_next(args, res_common):
     stream = torch.cuda.Stream()
     kv = aqua.KVPool(s.as_tuple(), pool)
     if pinned:
-        kv.set_host_path(aqua.AQUA_HOST_STAGED if args.host_path == "staged"
-                         else aqua.AQUA_HOST_ZERO_COPY)
+        _configure_host(kv, args.host_path)
     kv.swap_out([prompt], img, stream=stream)
     kv.sync(0)
     extra = {}
@@ -599,6 +616,8 @@ def run_next(args, res_common):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = kv.stats()
+    carrier = ([kv.link_engine(0), kv.link_engine(1)]
+               if pinned and args.host_path == "staged" else None)
     kv.close()
     if w == "migrate":
         d2h = np.mean([a.elapsed_time(b) for a, b, _ in evs])
@@ -632,6 +651,7 @@ def run_next(args, res_common):
                    "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
                    "image_blocks": n, "moved_bytes_per_step": moved,
                    "host_path": args.host_path if pinned else None,
+                   "link_carrier": carrier,
                    "parallelism": "single_gpu"},
         "roofline": {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
                      "frac": round(achieved / peak, 4), "traffic": None,
@@ -661,8 +681,13 @@ def main():
     ap.add_argument("--max-workgroups", type=int, default=0,
                     help="cap the swap kernels' grid (0: library default)")
     ap.add_argument("--host-path", default="zero_copy", choices=["zero_copy", "staged"],
-                    help="pinned-host workloads: the kernels over the link (the library's "
-                         "default), or HBM staging plus the runtime's copies")
+                    help="pinned-host workloads: the kernels writing host memory over the "
+                         "link (the zero-copy target these workloads are defined with), or "
+                         "HBM staging plus link copies on a copy engine (the library's "
+                         "default, which leaves the compute units to other streams)")
+    ap.add_argument("--link-engine", default="auto",
+                    help="staged path: carrier of the link copies, 'auto', 'runtime' (the HIP "
+                         "runtime's copies) or an SDMA engine index 0..15")
     ap.add_argument("--copy-reference", action="store_true",
                     help="one plain device copy of the payload size before timing")
     args = ap.parse_args()
@@ -670,6 +695,11 @@ def main():
         print("bench.py measures one GPU: the swap path runs on a single MI355X "
               "(no sharding, no collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    global _link_request
+    if args.link_engine not in LINK_ENGINE and not (args.link_engine.isdigit()
+                                                    and int(args.link_engine) <= 15):
+        ap.error("--link-engine: 'auto', 'runtime' or 0..15")
+    _link_request = args.link_engine
 
     import torch
 

@@ -240,26 +240,54 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
                                             uint32_t max_workgroups);
 
 /* How swaps with a pinned-host target move their bytes.
- *   AQUA_HOST_ZERO_COPY (default): the gather and scatter kernels read and
- *     write the host image directly over the link, with no HBM staging.
- *     Their workgroups stay resident for the whole transfer, so the library
- *     caps the grid (16 workgroups unless aqua_kv_pool_set_max_workgroups
- *     says otherwise), which is enough to saturate the link at a steady
- *     rate; kernels on other streams lose those compute units meanwhile.
- *   AQUA_HOST_STAGED: the paper's temporary-tensor scheme
+ *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
  *     (section 7, "Efficient context switching").  Layers pass through two
  *     HBM slots owned by the library (256 MiB each by default, allocated on
  *     a direction's first staged call, after waiting for every outstanding
- *     call): the gather kernel fills a slot and the runtime's copies move it
- *     over the link while the next slot is filled, and the reverse on
- *     swap-in.  Swap-outs and swap-ins have their own slots and copy stream,
- *     so a swap-out and a swap-in on different streams use both directions
- *     of the link at once.  The compute units are busy only for the short
- *     gathers and scatters, so concurrent kernels keep running; the link
- *     rate then depends on how the runtime carries its device-to-host
- *     copies. */
+ *     call): the gather kernel fills a slot and a copy engine moves it over
+ *     the link while the next slot is filled, and the reverse on swap-in.
+ *     Swap-outs and swap-ins have their own slots and link carrier (see
+ *     aqua_kv_pool_set_link_engine), so a swap-out and a swap-in on
+ *     different streams use both directions of the link at once.  The
+ *     compute units are busy only for the short gathers and scatters, so
+ *     concurrent kernels keep running.
+ *   AQUA_HOST_ZERO_COPY: the gather and scatter kernels read and write the
+ *     host image directly over the link, with no HBM staging.  Their
+ *     workgroups stay resident for the whole transfer, so the library caps
+ *     the grid (16 workgroups unless aqua_kv_pool_set_max_workgroups says
+ *     otherwise), which is enough to saturate the link; kernels on other
+ *     streams lose those compute units meanwhile, and a kernel that needs
+ *     every compute unit at once (a GEMM with one tile per unit) runs a
+ *     second round of tiles. */
 enum { AQUA_HOST_ZERO_COPY = 0, AQUA_HOST_STAGED = 1 };
 AQUA_API aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t pool, int32_t path);
+
+/* What carries the staged path's link copies for one direction (dir 0:
+ * swap-out, device to host; dir 1: swap-in, host to device).
+ *   0..15               that SDMA engine, driven through the HSA runtime by
+ *                       a library thread; the call's stream waits for the
+ *                       engine's progress on the device, with no host block.
+ *                       A staged call fails with AQUA_ERR_HIP (nothing
+ *                       enqueued) if the engine cannot be used.
+ *   AQUA_LINK_RUNTIME   the HIP runtime's own copies on a library stream; the
+ *                       runtime then picks the mechanism per copy (a blit
+ *                       kernel or any engine), and some engines reach only a
+ *                       fraction of the link rate.
+ *   AQUA_LINK_AUTO      (default) the HSA runtime's preferred engine for the
+ *                       direction if it names one, else the lowest-numbered
+ *                       available engine, the two directions on different
+ *                       engines where possible; the runtime's copies if no
+ *                       engine can be used.
+ * The choice is made on the direction's next staged call.  Waits for every
+ * outstanding call first.  dir other than 0 or 1, or another engine value:
+ * AQUA_ERR_INVALID.
+ * aqua_kv_pool_get_link_engine reports the carrier in use: an engine index,
+ * AQUA_LINK_RUNTIME, or AQUA_LINK_AUTO while no staged call has chosen. */
+enum { AQUA_LINK_RUNTIME = -1, AQUA_LINK_AUTO = -2 };
+AQUA_API aqua_status aqua_kv_pool_set_link_engine(aqua_kv_pool_t pool, int32_t dir,
+                                                  int32_t engine);
+AQUA_API aqua_status aqua_kv_pool_get_link_engine(aqua_kv_pool_t pool, int32_t dir,
+                                                  int32_t* engine);
 
 /* Copy the pool's counters into *out. */
 AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* out);

@@ -32,12 +32,14 @@ AQUA_ERR_STATE = -6
 AQUA_F16, AQUA_BF16, AQUA_FP8_E4M3 = 1, 2, 3
 AQUA_TARGET_DEVICE, AQUA_TARGET_HOST = 0, 1
 AQUA_HOST_ZERO_COPY, AQUA_HOST_STAGED = 0, 1
+AQUA_LINK_RUNTIME, AQUA_LINK_AUTO = -1, -2
 
 EXPORTS = (
     "aqua_kv_pool_create", "aqua_kv_pool_destroy", "aqua_swap_out",
     "aqua_swap_in", "aqua_swap_out_ex", "aqua_swap_in_ex", "aqua_migrate",
     "aqua_sync", "aqua_stream_wait", "aqua_query",
     "aqua_kv_pool_set_max_workgroups", "aqua_kv_pool_set_host_path",
+    "aqua_kv_pool_set_link_engine", "aqua_kv_pool_get_link_engine",
     "aqua_pool_stats_get", "aqua_status_str", "aqua_cfs_partition",
     "aqua_swap_space_create", "aqua_swap_space_destroy", "aqua_swap_alloc", "aqua_swap_free",
     "aqua_swap_locate", "aqua_swap_reclaim", "aqua_swap_restore", "aqua_swap_usage",
@@ -117,6 +119,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_query.argtypes = [P, u64]
     L.aqua_kv_pool_set_max_workgroups.argtypes = [P, i32, u32]
     L.aqua_kv_pool_set_host_path.argtypes = [P, i32]
+    L.aqua_kv_pool_set_link_engine.argtypes = [P, i32, i32]
+    L.aqua_kv_pool_get_link_engine.argtypes = [P, i32, ctypes.POINTER(i32)]
     L.aqua_pool_stats_get.argtypes = [P, ctypes.POINTER(aqua_pool_stats)]
     L.aqua_cfs_partition.argtypes = [P, u32, ctypes.POINTER(aqua_cfs_params), P, P,
                                      ctypes.POINTER(u32), ctypes.POINTER(u64)]
@@ -209,6 +213,16 @@ def aqua_kv_pool_set_max_workgroups(pool, target: int, n: int) -> int:
 
 def aqua_kv_pool_set_host_path(pool, path: int) -> int:
     return load().aqua_kv_pool_set_host_path(pool, path)
+
+
+def aqua_kv_pool_set_link_engine(pool, direction: int, engine: int) -> int:
+    return load().aqua_kv_pool_set_link_engine(pool, direction, engine)
+
+
+def aqua_kv_pool_get_link_engine(pool, direction: int):
+    e = ctypes.c_int32(0)
+    st = load().aqua_kv_pool_get_link_engine(pool, direction, ctypes.byref(e))
+    return st, e.value
 
 
 def aqua_pool_stats_get(pool):
@@ -436,6 +450,20 @@ class KVPool:
         st = aqua_kv_pool_set_host_path(self.handle, path)
         if st != AQUA_OK:
             raise AquaError(st, "aqua_kv_pool_set_host_path")
+
+    def set_link_engine(self, direction: int, engine: int) -> None:
+        """Carrier of the staged path's link copies for one direction (0:
+        swap-out, 1: swap-in): an SDMA engine index, AQUA_LINK_RUNTIME or
+        AQUA_LINK_AUTO."""
+        st = aqua_kv_pool_set_link_engine(self.handle, direction, engine)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_kv_pool_set_link_engine")
+
+    def link_engine(self, direction: int) -> int:
+        st, e = aqua_kv_pool_get_link_engine(self.handle, direction)
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_kv_pool_get_link_engine")
+        return e
 
     def stats(self) -> dict:
         st, s = aqua_pool_stats_get(self.handle)

@@ -23,7 +23,8 @@ CORE_LIB = os.path.join(PKG, "libaqua_core.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["aqua_core.cpp", "cfs.cpp", "swap_kernels.hip", "aqua_capi.hip"]
+HIP_SOURCES = ["aqua_core.cpp", "cfs.cpp", "swap_kernels.hip", "link_engine.hip",
+               "aqua_capi.hip"]
 CORE_SOURCES = ["aqua_core.cpp", "core_testapi.cpp"]
 
 # Packed fp32 instructions are switched off for every device compile.
@@ -48,7 +49,8 @@ def build_hip(out: str = HIP_LIB, extra=()) -> str:
         # hipcc compiles .cpp files as host code unless told they are HIP.
         srcs += (["-x", "hip", p] if s.endswith(".hip") else ["-x", "c++", p])
     tmp = out + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp])
+    _run([HIPCC, *HIP_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp,
+          "-L/opt/rocm/lib", "-lhsa-runtime64"])
     os.replace(tmp, out)
     return out
 

@@ -14,6 +14,7 @@
 
 #include "aqua.h"
 #include "aqua_core.h"
+#include "link_engine.h"
 #include "swap_kernels.h"
 
 namespace {
@@ -82,9 +83,16 @@ struct aqua_kv_pool {
     std::deque<RingUse> ring_uses;
 
     // Staged host path, per direction (0: swap-out, device to host; 1:
-    // swap-in, host to device): two HBM slots and a copy stream, so that a
-    // swap-out and a swap-in use both directions of the link at once.
-    int32_t host_path = AQUA_HOST_ZERO_COPY;
+    // swap-in, host to device): two HBM slots and a carrier for the link
+    // copies, so that a swap-out and a swap-in use both directions of the
+    // link at once.  The carrier is an SDMA engine driven by a LinkEngine,
+    // or the runtime's copies on a copy stream.
+    int32_t host_path = AQUA_HOST_STAGED;
+    int32_t link_request[2] = {AQUA_LINK_AUTO, AQUA_LINK_AUTO};
+    int32_t link_used[2] = {AQUA_LINK_AUTO, AQUA_LINK_AUTO};  // AUTO: not chosen yet
+    bool hsa_up = false;
+    aqua::LinkAgents agents;
+    aqua::LinkEngine link[2];
     hipStream_t copy[2] = {nullptr, nullptr};
     uint8_t* staging[2] = {nullptr, nullptr};
     uint64_t staging_bytes[2] = {0, 0};
@@ -174,8 +182,18 @@ void retire(aqua_kv_pool* p, uint32_t m, uint64_t ticket) {
     p->tracker.complete(m, ticket);
 }
 
+// A failure on a link engine's thread becomes the pool's sticky error.
+aqua_status check_links(aqua_kv_pool* p) {
+    for (int d = 0; d < 2; ++d) {
+        const hipError_t e = p->link[d].error();
+        if (e != hipSuccess) return latch(p, e);
+    }
+    return AQUA_OK;
+}
+
 // Non-blocking: retire whatever has finished.
 aqua_status poll(aqua_kv_pool* p) {
+    if (check_links(p) != AQUA_OK) return AQUA_ERR_HIP;
     for (uint32_t m = 0; m < p->outstanding.size(); ++m) {
         auto& q = p->outstanding[m];
         while (!q.empty()) {
@@ -204,7 +222,7 @@ aqua_status wait_ticket(aqua_kv_pool* p, uint64_t ticket) {
     const hipError_t e = hipEventSynchronize(ev);
     if (e != hipSuccess) return latch(p, e);
     retire(p, m, ticket);
-    return AQUA_OK;
+    return check_links(p);
 }
 
 aqua_status wait_all(aqua_kv_pool* p) {
@@ -217,7 +235,7 @@ aqua_status wait_all(aqua_kv_pool* p) {
         retire(p, m, last);
     }
     p->ring_uses.clear();
-    return AQUA_OK;
+    return check_links(p);
 }
 
 void free_rings(aqua_kv_pool* p) {
@@ -291,18 +309,52 @@ aqua_status ensure_staging(aqua_kv_pool* p, int dir, uint64_t bytes) {
     if (p->staging[dir]) (void)hipFree(p->staging[dir]);
     p->staging[dir] = nullptr;
     p->staging_bytes[dir] = 0;
-    if (!p->copy[dir] &&
-        hipStreamCreateWithFlags(&p->copy[dir], hipStreamNonBlocking) != hipSuccess) {
-        (void)hipGetLastError();
-        p->copy[dir] = nullptr;
-        return AQUA_ERR_HIP;
-    }
     if (hipMalloc((void**)&p->staging[dir], bytes) != hipSuccess) {
         (void)hipGetLastError();
         p->staging[dir] = nullptr;
         return AQUA_ERR_HIP;
     }
     p->staging_bytes[dir] = bytes;
+    return AQUA_OK;
+}
+
+// Chooses direction dir's carrier for link copies on its first staged call:
+// the requested engine, or for AQUA_LINK_AUTO the automatic engine choice,
+// falling back to the runtime's copies when the HSA runtime, the engine or
+// stream waits on signal memory are unavailable.  An explicitly requested
+// engine that cannot start is an error.
+aqua_status ensure_link(aqua_kv_pool* p, int dir) {
+    if (p->link_used[dir] != AQUA_LINK_AUTO) return AQUA_OK;
+    const int32_t req = p->link_request[dir];
+    if (req != AQUA_LINK_RUNTIME) {
+        int can_wait = 0;
+        if (hipDeviceGetAttribute(&can_wait, hipDeviceAttributeCanUseStreamWaitValue,
+                                  p->device) != hipSuccess) {
+            (void)hipGetLastError();
+            can_wait = 0;
+        }
+        if (can_wait && !p->hsa_up) p->hsa_up = aqua::link_acquire(p->device, &p->agents);
+        int32_t eng = req;
+        if (p->hsa_up && can_wait && eng == AQUA_LINK_AUTO) {
+            int32_t e2h = -1, h2d = -1;
+            aqua::link_auto_engines(p->agents, &e2h, &h2d);
+            eng = dir ? h2d : e2h;
+        }
+        if (p->hsa_up && can_wait && eng >= 0 &&
+            p->link[dir].start(p->device, p->agents, dir, eng) == hipSuccess) {
+            p->link_used[dir] = eng;
+            return AQUA_OK;
+        }
+        (void)hipGetLastError();
+        if (req >= 0) return AQUA_ERR_HIP;
+    }
+    if (!p->copy[dir] &&
+        hipStreamCreateWithFlags(&p->copy[dir], hipStreamNonBlocking) != hipSuccess) {
+        (void)hipGetLastError();
+        p->copy[dir] = nullptr;
+        return AQUA_ERR_HIP;
+    }
+    p->link_used[dir] = AQUA_LINK_RUNTIME;
     return AQUA_OK;
 }
 
@@ -359,22 +411,24 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
 }
 
 // Staged host path.  Layers go through two HBM slots of G layers each
-// (per direction: swap-outs and swap-ins have their own slots and copy
-// stream, so one of each can run at once on the two directions of the
-// link).  A slot holds, sequence after sequence, the sequence's G layers in image
-// order ([G][n_s][C] at G * first_s * C), so each sequence's piece of a
+// (per direction: swap-outs and swap-ins have their own slots and link
+// carrier, so one of each can run at once on the two directions of the
+// link).  A slot holds, sequence after sequence, the sequence's G layers in
+// image order ([G][n_s][C] at G * first_s * C), so each sequence's piece of a
 // layer group is contiguous both in the slot and in the host image: one
 // copy per sequence per group.  Swap-out: the gather fills a slot on the
-// call's stream, then the copy stream moves the pieces to the host image.
-// Swap-in: the copy stream fills a slot from the host image, then the
-// scatter drains it on the call's stream.  A slot is refilled only after
-// its previous user has finished with it.
-// Moves sequence q's layers [l0, l0 + nl) between a slot and the host image
-// on the copy stream: one copy when the image holds exactly the table's
-// blocks, else one per layer (only the first n of its m blocks).
-hipError_t stage_copies(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t* slot,
-                        uint32_t G, uint32_t l0, uint32_t nl) {
+// call's stream, then the carrier moves the pieces to the host image.
+// Swap-in: the carrier fills a slot from the host image, then the scatter
+// drains it on the call's stream.  A slot is refilled only after its
+// previous user has finished with it.
+//
+// The copies moving sequence q's layers [l0, l0 + nl) between a slot and the
+// host image: one piece when the image holds exactly the table's blocks,
+// else one per layer (only the first n of its m blocks).
+void stage_pieces(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t* slot, uint32_t G,
+                  uint32_t l0, uint32_t nl, std::vector<aqua::LinkPiece>* out) {
     const uint64_t C = p->shape.C;
+    out->clear();
     for (const StagedSeq& q : p->sseq) {
         uint8_t* s = slot + G * q.first * C;
         uint8_t* h = (uint8_t*)const_cast<void*>(buf) + q.off;
@@ -384,24 +438,41 @@ hipError_t stage_copies(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t*
             const uint64_t l = l0 + j;
             uint8_t* hj = h + l * q.m * C;
             uint8_t* sj = s + (uint64_t)j * q.n * C;
-            const hipError_t e =
-                to_host ? hipMemcpyAsync(hj, sj, bytes, hipMemcpyDeviceToHost, p->copy[0])
-                        : hipMemcpyAsync(sj, hj, bytes, hipMemcpyHostToDevice, p->copy[1]);
-            if (e != hipSuccess) return e;
+            out->push_back(to_host ? aqua::LinkPiece{hj, sj, bytes}
+                                   : aqua::LinkPiece{sj, hj, bytes});
         }
     }
-    return hipSuccess;
 }
 
-aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStream_t stream,
-                           const RunDesc* descs, uint32_t ndesc, uint64_t slot, uint32_t G,
-                           uint32_t l_begin, uint32_t l_end, Outstanding* rec) {
-    const uint32_t L = l_end;
+aqua::SwapLaunch slot_launch(aqua_kv_pool* p, bool is_in, uint8_t* slot, const RunDesc* descs,
+                             uint32_t ndesc, uint32_t l0, uint32_t nl) {
+    // The kernels only touch HBM here: no host-link grid cap.
+    aqua::SwapLaunch L = make_launch(p, is_in, slot, descs, ndesc, AQUA_TARGET_DEVICE);
+    L.first_layer = l0;
+    L.num_layers = nl;
+    L.img_l0 = l0;
+    return L;
+}
+
+// Link copies by the runtime, on the direction's copy stream.
+aqua_status enqueue_staged_runtime(aqua_kv_pool* p, bool is_in, const void* buf,
+                                   hipStream_t stream, const RunDesc* descs, uint32_t ndesc,
+                                   uint64_t slot, uint32_t G, uint32_t l_begin, uint32_t l_end,
+                                   Outstanding* rec) {
     hipError_t e = hipSuccess;
     auto ev = [&](hipEvent_t* x) -> hipError_t {
         hipError_t r = take_event(p, x);
         if (r == hipSuccess) rec->aux.push_back(*x);
         return r;
+    };
+    auto copies = [&](const std::vector<aqua::LinkPiece>& v) -> hipError_t {
+        for (const aqua::LinkPiece& pc : v) {
+            const hipError_t r = hipMemcpyAsync(
+                pc.dst, pc.src, pc.bytes, is_in ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost,
+                p->copy[is_in]);
+            if (r != hipSuccess) return r;
+        }
+        return hipSuccess;
     };
     // The copy stream starts after everything the call's stream must wait
     // for (ordering waits inserted for this call, earlier work).
@@ -411,16 +482,14 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
     hipStream_t copy = p->copy[is_in];
     if ((e = hipStreamWaitEvent(copy, start, 0)) != hipSuccess) return latch(p, e);
 
+    std::vector<aqua::LinkPiece> pieces;
     hipEvent_t slot_free[2] = {nullptr, nullptr};
     hipEvent_t last_copy = nullptr;
-    for (uint32_t l0 = l_begin, k = 0; l0 < L; l0 += G, ++k) {
-        const uint32_t nl = std::min<uint32_t>(G, L - l0);
+    for (uint32_t l0 = l_begin, k = 0; l0 < l_end; l0 += G, ++k) {
+        const uint32_t nl = std::min<uint32_t>(G, l_end - l0);
         uint8_t* s = p->staging[is_in] + (k % 2) * slot;
-        // The kernels only touch HBM here: no host-link grid cap.
-        aqua::SwapLaunch Lk = make_launch(p, is_in, s, descs, ndesc, AQUA_TARGET_DEVICE);
-        Lk.first_layer = l0;
-        Lk.num_layers = nl;
-        Lk.img_l0 = l0;
+        const aqua::SwapLaunch Lk = slot_launch(p, is_in, s, descs, ndesc, l0, nl);
+        stage_pieces(p, !is_in, buf, s, G, l0, nl, &pieces);
         hipEvent_t e1 = nullptr, e2 = nullptr;
         if ((e = ev(&e1)) != hipSuccess || (e = ev(&e2)) != hipSuccess) return latch(p, e);
         hipStream_t first = is_in ? copy : stream;   // fills the slot
@@ -428,7 +497,7 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
         if (slot_free[k % 2] && (e = hipStreamWaitEvent(first, slot_free[k % 2], 0)))
             return latch(p, e);
         if (is_in) {
-            if ((e = stage_copies(p, false, buf, s, G, l0, nl)) != hipSuccess) return latch(p, e);
+            if ((e = copies(pieces)) != hipSuccess) return latch(p, e);
         } else {
             (void)hipGetLastError();
             if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
@@ -439,7 +508,7 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
             (void)hipGetLastError();
             if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
         } else {
-            if ((e = stage_copies(p, true, buf, s, G, l0, nl)) != hipSuccess) return latch(p, e);
+            if ((e = copies(pieces)) != hipSuccess) return latch(p, e);
         }
         if ((e = hipEventRecord(e2, second)) != hipSuccess) return latch(p, e);
         slot_free[k % 2] = e2;
@@ -449,6 +518,84 @@ aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStre
     if (last_copy && (e = hipStreamWaitEvent(stream, last_copy, 0)) != hipSuccess)
         return latch(p, e);
     return AQUA_OK;
+}
+
+// Link copies on the direction's SDMA engine.  Each layer group is one job
+// of the LinkEngine, queued on the engine during this call and released by
+// a one-lane kernel on the call's stream; the stream waits on the engine's
+// completed-job count where it needs copies done.  Swap-out: group k's job
+// is released after its gather; the gather into a slot waits until the job
+// that last used the slot (two jobs back) has completed, and the call ends
+// after its last job.  Swap-in: the first two jobs are released after the
+// call's earlier work, job k + 2 after the scatter of job k, which shares
+// its slot; each scatter waits for its own job.
+aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
+                                  hipStream_t stream, const RunDesc* descs, uint32_t ndesc,
+                                  uint64_t slot, uint32_t G, uint32_t l_begin, uint32_t l_end) {
+    aqua::LinkEngine& w = p->link[is_in];
+    const uint32_t K = (l_end - l_begin + G - 1) / G;
+    std::vector<aqua::LinkPiece> pieces;
+    auto group = [&](uint32_t k, uint32_t* l0, uint32_t* nl) {
+        *l0 = l_begin + k * G;
+        *nl = std::min<uint32_t>(G, l_end - *l0);
+        return p->staging[is_in] + (k % 2) * slot;
+    };
+    auto submit = [&](uint32_t k, int64_t** flag) {
+        uint32_t l0, nl;
+        uint8_t* s = group(k, &l0, &nl);
+        stage_pieces(p, !is_in, buf, s, G, l0, nl, &pieces);
+        return w.submit(pieces, flag);
+    };
+    auto kernel = [&](uint32_t k) {
+        uint32_t l0, nl;
+        uint8_t* s = group(k, &l0, &nl);
+        (void)hipGetLastError();
+        return aqua::launch_swap(slot_launch(p, is_in, s, descs, ndesc, l0, nl), stream);
+    };
+    auto release = [&](int64_t* a, int64_t* b) -> hipError_t {
+        if (!a) std::swap(a, b);
+        return a ? aqua::launch_release_flags(a, b, stream) : hipSuccess;
+    };
+    hipError_t e = hipSuccess;
+    if (!is_in) {
+        uint64_t first = 0, job = 0;
+        for (uint32_t k = 0; k < K; ++k) {
+            if (k >= 2 && (e = w.stream_wait(stream, first + k - 1)) != hipSuccess)
+                return latch(p, e);
+            if ((e = kernel(k)) != hipSuccess) return latch(p, e);
+            int64_t* flag = nullptr;
+            job = submit(k, &flag);
+            if (k == 0) first = job;
+            if ((e = release(flag, nullptr)) != hipSuccess) return latch(p, e);
+        }
+        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess) return latch(p, e);
+    } else {
+        int64_t* f0 = nullptr;
+        int64_t* f1 = nullptr;
+        const uint64_t first = submit(0, &f0);
+        if (K > 1) (void)submit(1, &f1);
+        if ((e = release(f0, f1)) != hipSuccess) return latch(p, e);
+        for (uint32_t k = 0; k < K; ++k) {
+            if ((e = w.stream_wait(stream, first + k + 1)) != hipSuccess) return latch(p, e);
+            if ((e = kernel(k)) != hipSuccess) return latch(p, e);
+            if (k + 2 < K) {
+                int64_t* flag = nullptr;
+                (void)submit(k + 2, &flag);
+                if ((e = release(flag, nullptr)) != hipSuccess) return latch(p, e);
+            }
+        }
+    }
+    return AQUA_OK;
+}
+
+aqua_status enqueue_staged(aqua_kv_pool* p, bool is_in, const void* buf, hipStream_t stream,
+                           const RunDesc* descs, uint32_t ndesc, uint64_t slot, uint32_t G,
+                           uint32_t l_begin, uint32_t l_end, Outstanding* rec) {
+    if (p->link[is_in].running())
+        return enqueue_staged_engine(p, is_in, buf, stream, descs, ndesc, slot, G, l_begin,
+                                     l_end);
+    return enqueue_staged_runtime(p, is_in, buf, stream, descs, ndesc, slot, G, l_begin, l_end,
+                                  rec);
 }
 
 aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
@@ -526,6 +673,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         c.img_blocks = nullptr;
         aqua::plan_runs(p->shape, c, p->unit_bytes, &p->plan);
         st = ensure_staging(p, is_in, 2 * slot);
+        if (st == AQUA_OK) st = ensure_link(p, is_in);
         if (st != AQUA_OK) return st;
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
@@ -840,6 +988,10 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
     {
         DeviceGuard dg(p->device);
         if (p->sticky == hipSuccess) st = wait_all(p);
+        // The link threads may still wait on the events below.
+        for (int dir = 0; dir < 2; ++dir) p->link[dir].stop();
+        if (p->hsa_up) aqua::link_release();
+        p->hsa_up = false;
         for (auto& q : p->outstanding)
             for (const Outstanding& o : q) {
                 (void)hipEventDestroy(o.ev);
@@ -950,6 +1102,26 @@ aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t p, int32_t target,
 aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t p, int32_t path) {
     if (!p || (path != AQUA_HOST_ZERO_COPY && path != AQUA_HOST_STAGED)) return AQUA_ERR_INVALID;
     p->host_path = path;
+    return AQUA_OK;
+}
+
+aqua_status aqua_kv_pool_set_link_engine(aqua_kv_pool_t p, int32_t dir, int32_t engine) {
+    if (!p || (dir != 0 && dir != 1) ||
+        !(engine == AQUA_LINK_AUTO || engine == AQUA_LINK_RUNTIME || (engine >= 0 && engine <= 15)))
+        return AQUA_ERR_INVALID;
+    if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
+    DeviceGuard dg(p->device);
+    const aqua_status st = wait_all(p);
+    if (st != AQUA_OK) return st;
+    p->link[dir].stop();
+    p->link_request[dir] = engine;
+    p->link_used[dir] = AQUA_LINK_AUTO;
+    return AQUA_OK;
+}
+
+aqua_status aqua_kv_pool_get_link_engine(aqua_kv_pool_t p, int32_t dir, int32_t* engine) {
+    if (!p || (dir != 0 && dir != 1) || !engine) return AQUA_ERR_INVALID;
+    *engine = p->link_used[dir];
     return AQUA_OK;
 }
 

@@ -1,0 +1,137 @@
+// link_engine.h -- copies over the host link on one chosen SDMA engine.
+//
+// The staged host path (the paper's temporary-tensor scheme, section 7,
+// "Efficient context switching") moves each layer group between an HBM slot
+// and pinned host memory.  Left to the runtime, a device-to-host copy may run
+// as a blit kernel or on any of the device's copy engines, and not all
+// engines reach the link rate.  A LinkEngine carries those copies on one
+// engine through the HSA runtime instead.
+//
+// A job is the set of copies of one layer group.  Its copies enter the
+// engine's queue when the job is submitted, during the swap call, each made
+// to wait for the job's ready flag; a one-lane kernel on the call's stream
+// releases the flag once the slot may be read or overwritten.  A library
+// thread waits for the jobs' completions in order and publishes the number
+// of completed jobs.  A stream that needs copies done is held by a host
+// function (hipLaunchHostFunc) that returns once the count is reached: the
+// command processor holds the stream, and no wave stays resident.  (A wave
+// waiting on a compute unit, even asleep, makes a full-chip kernel such as a
+// 256-tile GEMM run a second round of tiles; the runtime's own stream wait
+// on memory is such a kernel.)
+//
+// The engine runs its queue in order.  Everything in it, this library's
+// copies and any other user's, was queued after the work it depends on, so
+// the queue always drains: a job is never queued behind a copy that waits
+// for that job.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hsa/hsa.h>
+
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstdint>
+#include <deque>
+#include <memory>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+namespace aqua {
+
+// The GPU agent of a HIP device and the CPU agent nearest to it.
+struct LinkAgents {
+    hsa_agent_t gpu{};
+    hsa_agent_t cpu{};
+};
+
+// Initialises the HSA runtime (reference counted) and finds the agents of
+// `device`.  On success the caller owes one link_release().
+bool link_acquire(int device, LinkAgents* out);
+void link_release();
+
+// Engines for the two directions when the caller names none: the HSA
+// runtime's preferred engine for the direction if it names one, else the
+// lowest-numbered available engine, the two directions on different engines
+// where possible.  -1 where no engine is available.
+void link_auto_engines(const LinkAgents& a, int32_t* d2h, int32_t* h2d);
+
+// Enqueues one lane that stores 0, with system-scope release ordering, to
+// each non-null flag (a job's ready flag from LinkEngine::submit): the
+// stores are ordered after everything enqueued on `stream` before it.
+hipError_t launch_release_flags(int64_t* a, int64_t* b, hipStream_t stream);
+
+// Completed-job count of a LinkEngine.
+struct LinkProgress {
+    std::mutex mu;
+    std::condition_variable cv;
+    uint64_t completed = 0;
+    std::atomic<bool> gave_up{false};  // a wait hit its time limit
+    // Blocks until `completed` >= count; false (and gave_up set) after `limit`.
+    bool wait_for(uint64_t count, std::chrono::seconds limit);
+};
+
+struct LinkPiece {
+    void* dst;
+    const void* src;
+    uint64_t bytes;
+};
+
+class LinkEngine {
+  public:
+    LinkEngine() = default;
+    LinkEngine(const LinkEngine&) = delete;
+    LinkEngine& operator=(const LinkEngine&) = delete;
+    ~LinkEngine() { stop(); }
+
+    // dir 0: device memory to pinned host memory; 1: the reverse.
+    hipError_t start(int device, const LinkAgents& a, int dir, int32_t engine);
+    // Waits for every submitted job, then ends the thread.
+    void stop();
+
+    // Queues the copies of the next job on the engine, to run once the
+    // job's ready flag is released (launch_release_flags).  Returns the job's
+    // index (0, 1, ... in submission order) and the flag's device address.
+    // On failure the job still counts as submitted and is published, with
+    // the error kept for error().
+    uint64_t submit(const std::vector<LinkPiece>& pieces, int64_t** flag);
+    // Makes `stream` wait until `count` jobs have completed (a host function
+    // that gives up after the job time limit; error() reports it).
+    hipError_t stream_wait(hipStream_t stream, uint64_t count);
+
+    // First failure (hipSuccess if none).  A failed job is still published,
+    // so that no stream waits forever.
+    hipError_t error() const;
+    int32_t engine() const { return engine_; }
+    bool running() const { return th_.joinable(); }
+
+  private:
+    struct Job {
+        uint64_t index;
+        hsa_signal_t done;   // decremented once per completed copy
+        hsa_signal_t ready;  // the copies' dependency, released by a kernel
+    };
+    void loop();
+    void fail(hipError_t e);
+    void publish(uint64_t completed);
+    bool take_signals(hsa_signal_t* done, hsa_signal_t* ready);
+
+    int device_ = 0;
+    int32_t engine_ = -1;
+    hsa_agent_t dst_agent_{}, src_agent_{};
+    // Shared with the host functions holding streams, which may run after
+    // the engine has stopped.
+    std::shared_ptr<LinkProgress> progress_;
+    uint64_t issued_ = 0;    // jobs submitted (caller's thread)
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::deque<Job> q_;      // submitted, not yet published
+    std::vector<hsa_signal_t> spare_done_, spare_ready_, all_;
+    bool stop_ = false;
+    std::atomic<bool> stopping_{false};
+    std::atomic<int32_t> err_{0};
+    std::thread th_;
+};
+
+}  // namespace aqua

@@ -1,0 +1,328 @@
+// link_engine.hip -- host-link copies on a chosen SDMA engine, ordered against
+// HIP streams through a completed-job count in signal memory.
+#include "link_engine.h"
+
+#include <hsa/hsa_ext_amd.h>
+
+#include <new>
+
+#include <chrono>
+
+namespace aqua {
+
+namespace {
+
+struct FindGpu {
+    uint32_t domain, bus, dev;
+    hsa_agent_t found;
+    bool hit;
+};
+
+hsa_status_t find_gpu(hsa_agent_t a, void* data) {
+    FindGpu* f = static_cast<FindGpu*>(data);
+    hsa_device_type_t t;
+    if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &t) != HSA_STATUS_SUCCESS ||
+        t != HSA_DEVICE_TYPE_GPU)
+        return HSA_STATUS_SUCCESS;
+    uint32_t bdf = 0, dom = 0;
+    if (hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_BDFID, &bdf) !=
+        HSA_STATUS_SUCCESS)
+        return HSA_STATUS_SUCCESS;
+    if (hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_DOMAIN, &dom) !=
+        HSA_STATUS_SUCCESS)
+        dom = 0;
+    if ((bdf >> 8) == f->bus && ((bdf >> 3) & 0x1f) == f->dev && dom == f->domain) {
+        f->found = a;
+        f->hit = true;
+        return HSA_STATUS_INFO_BREAK;
+    }
+    return HSA_STATUS_SUCCESS;
+}
+
+hsa_status_t first_cpu(hsa_agent_t a, void* data) {
+    hsa_device_type_t t;
+    if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &t) == HSA_STATUS_SUCCESS &&
+        t == HSA_DEVICE_TYPE_CPU) {
+        *static_cast<hsa_agent_t*>(data) = a;
+        return HSA_STATUS_INFO_BREAK;
+    }
+    return HSA_STATUS_SUCCESS;
+}
+
+int32_t lowest_bit(uint32_t m) { return m ? (int32_t)__builtin_ctz(m) : -1; }
+
+// A job's copies take milliseconds once its ready flag is released; a job
+// not complete this long after the release is taken as failed.  (Before the
+// release the job waits for earlier work on the call's stream, for as long
+// as that takes.)
+constexpr auto kJobTimeLimit = std::chrono::seconds(60);
+// Wait slices, in HSA timestamp ticks (nanoseconds to 10 ns each).
+constexpr uint64_t kWaitHint = 10000000ull;
+
+// Releases up to two ready flags (see launch_release_flags).
+__global__ __launch_bounds__(64) void release_flags_kernel(int64_t* a, int64_t* b) {
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(a, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (b) __hip_atomic_store(b, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_release_flags(int64_t* a, int64_t* b, hipStream_t stream) {
+    if (!a) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(release_flags_kernel, dim3(1), dim3(64), 0, stream, a, b);
+    return hipGetLastError();
+}
+
+bool link_acquire(int device, LinkAgents* out) {
+    if (hsa_init() != HSA_STATUS_SUCCESS) return false;
+    int bus = 0, dev = 0, dom = 0;
+    if (hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, device) != hipSuccess ||
+        hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, device) != hipSuccess ||
+        hipDeviceGetAttribute(&dom, hipDeviceAttributePciDomainId, device) != hipSuccess) {
+        (void)hipGetLastError();
+        hsa_shut_down();
+        return false;
+    }
+    FindGpu f{(uint32_t)dom, (uint32_t)bus, (uint32_t)dev, {0}, false};
+    (void)hsa_iterate_agents(find_gpu, &f);
+    if (!f.hit) {
+        hsa_shut_down();
+        return false;
+    }
+    hsa_agent_t cpu{0};
+    if (hsa_agent_get_info(f.found, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_NEAREST_CPU, &cpu) !=
+            HSA_STATUS_SUCCESS ||
+        !cpu.handle) {
+        cpu.handle = 0;
+        (void)hsa_iterate_agents(first_cpu, &cpu);
+    }
+    if (!cpu.handle) {
+        hsa_shut_down();
+        return false;
+    }
+    out->gpu = f.found;
+    out->cpu = cpu;
+    return true;
+}
+
+void link_release() { hsa_shut_down(); }
+
+void link_auto_engines(const LinkAgents& a, int32_t* d2h, int32_t* h2d) {
+    uint32_t av[2] = {0, 0}, pref[2] = {0, 0};
+    if (hsa_amd_memory_copy_engine_status(a.cpu, a.gpu, &av[0]) != HSA_STATUS_SUCCESS) av[0] = 0;
+    if (hsa_amd_memory_copy_engine_status(a.gpu, a.cpu, &av[1]) != HSA_STATUS_SUCCESS) av[1] = 0;
+    if (hsa_amd_memory_get_preferred_copy_engine(a.cpu, a.gpu, &pref[0]) != HSA_STATUS_SUCCESS)
+        pref[0] = 0;
+    if (hsa_amd_memory_get_preferred_copy_engine(a.gpu, a.cpu, &pref[1]) != HSA_STATUS_SUCCESS)
+        pref[1] = 0;
+    const uint32_t m0 = (pref[0] & av[0]) ? (pref[0] & av[0]) : av[0];
+    *d2h = lowest_bit(m0);
+    const uint32_t m1 = (pref[1] & av[1]) ? (pref[1] & av[1]) : av[1];
+    const uint32_t m1x = *d2h >= 0 ? (m1 & ~(1u << *d2h)) : m1;
+    *h2d = lowest_bit(m1x ? m1x : m1);
+}
+
+hipError_t LinkEngine::start(int device, const LinkAgents& a, int dir, int32_t engine) {
+    if (running() || engine < 0 || engine > 15) return hipErrorInvalidValue;
+    device_ = device;
+    engine_ = engine;
+    dst_agent_ = dir == 0 ? a.cpu : a.gpu;
+    src_agent_ = dir == 0 ? a.gpu : a.cpu;
+    progress_ = std::make_shared<LinkProgress>();
+    issued_ = 0;
+    stop_ = false;
+    err_.store(0);
+    th_ = std::thread([this] { loop(); });
+    return hipSuccess;
+}
+
+void LinkEngine::stop() {
+    if (!th_.joinable()) return;
+    {
+        std::lock_guard<std::mutex> lk(mu_);
+        stop_ = true;
+    }
+    stopping_.store(true, std::memory_order_release);
+    cv_.notify_all();
+    th_.join();
+    stopping_.store(false);
+    for (hsa_signal_t sg : all_) hsa_signal_destroy(sg);
+    all_.clear();
+    spare_done_.clear();
+    spare_ready_.clear();
+    progress_.reset();
+}
+
+bool LinkEngine::take_signals(hsa_signal_t* done, hsa_signal_t* ready) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (spare_done_.empty()) {
+        hsa_signal_t sg;
+        if (hsa_signal_create(0, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) return false;
+        all_.push_back(sg);
+        spare_done_.push_back(sg);
+    }
+    if (spare_ready_.empty()) {
+        // Waited on by the engine only; a kernel stores its value directly.
+        hsa_signal_t sg;
+        if (hsa_amd_signal_create(1, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, &sg) !=
+            HSA_STATUS_SUCCESS)
+            return false;
+        all_.push_back(sg);
+        spare_ready_.push_back(sg);
+    }
+    *done = spare_done_.back();
+    spare_done_.pop_back();
+    *ready = spare_ready_.back();
+    spare_ready_.pop_back();
+    return true;
+}
+
+uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag) {
+    *flag = nullptr;
+    const uint64_t index = issued_++;
+    Job job{index, {0}, {0}};
+    volatile hsa_signal_value_t* value = nullptr;
+    if (err_.load(std::memory_order_acquire) == 0) {
+        if (!take_signals(&job.done, &job.ready)) {
+            fail(hipErrorOutOfMemory);
+        } else if (hsa_amd_signal_value_pointer(job.ready, &value) != HSA_STATUS_SUCCESS) {
+            fail(hipErrorInvalidValue);
+            std::lock_guard<std::mutex> lk(mu_);
+            spare_done_.push_back(job.done);
+            spare_ready_.push_back(job.ready);
+            job.done.handle = job.ready.handle = 0;
+        }
+    }
+    if (job.done.handle) {
+        const uint64_t n = pieces.size();
+        hsa_signal_store_relaxed(job.ready, 1);
+        hsa_signal_store_relaxed(job.done, (hsa_signal_value_t)n);
+        uint64_t issued = 0;
+        for (const LinkPiece& pc : pieces) {
+            if (hsa_amd_memory_async_copy_on_engine(
+                    pc.dst, dst_agent_, pc.src, src_agent_, pc.bytes, 1, &job.ready, job.done,
+                    (hsa_amd_sdma_engine_id_t)(1u << engine_), true) != HSA_STATUS_SUCCESS) {
+                fail(hipErrorUnknown);
+                break;
+            }
+            ++issued;
+        }
+        if (issued < n) hsa_signal_subtract_relaxed(job.done, (hsa_signal_value_t)(n - issued));
+        // Copies already queued wait for the flag, so it is handed out even
+        // when some failed to queue.
+        *flag = const_cast<int64_t*>(value);
+    }
+    {
+        std::lock_guard<std::mutex> lk(mu_);
+        q_.push_back(job);
+    }
+    cv_.notify_one();
+    return index;
+}
+
+bool LinkProgress::wait_for(uint64_t count, std::chrono::seconds limit) {
+    std::unique_lock<std::mutex> lk(mu);
+    if (cv.wait_for(lk, limit, [&] { return completed >= count; })) return true;
+    gave_up.store(true, std::memory_order_release);
+    return false;
+}
+
+namespace {
+
+struct HoldArgs {
+    std::shared_ptr<LinkProgress> progress;  // alive while the function is pending
+    uint64_t count;
+};
+
+// Runs on the runtime's callback thread when the stream reaches it; the
+// stream's later work waits until it returns.  Makes no HIP call.
+void hold_stream(void* arg) {
+    HoldArgs* a = static_cast<HoldArgs*>(arg);
+    (void)a->progress->wait_for(a->count, kJobTimeLimit);
+    delete a;
+}
+
+}  // namespace
+
+hipError_t LinkEngine::stream_wait(hipStream_t stream, uint64_t count) {
+    {
+        std::lock_guard<std::mutex> lk(progress_->mu);
+        if (progress_->completed >= count) return hipSuccess;  // nothing to wait for
+    }
+    HoldArgs* a = new (std::nothrow) HoldArgs{progress_, count};
+    if (!a) return hipErrorOutOfMemory;
+    const hipError_t e = hipLaunchHostFunc(stream, hold_stream, a);
+    if (e != hipSuccess) delete a;
+    return e;
+}
+
+hipError_t LinkEngine::error() const {
+    const int32_t e = err_.load(std::memory_order_acquire);
+    if (e) return (hipError_t)e;
+    if (progress_ && progress_->gave_up.load(std::memory_order_acquire))
+        return hipErrorLaunchTimeOut;
+    return hipSuccess;
+}
+
+void LinkEngine::fail(hipError_t e) {
+    int32_t none = 0;
+    (void)err_.compare_exchange_strong(none, (int32_t)e);
+}
+
+void LinkEngine::publish(uint64_t completed) {
+    {
+        std::lock_guard<std::mutex> lk(progress_->mu);
+        progress_->completed = completed;
+    }
+    progress_->cv.notify_all();
+}
+
+void LinkEngine::loop() {
+    for (;;) {
+        Job job;
+        {
+            std::unique_lock<std::mutex> lk(mu_);
+            cv_.wait(lk, [&] { return stop_ || !q_.empty(); });
+            if (q_.empty()) return;  // stopped, nothing left
+            job = q_.front();
+        }
+        bool recycle = job.done.handle != 0;
+        if (job.done.handle) {
+            auto t0 = std::chrono::steady_clock::now();
+            bool released = false;
+            while (hsa_signal_wait_scacquire(job.done, HSA_SIGNAL_CONDITION_LT, 1, kWaitHint,
+                                             HSA_WAIT_STATE_BLOCKED) >= 1) {
+                if (!released && stopping_.load(std::memory_order_acquire)) {
+                    // Stopping: a flag not released by now may never be (a
+                    // call that failed before launching its release), so
+                    // the time limit runs from here as well.
+                    released = hsa_signal_load_relaxed(job.ready) == 0;
+                    if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
+                        fail(hipErrorLaunchTimeOut);
+                        recycle = false;
+                        break;
+                    }
+                } else if (!released) {
+                    released = hsa_signal_load_relaxed(job.ready) == 0;
+                    t0 = std::chrono::steady_clock::now();
+                } else if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
+                    // The engine may still touch these signals: never reuse them.
+                    fail(hipErrorLaunchTimeOut);
+                    recycle = false;
+                    break;
+                }
+            }
+        }
+        publish(job.index + 1);
+        std::lock_guard<std::mutex> lk(mu_);
+        q_.pop_front();
+        if (recycle) {
+            spare_done_.push_back(job.done);
+            spare_ready_.push_back(job.ready);
+        }
+    }
+}
+
+}  // namespace aqua

@@ -27,7 +27,8 @@ def _gpu():
 
 
 def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
-               buf_bytes=None, pinned=False, sentinel=True, stream=None, host_path=None):
+               buf_bytes=None, pinned=False, sentinel=True, stream=None, host_path=None,
+               carrier=None):
     """swap_out(out_tables) then swap_in(in_tables) on the GPU and in the
     oracle; compares the image, guards and the whole pool."""
     C = shape.chunk_bytes
@@ -47,6 +48,9 @@ def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
     kv = aqua.KVPool(shape.as_tuple(), pool)
     if host_path is not None:
         kv.set_host_path(host_path)
+    if carrier is not None:
+        for direction in (0, 1):
+            kv.set_link_engine(direction, carrier)
     try:
         t1 = kv.swap_out(out_tables, inner, img_offsets, stream=stream)
         kv.sync(t1)
@@ -63,6 +67,13 @@ def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
         assert_bytes_equal(host(buf), want, "swap-in changed the image or guards")
         st = kv.stats()
         assert st["calls_out"] == 1 and st["calls_in"] == 1 and st["hip_error"] == 0
+        if carrier is not None:
+            used = [kv.link_engine(0), kv.link_engine(1)]
+            say("link carriers", used)
+            if carrier == aqua.AQUA_LINK_AUTO:
+                assert all(u >= 0 or u == aqua.AQUA_LINK_RUNTIME for u in used)
+            else:
+                assert used == [carrier, carrier]
     finally:
         kv.close()
     return pool_h
@@ -167,6 +178,85 @@ def test_pinned_host_staged_placed_images(shape):
     say("staged placed", shape)
     _roundtrip(shape, 8, out_tables, in_tables, None, img_offsets=offs, buf_bytes=pos + 4096,
                pinned=True, host_path=aqua.AQUA_HOST_STAGED)
+
+
+@pytest.mark.parametrize("carrier", [aqua.AQUA_LINK_AUTO, aqua.AQUA_LINK_RUNTIME, 3],
+                         ids=["auto", "runtime", "engine3"])
+def test_staged_link_carriers_cycle_slots(carrier, monkeypatch):
+    """Staged swaps through 1 MiB slots, so that every call refills both
+    slots several times (one layer per slot fill), with the link copies on
+    the automatic choice, on the runtime's copies and on engine 3."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    shape = wl.KVShape(8, 1024, 4, 16, 64, wl.BF16)       # 16 KiB chunks
+    perm = wl.permutation(shape.num_blocks, 77)
+    out_tables = [perm[0:100], perm[100:130], perm[130:300]]
+    in_tables = [perm[300:400], perm[400:430], perm[430:600]]
+    say("staged slot cycling", carrier)
+    _roundtrip(shape, 21, out_tables, in_tables, None, pinned=True,
+               host_path=aqua.AQUA_HOST_STAGED, carrier=carrier)
+
+
+@pytest.mark.parametrize("carrier", [aqua.AQUA_LINK_AUTO, aqua.AQUA_LINK_RUNTIME],
+                         ids=["auto", "runtime"])
+def test_staged_calls_back_to_back_without_host_sync(carrier, monkeypatch):
+    """Six staged calls with no host sync between them: out, in, out, in on
+    one stream through two pinned images, then out and in on a second
+    stream.  Each call cycles 1 MiB slots several times, so a call's first
+    link job is queued while the previous call's last job may still be in
+    flight.  The pool and all three images must equal the oracle's replay."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    shape = wl.KVShape(8, 1024, 4, 16, 64, wl.BF16)       # 16 KiB chunks
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 91)
+    ta = [perm[0:100], perm[100:130], perm[130:300]]
+    tb = [perm[300:400], perm[400:430], perm[430:600]]
+    tc = [perm[600:700], perm[700:730], perm[730:900]]
+    owner = {b: (p, i) for p, t in enumerate(ta) for i, b in enumerate(t)}
+    pool = device_pool(shape, 31, owner)
+    pool_h = host(pool)
+    size = shape.image_bytes(300)
+    imgs = [guarded_buffer(size, G, True) for _ in range(3)]
+    want = [np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8) for _ in range(3)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    kv.set_host_path(aqua.AQUA_HOST_STAGED)
+    for direction in (0, 1):
+        kv.set_link_engine(direction, carrier)
+    calls = [("out", ta, 0, s1), ("in", tb, 0, s1), ("out", tb, 1, s1), ("in", ta, 1, s1),
+             ("out", ta, 2, s2), ("in", tc, 2, s2)]
+    say("staged back to back", carrier)
+    try:
+        for kind, t, k, st in calls:
+            inner = imgs[k][G:G + size]
+            (kv.swap_out if kind == "out" else kv.swap_in)(t, inner, stream=st)
+        kv.sync()
+        for kind, t, k, _ in calls:
+            fn = oracle.swap_out if kind == "out" else oracle.swap_in
+            assert fn(d, pool_h, t, want[k][G:G + size]) == 0
+        assert_bytes_equal(host(pool), pool_h, "pool after six staged calls")
+        for k in range(3):
+            assert_bytes_equal(host(imgs[k]), want[k], f"image {k}")
+        stt = kv.stats()
+        say("link carriers", [kv.link_engine(0), kv.link_engine(1)], stt["waits_inserted"])
+        assert stt["hip_error"] == 0 and stt["calls_out"] == 3 and stt["calls_in"] == 3
+    finally:
+        kv.close()
+
+
+def test_link_engine_setter_rejects_bad_arguments():
+    shape = wl.KVShape(2, 64, 1, 2, 8, wl.BF16)
+    pool = device_pool(shape, 3)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        assert kv.link_engine(0) == aqua.AQUA_LINK_AUTO      # nothing staged yet
+        for direction, engine in [(2, 0), (-1, 0), (0, 16), (1, -3)]:
+            with pytest.raises(aqua.AquaError) as ei:
+                kv.set_link_engine(direction, engine)
+            assert ei.value.status == aqua.AQUA_ERR_INVALID
+        kv.set_link_engine(1, aqua.AQUA_LINK_RUNTIME)
+        assert kv.link_engine(1) == aqua.AQUA_LINK_AUTO      # chosen on the next staged call
+    finally:
+        kv.close()
 
 
 def test_errors_match_oracle_and_leave_no_trace():
