@@ -247,6 +247,7 @@ def run_pair(args, res_common):
         alone_ms = gemm_ms(alone)
         t0 = time.perf_counter()
         during = []
+    st0 = kv.stats()
     for i in range(args.steps):
         if args.gemm:
             during += gemm_run(comp, a, per_step)
@@ -254,7 +255,7 @@ def run_pair(args, res_common):
     kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    st = kv.stats()
+    st = _since(kv.stats(), st0)
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
                if pinned and args.host_path == "staged" else None)
     kv.close()
@@ -347,6 +348,12 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
     return out
 
 
+def _since(after: dict, before: dict) -> dict:
+    """Pool counters accumulated between two snapshots (the timed steps
+    only: the first staged call of a direction also allocates its slots)."""
+    return {k: (v - before[k] if k != "hip_error" else v) for k, v in after.items()}
+
+
 LINK_ENGINE = {"auto": -2, "runtime": -1}
 _link_request = "auto"
 
@@ -403,13 +410,14 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
         one(k, False)
     kv.sync(0)
     torch.cuda.synchronize()
+    st0 = kv.stats()
     t0 = time.perf_counter()
     for k in ids[warmup:]:
         one(k, True)
     kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    st = kv.stats()
+    st = _since(kv.stats(), st0)
     kv.close()
     unit = s.num_layers * s.chunk_bytes
     out_b = np.array([e[4] for e in evs], dtype=np.float64) * unit
@@ -609,13 +617,14 @@ def run_next(args, res_common):
     kv.sync(0)
     torch.cuda.synchronize()
     evs = []
+    st0 = kv.stats()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step(evs)
     kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    st = kv.stats()
+    st = _since(kv.stats(), st0)
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
                if pinned and args.host_path == "staged" else None)
     kv.close()

@@ -242,9 +242,10 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
 /* How swaps with a pinned-host target move their bytes.
  *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
  *     (section 7, "Efficient context switching").  Layers pass through two
- *     HBM slots owned by the library (256 MiB each by default, allocated on
- *     a direction's first staged call, after waiting for every outstanding
- *     call): the gather kernel fills a slot and a copy engine moves it over
+ *     HBM slots owned by the library (256 MiB each by default, allocated
+ *     for both directions on the pool's first staged call, after waiting for
+ *     every outstanding call, and grown the same way when a call needs
+ *     larger ones): the gather kernel fills a slot and a copy engine moves it over
  *     the link while the next slot is filled, and the reverse on swap-in.
  *     Swap-outs and swap-ins have their own slots and link carrier (see
  *     aqua_kv_pool_set_link_engine), so a swap-out and a swap-in on

@@ -301,21 +301,56 @@ aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off) {
 }
 
 // Makes direction dir's staging buffer hold at least `bytes`, waiting for
-// every outstanding call before it is replaced.
+// every outstanding call before it is replaced.  A direction without slots
+// gets them at the same time, best effort (two slots of the default size,
+// or `bytes` if larger), so that its first staged call does not wait for
+// this one.
 aqua_status ensure_staging(aqua_kv_pool* p, int dir, uint64_t bytes) {
     if (bytes <= p->staging_bytes[dir]) return AQUA_OK;
     aqua_status st = wait_all(p);
     if (st != AQUA_OK) return st;
-    if (p->staging[dir]) (void)hipFree(p->staging[dir]);
-    p->staging[dir] = nullptr;
-    p->staging_bytes[dir] = 0;
-    if (hipMalloc((void**)&p->staging[dir], bytes) != hipSuccess) {
-        (void)hipGetLastError();
-        p->staging[dir] = nullptr;
-        return AQUA_ERR_HIP;
-    }
-    p->staging_bytes[dir] = bytes;
-    return AQUA_OK;
+    auto alloc = [&](int d, uint64_t nb) -> aqua_status {
+        if (p->staging[d]) (void)hipFree(p->staging[d]);
+        p->staging[d] = nullptr;
+        p->staging_bytes[d] = 0;
+        if (hipMalloc((void**)&p->staging[d], nb) != hipSuccess) {
+            (void)hipGetLastError();
+            p->staging[d] = nullptr;
+            return AQUA_ERR_HIP;
+        }
+        p->staging_bytes[d] = nb;
+        return AQUA_OK;
+    };
+    st = alloc(dir, bytes);
+    // Best effort: on failure the other direction allocates on its own call.
+    if (st == AQUA_OK && !p->staging[1 - dir])
+        (void)alloc(1 - dir, std::max<uint64_t>(bytes, 2 * p->slot_target));
+    return st;
+}
+
+// Copies n 16-byte vectors of run descriptors from the pinned host ring to
+// the device ring (see upload_descs).
+__global__ __launch_bounds__(256) void upload_descs_kernel(const uint4* __restrict__ src,
+                                                           uint4* __restrict__ dst, uint32_t n) {
+    for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < n; i += gridDim.x * 256u)
+        dst[i] = src[i];
+}
+
+// Moves a call's descriptors, [ring_off, ring_off + bytes) of the rings, to
+// the device ring on the call's stream: one pass over the link ahead of the
+// call's kernels instead of a fetch per workgroup while the link carries
+// the call's own data.  A kernel, not a runtime copy: the runtime can hold
+// the calling thread on such a small copy until the stream's earlier host
+// functions have run.  `bytes` is a multiple of 32 (whole descriptors).
+hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipStream_t stream) {
+    const uint32_t n = (uint32_t)(bytes / 16);
+    if (!n) return hipSuccess;
+    const uint32_t grid = std::min<uint32_t>(256u, (n + 255u) / 256u);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(upload_descs_kernel, dim3(grid), dim3(256), 0, stream,
+                       reinterpret_cast<const uint4*>(p->ring_host_dev + ring_off),
+                       reinterpret_cast<uint4*>(p->ring_dev + ring_off), n);
+    return hipGetLastError();
 }
 
 // Chooses direction dir's carrier for link copies on its first staged call:
@@ -739,8 +774,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         const uint8_t* descs = p->ring_host_dev + ring_off;
         if (staged) {
             descs = p->ring_dev + ring_off;
-            e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
-                               hipMemcpyHostToDevice, stream);
+            e = upload_descs(p, ring_off, dbytes, stream);
         }
         if (e != hipSuccess) return latch(p, e);
         if (staged) {
@@ -864,8 +898,7 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
         // Descriptors go to the device ring: a migration touching host
         // memory keeps the link busy.
         std::memcpy(p->ring_host + ring_off, pieces.data(), dbytes);
-        hipError_t e = hipMemcpyAsync(p->ring_dev + ring_off, p->ring_host + ring_off, dbytes,
-                                      hipMemcpyHostToDevice, stream);
+        hipError_t e = upload_descs(p, ring_off, dbytes, stream);
         if (e != hipSuccess) return latch(p, e);
         const bool host_side = src_target == AQUA_TARGET_HOST || dst_target == AQUA_TARGET_HOST;
         (void)hipGetLastError();

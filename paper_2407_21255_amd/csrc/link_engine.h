@@ -109,13 +109,13 @@ class LinkEngine {
   private:
     struct Job {
         uint64_t index;
-        hsa_signal_t done;   // decremented once per completed copy
+        uint64_t end;        // copies queued on the engine up to and including this job
         hsa_signal_t ready;  // the copies' dependency, released by a kernel
     };
     void loop();
     void fail(hipError_t e);
     void publish(uint64_t completed);
-    bool take_signals(hsa_signal_t* done, hsa_signal_t* ready);
+    bool take_ready(hsa_signal_t* ready);
 
     int device_ = 0;
     int32_t engine_ = -1;
@@ -127,7 +127,9 @@ class LinkEngine {
     std::mutex mu_;
     std::condition_variable cv_;
     std::deque<Job> q_;      // submitted, not yet published
-    std::vector<hsa_signal_t> spare_done_, spare_ready_, all_;
+    hsa_signal_t done_{0};   // decremented by every completed copy, in queue order
+    uint64_t queued_ = 0;    // copies queued so far (caller's thread)
+    std::vector<hsa_signal_t> spare_ready_, all_;
     bool stop_ = false;
     std::atomic<bool> stopping_{false};
     std::atomic<int32_t> err_{0};

@@ -58,6 +58,8 @@ int32_t lowest_bit(uint32_t m) { return m ? (int32_t)__builtin_ctz(m) : -1; }
 constexpr auto kJobTimeLimit = std::chrono::seconds(60);
 // Wait slices, in HSA timestamp ticks (nanoseconds to 10 ns each).
 constexpr uint64_t kWaitHint = 10000000ull;
+// Start value of an engine's completion signal, which every copy decrements.
+constexpr hsa_signal_value_t kDoneBase = (hsa_signal_value_t)1 << 62;
 
 // Releases up to two ready flags (see launch_release_flags).
 __global__ __launch_bounds__(64) void release_flags_kernel(int64_t* a, int64_t* b) {
@@ -131,6 +133,11 @@ hipError_t LinkEngine::start(int device, const LinkAgents& a, int dir, int32_t e
     dst_agent_ = dir == 0 ? a.cpu : a.gpu;
     src_agent_ = dir == 0 ? a.gpu : a.cpu;
     progress_ = std::make_shared<LinkProgress>();
+    if (hsa_signal_create(kDoneBase, 0, nullptr, &done_) != HSA_STATUS_SUCCESS) {
+        done_.handle = 0;
+        return hipErrorOutOfMemory;
+    }
+    queued_ = 0;
     issued_ = 0;
     stop_ = false;
     err_.store(0);
@@ -150,19 +157,14 @@ void LinkEngine::stop() {
     stopping_.store(false);
     for (hsa_signal_t sg : all_) hsa_signal_destroy(sg);
     all_.clear();
-    spare_done_.clear();
     spare_ready_.clear();
+    if (done_.handle) hsa_signal_destroy(done_);
+    done_.handle = 0;
     progress_.reset();
 }
 
-bool LinkEngine::take_signals(hsa_signal_t* done, hsa_signal_t* ready) {
+bool LinkEngine::take_ready(hsa_signal_t* ready) {
     std::lock_guard<std::mutex> lk(mu_);
-    if (spare_done_.empty()) {
-        hsa_signal_t sg;
-        if (hsa_signal_create(0, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) return false;
-        all_.push_back(sg);
-        spare_done_.push_back(sg);
-    }
     if (spare_ready_.empty()) {
         // Waited on by the engine only; a kernel stores its value directly.
         hsa_signal_t sg;
@@ -172,8 +174,6 @@ bool LinkEngine::take_signals(hsa_signal_t* done, hsa_signal_t* ready) {
         all_.push_back(sg);
         spare_ready_.push_back(sg);
     }
-    *done = spare_done_.back();
-    spare_done_.pop_back();
     *ready = spare_ready_.back();
     spare_ready_.pop_back();
     return true;
@@ -182,34 +182,30 @@ bool LinkEngine::take_signals(hsa_signal_t* done, hsa_signal_t* ready) {
 uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag) {
     *flag = nullptr;
     const uint64_t index = issued_++;
-    Job job{index, {0}, {0}};
+    Job job{index, queued_, {0}};
     volatile hsa_signal_value_t* value = nullptr;
     if (err_.load(std::memory_order_acquire) == 0) {
-        if (!take_signals(&job.done, &job.ready)) {
+        if (!take_ready(&job.ready)) {
             fail(hipErrorOutOfMemory);
         } else if (hsa_amd_signal_value_pointer(job.ready, &value) != HSA_STATUS_SUCCESS) {
             fail(hipErrorInvalidValue);
             std::lock_guard<std::mutex> lk(mu_);
-            spare_done_.push_back(job.done);
             spare_ready_.push_back(job.ready);
-            job.done.handle = job.ready.handle = 0;
+            job.ready.handle = 0;
         }
     }
-    if (job.done.handle) {
-        const uint64_t n = pieces.size();
+    if (job.ready.handle) {
         hsa_signal_store_relaxed(job.ready, 1);
-        hsa_signal_store_relaxed(job.done, (hsa_signal_value_t)n);
-        uint64_t issued = 0;
         for (const LinkPiece& pc : pieces) {
             if (hsa_amd_memory_async_copy_on_engine(
-                    pc.dst, dst_agent_, pc.src, src_agent_, pc.bytes, 1, &job.ready, job.done,
+                    pc.dst, dst_agent_, pc.src, src_agent_, pc.bytes, 1, &job.ready, done_,
                     (hsa_amd_sdma_engine_id_t)(1u << engine_), true) != HSA_STATUS_SUCCESS) {
                 fail(hipErrorUnknown);
                 break;
             }
-            ++issued;
+            ++queued_;
         }
-        if (issued < n) hsa_signal_subtract_relaxed(job.done, (hsa_signal_value_t)(n - issued));
+        job.end = queued_;
         // Copies already queued wait for the flag, so it is handed out even
         // when some failed to queue.
         *flag = const_cast<int64_t*>(value);
@@ -288,12 +284,16 @@ void LinkEngine::loop() {
             if (q_.empty()) return;  // stopped, nothing left
             job = q_.front();
         }
-        bool recycle = job.done.handle != 0;
-        if (job.done.handle) {
+        // The engine completes copies in queue order, each decrementing
+        // done_ once: the job is complete when done_ has dropped by the
+        // number of copies queued up to and including it.
+        const hsa_signal_value_t target = kDoneBase - (hsa_signal_value_t)job.end;
+        bool recycle = job.ready.handle != 0;
+        if (job.ready.handle) {
             auto t0 = std::chrono::steady_clock::now();
             bool released = false;
-            while (hsa_signal_wait_scacquire(job.done, HSA_SIGNAL_CONDITION_LT, 1, kWaitHint,
-                                             HSA_WAIT_STATE_BLOCKED) >= 1) {
+            while (hsa_signal_wait_scacquire(done_, HSA_SIGNAL_CONDITION_LT, target + 1,
+                                             kWaitHint, HSA_WAIT_STATE_BLOCKED) > target) {
                 if (!released && stopping_.load(std::memory_order_acquire)) {
                     // Stopping: a flag not released by now may never be (a
                     // call that failed before launching its release), so
@@ -308,7 +308,7 @@ void LinkEngine::loop() {
                     released = hsa_signal_load_relaxed(job.ready) == 0;
                     t0 = std::chrono::steady_clock::now();
                 } else if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
-                    // The engine may still touch these signals: never reuse them.
+                    // The engine may still wait on this flag: never reuse it.
                     fail(hipErrorLaunchTimeOut);
                     recycle = false;
                     break;
@@ -318,10 +318,7 @@ void LinkEngine::loop() {
         publish(job.index + 1);
         std::lock_guard<std::mutex> lk(mu_);
         q_.pop_front();
-        if (recycle) {
-            spare_done_.push_back(job.done);
-            spare_ready_.push_back(job.ready);
-        }
+        if (recycle) spare_ready_.push_back(job.ready);
     }
 }
 
