@@ -166,6 +166,39 @@ def gemm_run(stream, a, iters, per_kernel=True):
     return evs
 
 
+class GemmCompanion:
+    """4096^3 bf16 GEMMs on a compute stream beside the timed steps: about
+    one step's worth per step (estimated from the warm-up), first timed
+    alone, after a warm-up, so that both figures cover the same span of
+    sustained work."""
+
+    def __init__(self, step_s, steps):
+        import torch
+        self.comp = torch.cuda.Stream()
+        self.a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+        gemm_run(self.comp, self.a, 20)
+        torch.cuda.synchronize()
+        est = gemm_run(self.comp, self.a, 20, per_kernel=False)
+        torch.cuda.synchronize()
+        self.per_step = max(1, int(step_s * 1e3 / (gemm_ms(est) / 20)))
+        self.n = self.per_step * steps
+        alone = gemm_run(self.comp, self.a, self.n)
+        torch.cuda.synchronize()
+        self.alone_ms = gemm_ms(alone)
+        self.during = []
+
+    def step(self):
+        self.during += gemm_run(self.comp, self.a, self.per_step)
+
+    def result(self):
+        # Kernel time of each GEMM alone and while the swaps run (gaps in the
+        # compute stream are not counted).
+        during_ms = gemm_ms(self.during)
+        return {"gemm_ms_alone": round(self.alone_ms, 4),
+                "gemm_ms_during_swaps": round(during_ms, 4), "gemm_iters": self.n,
+                "slowdown": round(during_ms / self.alone_ms - 1, 4)}
+
+
 def gemm_ms(evs):
     return sum(x.elapsed_time(y) for x, y in evs) / len(evs)
 
@@ -227,30 +260,14 @@ def run_pair(args, res_common):
     kv.sync(0)
     torch.cuda.synchronize()
     step_s = (time.perf_counter() - tw) / (args.warmup - 1) if args.warmup > 1 else 0.0
+    # GEMMs enqueued step by step beside the swaps, so that both streams
+    # start together.
+    comp = GemmCompanion(step_s, args.steps) if args.gemm else None
     t0 = time.perf_counter()
-    if args.gemm:
-        # GEMMs on a compute stream for about the length of the timed window
-        # (estimated from the warm-up steps), enqueued step by step beside the
-        # swaps so that both streams start together.  The same number of
-        # GEMMs is first timed alone, after a warm-up, so that both figures
-        # cover the same span of sustained work.
-        comp = torch.cuda.Stream()
-        a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
-        gemm_run(comp, a, 20)
-        torch.cuda.synchronize()
-        est = gemm_run(comp, a, 20, per_kernel=False)
-        torch.cuda.synchronize()
-        per_step = max(1, int(step_s * 1e3 / (gemm_ms(est) / 20)))
-        n_g = per_step * args.steps
-        alone = gemm_run(comp, a, n_g)
-        torch.cuda.synchronize()
-        alone_ms = gemm_ms(alone)
-        t0 = time.perf_counter()
-        during = []
     st0 = kv.stats()
     for i in range(args.steps):
-        if args.gemm:
-            during += gemm_run(comp, a, per_step)
+        if comp:
+            comp.step()
         step(args.warmup + i, True)
     kv.sync(0)
     torch.cuda.synchronize()
@@ -259,12 +276,8 @@ def run_pair(args, res_common):
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
                if pinned and args.host_path == "staged" else None)
     kv.close()
-    if args.gemm:
-        # Kernel time of each GEMM alone and while the swaps run (gaps in the
-        # compute stream are not counted).
-        during_ms = gemm_ms(during)
-        gemm = {"gemm_ms_alone": round(alone_ms, 4), "gemm_ms_during_swaps": round(during_ms, 4),
-                "gemm_iters": n_g, "slowdown": round(during_ms / alone_ms - 1, 4)}
+    if comp:
+        gemm = comp.result()
 
     out_ms = np.array([a.elapsed_time(b) for a, b, _ in evs])
     in_ms = np.array([b.elapsed_time(c) for _, b, c in evs])
@@ -358,17 +371,21 @@ LINK_ENGINE = {"auto": -2, "runtime": -1}
 _link_request = "auto"
 
 
+def _configure_link(kv):
+    """Carrier of a pool's link copies (``--link-engine``): staged host swaps
+    and migrations between HBM and host memory."""
+    e = LINK_ENGINE.get(_link_request)
+    e = int(_link_request) if e is None else e
+    for direction in (0, 1):
+        kv.set_link_engine(direction, e)
+
+
 def _configure_host(kv, host_path):
-    """Host path of a pool, and for the staged path the carrier of its link
-    copies (``--link-engine``)."""
+    """Host path of a pool and the carrier of its link copies."""
     from paper_2407_21255_amd import aqua
     kv.set_host_path(aqua.AQUA_HOST_STAGED if host_path == "staged"
                      else aqua.AQUA_HOST_ZERO_COPY)
-    if host_path == "staged":
-        e = LINK_ENGINE.get(_link_request)
-        e = int(_link_request) if e is None else e
-        for direction in (0, 1):
-            kv.set_link_engine(direction, e)
+    _configure_link(kv)
 
 
 def _time_slices(sched, pool, region, ids, warmup, host_path=None):
@@ -576,6 +593,8 @@ def run_next(args, res_common):
     kv = aqua.KVPool(s.as_tuple(), pool)
     if pinned:
         _configure_host(kv, args.host_path)
+    else:
+        _configure_link(kv)
     kv.swap_out([prompt], img, stream=stream)
     kv.sync(0)
     extra = {}
@@ -612,21 +631,33 @@ def run_next(args, res_common):
             e1.record(stream)
             timed_evs.append((e0, e1))
     warm = []
-    for _ in range(args.warmup):
+    tw = None
+    # With GEMMs beside the steps, a warm step after the first sizes the GEMM
+    # load.
+    for i in range(max(args.warmup, 2) if args.gemm else args.warmup):
+        if i == 1:
+            kv.sync(0)
+            torch.cuda.synchronize()
+            tw = time.perf_counter()
         step(warm)
     kv.sync(0)
     torch.cuda.synchronize()
+    n_warm = max(args.warmup, 2) if args.gemm else args.warmup
+    step_s = (time.perf_counter() - tw) / (n_warm - 1) if tw is not None else 0.0
+    comp = GemmCompanion(step_s, args.steps) if args.gemm else None
     evs = []
     st0 = kv.stats()
     t0 = time.perf_counter()
     for _ in range(args.steps):
+        if comp:
+            comp.step()
         step(evs)
     kv.sync(0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = _since(kv.stats(), st0)
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
-               if pinned and args.host_path == "staged" else None)
+               if (pinned and args.host_path == "staged") or w == "migrate" else None)
     kv.close()
     if w == "migrate":
         d2h = np.mean([a.elapsed_time(b) for a, b, _ in evs])
@@ -669,6 +700,8 @@ def run_next(args, res_common):
                                                        st["calls_migrate"]) / 1e3, 2),
         "kernel_source": _kernel_hash(),
     })
+    if comp:
+        res["compute_stream"] = comp.result()
     res.update(extra)
     return res, s
 

@@ -212,8 +212,12 @@ AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
  * Destination ranges must not overlap each other or any source range
  * (AQUA_ERR_DUPLICATE); ranges must fit their buffers (AQUA_ERR_CAPACITY).
  * Ordered with the pool's swaps like any call that reads the source ranges
- * and writes the destination ranges.  Uses the range-copy kernel (capped
- * like zero-copy swaps when either side is host memory). */
+ * and writes the destination ranges.  Between device and host memory each
+ * range is one copy on that direction's copy engine (see
+ * aqua_kv_pool_set_link_engine; no compute unit is used while it moves);
+ * device to device, host to host, or with the direction set to the
+ * runtime's copies, the range-copy kernel moves the bytes (capped like
+ * zero-copy swaps when either side is host memory). */
 AQUA_API aqua_status aqua_migrate(aqua_kv_pool_t pool, const void* src, uint64_t src_bytes,
                                   int32_t src_target, void* dst, uint64_t dst_bytes,
                                   int32_t dst_target, uint32_t n,

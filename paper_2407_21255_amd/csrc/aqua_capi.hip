@@ -353,29 +353,23 @@ hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipS
     return hipGetLastError();
 }
 
-// Chooses direction dir's carrier for link copies on its first staged call:
-// the requested engine, or for AQUA_LINK_AUTO the automatic engine choice,
-// falling back to the runtime's copies when the HSA runtime, the engine or
-// stream waits on signal memory are unavailable.  An explicitly requested
-// engine that cannot start is an error.
+// Chooses direction dir's carrier for link copies on its first staged call
+// or host-side migration: the requested engine, or for AQUA_LINK_AUTO the
+// automatic engine choice, falling back to the runtime's copies when the
+// HSA runtime or the engine is unavailable.  An explicitly requested engine
+// that cannot start is an error.
 aqua_status ensure_link(aqua_kv_pool* p, int dir) {
     if (p->link_used[dir] != AQUA_LINK_AUTO) return AQUA_OK;
     const int32_t req = p->link_request[dir];
     if (req != AQUA_LINK_RUNTIME) {
-        int can_wait = 0;
-        if (hipDeviceGetAttribute(&can_wait, hipDeviceAttributeCanUseStreamWaitValue,
-                                  p->device) != hipSuccess) {
-            (void)hipGetLastError();
-            can_wait = 0;
-        }
-        if (can_wait && !p->hsa_up) p->hsa_up = aqua::link_acquire(p->device, &p->agents);
+        if (!p->hsa_up) p->hsa_up = aqua::link_acquire(p->device, &p->agents);
         int32_t eng = req;
-        if (p->hsa_up && can_wait && eng == AQUA_LINK_AUTO) {
+        if (p->hsa_up && eng == AQUA_LINK_AUTO) {
             int32_t e2h = -1, h2d = -1;
             aqua::link_auto_engines(p->agents, &e2h, &h2d);
             eng = dir ? h2d : e2h;
         }
-        if (p->hsa_up && can_wait && eng >= 0 &&
+        if (p->hsa_up && eng >= 0 &&
             p->link[dir].start(p->device, p->agents, dir, eng) == hipSuccess) {
             p->link_used[dir] = eng;
             return AQUA_OK;
@@ -856,11 +850,22 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
     hipStream_t stream = (hipStream_t)stream_ptr;
     st = poll(p);
     if (st != AQUA_OK) return st;
+    // Between the HBM region and pinned host memory the ranges go to the
+    // direction's copy engine when it has one, one engine copy per range;
+    // otherwise the range-copy kernel moves them.
+    const int link_dir = (src_target == AQUA_TARGET_DEVICE && dst_target == AQUA_TARGET_HOST)   ? 0
+                         : (src_target == AQUA_TARGET_HOST && dst_target == AQUA_TARGET_DEVICE) ? 1
+                                                                                                : -1;
+    if (moved && link_dir >= 0) {
+        st = ensure_link(p, link_dir);
+        if (st != AQUA_OK) return st;
+    }
+    const bool engine = moved && link_dir >= 0 && p->link[link_dir].running();
     const uint32_t lane = lane_for(p, stream);
     const uint64_t ticket = p->next_ticket;
 
     std::vector<aqua::CopyDesc> pieces;
-    aqua::plan_copies(n, so, dof, len, kDefaultUnitBytes, &pieces);
+    if (!engine) aqua::plan_copies(n, so, dof, len, kDefaultUnitBytes, &pieces);
     p->ranges.clear();
     std::vector<std::pair<uint64_t, uint64_t>> wr;
     for (uint32_t k = 0; k < n; ++k) {
@@ -894,6 +899,18 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
         p->stats.waits_inserted++;
     }
     Outstanding rec{ticket, nullptr, {}};
+    if (engine) {
+        std::vector<aqua::LinkPiece> copies;
+        for (uint32_t k = 0; k < n; ++k)
+            if (len[k])
+                copies.push_back({(uint8_t*)dst + dof[k], (const uint8_t*)src + so[k], len[k]});
+        aqua::LinkEngine& w = p->link[link_dir];
+        int64_t* flag = nullptr;
+        const uint64_t job = w.submit(copies, &flag);
+        hipError_t e = flag ? aqua::launch_release_flags(flag, nullptr, stream) : hipSuccess;
+        if (e == hipSuccess) e = w.stream_wait(stream, job + 1);
+        if (e != hipSuccess) return latch(p, e);
+    }
     if (dbytes) {
         // Descriptors go to the device ring: a migration touching host
         // memory keeps the link busy.

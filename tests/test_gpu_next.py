@@ -140,11 +140,14 @@ def test_layer_by_layer_offload_and_reload():
         kv.close()
 
 
+@pytest.mark.parametrize("carrier", ["engine", "kernel"])
 @pytest.mark.parametrize("back", ["staged", "zero_copy"])
-def test_migration_between_hbm_and_host_then_swap_in(back):
+def test_migration_between_hbm_and_host_then_swap_in(back, carrier):
     """Reclaim: images swapped out to the HBM region move to pinned host
     memory (and one back), on other streams with no host sync; a swap-in
-    from the new place equals the oracle's."""
+    from the new place equals the oracle's.  The migrations run on the
+    copy engines, or (with the runtime's copies as the link carrier) on
+    the range-copy kernel."""
     shape = wl.KVShape(8, 2048, 8, 16, 128, wl.BF16)
     d = odesc(shape)
     case = wl.fragmented_case("mig", shape, 31, 8, 96, 4)
@@ -158,6 +161,9 @@ def test_migration_between_hbm_and_host_then_swap_in(back):
     sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     kv = aqua.KVPool(shape.as_tuple(), pool)
     kv.set_host_path(HOST_PATHS[back])
+    if carrier == "kernel":
+        for direction in (0, 1):
+            kv.set_link_engine(direction, aqua.AQUA_LINK_RUNTIME)
     try:
         # Images at offset 4096 in the region; moved to offset 8192 - 4096 + 0
         # of the host buffer as two ranges, then one image back to HBM.
@@ -182,7 +188,7 @@ def test_migration_between_hbm_and_host_then_swap_in(back):
         kv.swap_in(case.in_tables[:1], region2, [0], stream=sa)
         kv.sync()
         st = kv.stats()
-        say("migration", back, st)
+        say("migration", back, carrier, [kv.link_engine(0), kv.link_engine(1)], st)
         reg_h = np.zeros(region.numel(), dtype=np.uint8)
         hb_h = np.zeros(host_buf.numel(), dtype=np.uint8)
         r2_h = np.zeros(region2.numel(), dtype=np.uint8)
