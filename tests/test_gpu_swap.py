@@ -243,6 +243,75 @@ def test_staged_calls_back_to_back_without_host_sync(carrier, monkeypatch):
         kv.close()
 
 
+def _staged_case(seed):
+    shape = wl.KVShape(8, 1024, 4, 16, 64, wl.BF16)       # 16 KiB chunks
+    perm = wl.permutation(shape.num_blocks, seed)
+    ta = [perm[0:100], perm[100:130], perm[130:300]]
+    tb = [perm[300:400], perm[400:430], perm[430:600]]
+    owner = {b: (p, i) for p, t in enumerate(ta) for i, b in enumerate(t)}
+    return shape, ta, tb, owner
+
+
+def test_staged_pool_closed_with_calls_in_flight(monkeypatch):
+    """Closing a pool right after staged calls (no sync) waits for their
+    link copies and stops the engine threads; the bytes are complete."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    shape, ta, tb, owner = _staged_case(97)
+    d = odesc(shape)
+    pool = device_pool(shape, 33, owner)
+    pool_h = host(pool)
+    size = shape.image_bytes(300)
+    img = guarded_buffer(size, G, True)
+    want = np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8)
+    s1 = torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    kv.set_host_path(aqua.AQUA_HOST_STAGED)
+    kv.swap_out(ta, img[G:G + size], stream=s1)
+    kv.swap_in(tb, img[G:G + size], stream=s1)
+    kv.close()
+    torch.cuda.synchronize()
+    assert oracle.swap_out(d, pool_h, ta, want[G:G + size]) == 0
+    assert oracle.swap_in(d, pool_h, tb, want[G:G + size]) == 0
+    assert_bytes_equal(host(img), want, "image")
+    assert_bytes_equal(host(pool), pool_h, "pool")
+
+
+def test_link_carrier_switched_between_calls(monkeypatch):
+    """The carrier changes between staged calls (automatic engine, engine 3,
+    the runtime's copies); each switch waits for outstanding calls, and
+    every call's bytes equal the oracle's."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    shape, ta, tb, owner = _staged_case(98)
+    d = odesc(shape)
+    pool = device_pool(shape, 34, owner)
+    pool_h = host(pool)
+    size = shape.image_bytes(300)
+    imgs = [guarded_buffer(size, G, True) for _ in range(3)]
+    want = [np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8) for _ in range(3)]
+    s1 = torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    kv.set_host_path(aqua.AQUA_HOST_STAGED)
+    steps = [(aqua.AQUA_LINK_AUTO, ta, tb), (3, tb, ta), (aqua.AQUA_LINK_RUNTIME, ta, tb)]
+    try:
+        used = []
+        for k, (carrier, out_t, in_t) in enumerate(steps):
+            for direction in (0, 1):
+                kv.set_link_engine(direction, carrier)
+            kv.swap_out(out_t, imgs[k][G:G + size], stream=s1)
+            kv.swap_in(in_t, imgs[k][G:G + size], stream=s1)
+            used.append([kv.link_engine(0), kv.link_engine(1)])
+        kv.sync()
+        say("carriers used", used)
+        assert used[1] == [3, 3] and used[2] == [aqua.AQUA_LINK_RUNTIME] * 2
+        for k, (_, out_t, in_t) in enumerate(steps):
+            assert oracle.swap_out(d, pool_h, out_t, want[k][G:G + size]) == 0
+            assert oracle.swap_in(d, pool_h, in_t, want[k][G:G + size]) == 0
+            assert_bytes_equal(host(imgs[k]), want[k], f"image {k}")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+    finally:
+        kv.close()
+
+
 def test_link_engine_setter_rejects_bad_arguments():
     shape = wl.KVShape(2, 64, 1, 2, 8, wl.BF16)
     pool = device_pool(shape, 3)
