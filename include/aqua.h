@@ -246,7 +246,7 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
 /* How swaps with a pinned-host target move their bytes.
  *   AQUA_HOST_STAGED (default): the paper's temporary-tensor scheme
  *     (section 7, "Efficient context switching").  Layers pass through two
- *     HBM slots owned by the library (256 MiB each by default, allocated
+ *     HBM slots owned by the library (512 MiB each by default, allocated
  *     for both directions on the pool's first staged call, after waiting for
  *     every outstanding call, and grown the same way when a call needs
  *     larger ones): the gather kernel fills a slot and a copy engine moves it over

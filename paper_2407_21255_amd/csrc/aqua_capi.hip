@@ -24,7 +24,7 @@ using aqua::RunDesc;
 
 constexpr uint64_t kDefaultRingBytes = 4ull << 20;  // 131072 descriptors
 constexpr uint64_t kDefaultUnitBytes = 64ull << 10;
-constexpr uint64_t kDefaultSlotBytes = 256ull << 20;  // staged path, per slot
+constexpr uint64_t kDefaultSlotBytes = 512ull << 20;  // staged path, per slot
 constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 
 uint64_t env_u64(const char* name, uint64_t dflt) {
