@@ -1038,8 +1038,8 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
     {
         DeviceGuard dg(p->device);
         if (p->sticky == hipSuccess) st = wait_all(p);
-        // The link threads may still wait on the events below.
-        for (int dir = 0; dir < 2; ++dir) p->link[dir].stop();
+        // The link threads may still wait for jobs of calls that failed.
+        for (int dir = 0; dir < 2; ++dir) p->link[dir].stop(p->sticky != hipSuccess);
         if (p->hsa_up) aqua::link_release();
         p->hsa_up = false;
         for (auto& q : p->outstanding)

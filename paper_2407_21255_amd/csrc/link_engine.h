@@ -87,8 +87,10 @@ class LinkEngine {
 
     // dir 0: device memory to pinned host memory; 1: the reverse.
     hipError_t start(int device, const LinkAgents& a, int dir, int32_t engine);
-    // Waits for every submitted job, then ends the thread.
-    void stop();
+    // Waits for every submitted job, then ends the thread.  With `abandon`
+    // (after a failure), jobs whose ready flag was never released are
+    // given up at once instead of after the job time limit.
+    void stop(bool abandon = false);
 
     // Queues the copies of the next job on the engine, to run once the
     // job's ready flag is released (launch_release_flags).  Returns the job's
@@ -132,6 +134,7 @@ class LinkEngine {
     std::vector<hsa_signal_t> spare_ready_, all_;
     bool stop_ = false;
     std::atomic<bool> stopping_{false};
+    std::atomic<bool> abandon_{false};
     std::atomic<int32_t> err_{0};
     std::thread th_;
 };

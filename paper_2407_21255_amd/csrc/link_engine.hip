@@ -145,8 +145,9 @@ hipError_t LinkEngine::start(int device, const LinkAgents& a, int dir, int32_t e
     return hipSuccess;
 }
 
-void LinkEngine::stop() {
+void LinkEngine::stop(bool abandon) {
     if (!th_.joinable()) return;
+    abandon_.store(abandon, std::memory_order_release);
     {
         std::lock_guard<std::mutex> lk(mu_);
         stop_ = true;
@@ -155,6 +156,7 @@ void LinkEngine::stop() {
     cv_.notify_all();
     th_.join();
     stopping_.store(false);
+    abandon_.store(false);
     for (hsa_signal_t sg : all_) hsa_signal_destroy(sg);
     all_.clear();
     spare_ready_.clear();
@@ -297,8 +299,13 @@ void LinkEngine::loop() {
                 if (!released && stopping_.load(std::memory_order_acquire)) {
                     // Stopping: a flag not released by now may never be (a
                     // call that failed before launching its release), so
-                    // the time limit runs from here as well.
+                    // the time limit runs from here as well; a stop after a
+                    // failure abandons such jobs at once.
                     released = hsa_signal_load_relaxed(job.ready) == 0;
+                    if (!released && abandon_.load(std::memory_order_acquire)) {
+                        recycle = false;
+                        break;
+                    }
                     if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
                         fail(hipErrorLaunchTimeOut);
                         recycle = false;
