@@ -15,6 +15,7 @@ of 16 fragmented 2048-token prompts preempted to an HBM offload region.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -26,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, read + write combined
+HIP_MEMCPY_D2D_NO_CU = 1024  # hipMemcpyDeviceToDeviceNoCU: a copy engine, no compute units
 HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 --pmc
@@ -237,16 +239,42 @@ def run_pair(args, res_common):
     if pinned:
         _configure_host(kv, args.host_path)
     evs = []
+    two_step = args.two_step if not pinned else None
+    if two_step:
+        # The paper's scheme as an ablation: gather into a temporary HBM
+        # tensor, then one bulk copy into the offload region, and the reverse
+        # on swap-in.  The bulk copy is the runtime's own device-to-device
+        # copy, on its blit kernel or (NoCU) on a copy engine.
+        temp = torch.empty(payload, dtype=torch.uint8, device="cuda")
+        hip = ctypes.CDLL("libamdhip64.so.7")
+        hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_int, ctypes.c_void_p]
+
+        def bulk(dst_t, src_t):
+            if two_step == "blit":
+                with torch.cuda.stream(stream):
+                    dst_t.copy_(src_t)
+            else:
+                assert hip.hipMemcpyAsync(dst_t.data_ptr(), src_t.data_ptr(), payload,
+                                          HIP_MEMCPY_D2D_NO_CU, stream.cuda_stream) == 0
 
     def step(i, timed):
         src, dst = (tab_a, tab_b) if i % 2 == 0 else (tab_b, tab_a)
         if timed:
             e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
             e0.record(stream)
-        kv.swap_out(src, img, stream=stream)
+        if two_step:
+            kv.swap_out(src, temp, stream=stream)
+            bulk(img, temp)
+        else:
+            kv.swap_out(src, img, stream=stream)
         if timed:
             e1.record(stream)
-        kv.swap_in(dst, img, stream=stream)
+        if two_step:
+            bulk(temp, img)
+            kv.swap_in(dst, temp, stream=stream)
+        else:
+            kv.swap_in(dst, img, stream=stream)
         if timed:
             e2.record(stream)
             evs.append((e0, e1, e2))
@@ -286,6 +314,9 @@ def run_pair(args, res_common):
         ("scatter (swap-in)", in_ms)
     if pinned:
         bound, peak, alg = "host_link", HOST_LINK_PEAK_GBS, payload
+    elif two_step:
+        # Gather and bulk copy each read and write the payload once.
+        bound, peak, alg = "hbm", HBM_PEAK_GBS, 4 * payload
     else:
         bound, peak, alg = "hbm", HBM_PEAK_GBS, 2 * payload
     achieved = alg / (dom_ms.mean() * 1e-3) / 1e9
@@ -304,13 +335,15 @@ def run_pair(args, res_common):
             "offload_target": "pinned_host" if pinned else "hbm",
             "host_path": args.host_path if pinned else None,
             "link_carrier": carrier,
+            "two_step": two_step,
             "parallelism": "single_gpu",
         },
         "roofline": {
             "bound": bound, "kernel": dom,
             "achieved": round(achieved, 1), "peak": peak,
             "unit": "GB/s", "frac": round(achieved / peak, 4),
-            "traffic": MEASURED_TRAFFIC.get((args.workload, khash), {}).get(dom),
+            "traffic": (None if two_step else
+                        MEASURED_TRAFFIC.get((args.workload, khash), {}).get(dom)),
             "algorithmic_bytes_per_launch": alg,
         },
         "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
@@ -727,6 +760,10 @@ def main():
                          "link (the zero-copy target these workloads are defined with), or "
                          "HBM staging plus link copies on a copy engine (the library's "
                          "default, which leaves the compute units to other streams)")
+    ap.add_argument("--two-step", choices=["blit", "sdma"], default=None,
+                    help="HBM-target pair workloads: the paper's two-step scheme as an ablation "
+                         "(gather into a temporary HBM tensor, then one runtime device-to-device "
+                         "copy on its blit kernel or on a copy engine)")
     ap.add_argument("--link-engine", default="auto",
                     help="staged path: carrier of the link copies, 'auto', 'runtime' (the HIP "
                          "runtime's copies) or an SDMA engine index 0..15")
