@@ -214,7 +214,7 @@ AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
  * Ordered with the pool's swaps like any call that reads the source ranges
  * and writes the destination ranges.  Between device and host memory each
  * range is one copy on that direction's copy engine (see
- * aqua_kv_pool_set_link_engine; no compute unit is used while it moves);
+ * aqua_kv_pool_set_link_engine; no compute unit copies the bytes);
  * device to device, host to host, or with the direction set to the
  * runtime's copies, the range-copy kernel moves the bytes (capped like
  * zero-copy swaps when either side is host memory). */
@@ -271,7 +271,14 @@ AQUA_API aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t pool, int32_t pat
  * swap-out, device to host; dir 1: swap-in, host to device).
  *   0..15               that SDMA engine, driven through the HSA runtime by
  *                       a library thread; the call's stream waits for the
- *                       engine's progress on the device, with no host block.
+ *                       engine's progress on the device, with no host block
+ *                       (hipStreamWaitValue64).  Set GPU_STREAMOPS_CP_WAIT=1
+ *                       in the environment before the HIP runtime starts so
+ *                       that the runtime holds such waits in the command
+ *                       processor; otherwise it keeps a one-wave kernel
+ *                       resident per wait, which slows kernels that fill
+ *                       every compute unit (the Python package sets it when
+ *                       imported).
  *                       A staged call fails with AQUA_ERR_HIP (nothing
  *                       enqueued) if the engine cannot be used.
  *   AQUA_LINK_RUNTIME   the HIP runtime's own copies on a library stream; the

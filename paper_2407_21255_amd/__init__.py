@@ -7,6 +7,17 @@ Modules:
   workload  seeded synthetic inputs (pools, block tables, schedules).
   build     in-tree build of libaqua.so (hipcc, gfx950) and the host core.
 
-Importing the package loads nothing native; ``aqua.load()`` does, and fails
-loudly if the library has not been built.
+Importing the package loads nothing native (it only sets one HIP runtime
+option, below); ``aqua.load()`` does, and fails loudly if the library has
+not been built.
 """
+import os as _os
+
+# The staged host path and host-side migrations make streams wait for the
+# copy engines (hipStreamWaitValue64).  With this runtime setting the command
+# processor holds such a stream; without it the runtime keeps a one-wave
+# kernel resident for the wait, which slows kernels that fill every compute
+# unit once.  It takes effect only if set before the HIP runtime starts, so
+# it is set when the package is imported, unless the environment says
+# otherwise.
+_os.environ.setdefault("GPU_STREAMOPS_CP_WAIT", "1")

@@ -409,4 +409,18 @@ uint64_t RangeAllocator::granted(uint64_t off) const {
     return u == used_.end() ? 0 : u->second;
 }
 
+void pick_link_engines(uint32_t d2h_avail, uint32_t d2h_pref, uint32_t h2d_avail,
+                       uint32_t h2d_pref, uint32_t fast, int32_t* d2h, int32_t* h2d) {
+    auto lowest = [](uint32_t m) { return m ? (int32_t)__builtin_ctz(m) : -1; };
+    auto candidates = [&](uint32_t avail, uint32_t pref) -> uint32_t {
+        if (pref & avail) return pref & avail;
+        const uint32_t f = fast ? fast : avail;
+        return (f & avail) ? (f & avail) : f;
+    };
+    *d2h = lowest(candidates(d2h_avail, d2h_pref));
+    const uint32_t m1 = candidates(h2d_avail, h2d_pref);
+    const uint32_t m1x = *d2h >= 0 ? (m1 & ~(1u << *d2h)) : m1;
+    *h2d = lowest(m1x ? m1x : m1);
+}
+
 }  // namespace aqua

@@ -190,6 +190,17 @@ private:
 // space's device region and its host region).  Every range starts on an
 // `align` boundary and is a multiple of it; freeing coalesces neighbours.
 // Host bookkeeping only: whoever reuses a freed range orders the reuse.
+// Copy engines for the two link directions from the runtime's masks (bit e:
+// engine e).  Per direction the candidates are the runtime's preferred
+// engines that are available; else the `fast` engines (those that carry the
+// host link at its rate) that are available; else the `fast` engines, shared
+// with their other users, rather than a slower free one.  The lowest-numbered
+// candidate is taken, the host-to-device direction on a different engine from
+// the device-to-host one where its candidates allow.  With `fast` empty the
+// available engines stand in for it.  -1 for a direction with no candidate.
+void pick_link_engines(uint32_t d2h_avail, uint32_t d2h_pref, uint32_t h2d_avail,
+                       uint32_t h2d_pref, uint32_t fast, int32_t* d2h, int32_t* h2d);
+
 class RangeAllocator {
 public:
     void reset(uint64_t size, uint64_t align);

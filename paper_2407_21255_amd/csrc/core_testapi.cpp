@@ -176,6 +176,11 @@ uint64_t aqua_core_tracker_live_ranges(void* t) {
     return static_cast<aqua::HazardTracker*>(t)->live_ranges();
 }
 
+void aqua_core_pick_link_engines(uint32_t d2h_avail, uint32_t d2h_pref, uint32_t h2d_avail,
+                                 uint32_t h2d_pref, uint32_t fast, int32_t* d2h, int32_t* h2d) {
+    aqua::pick_link_engines(d2h_avail, d2h_pref, h2d_avail, h2d_pref, fast, d2h, h2d);
+}
+
 void* aqua_core_ranges_new(uint64_t size, uint64_t align) {
     auto* r = new aqua::RangeAllocator();
     r->reset(size, align);

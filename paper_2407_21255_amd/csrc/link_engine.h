@@ -12,12 +12,21 @@
 // to wait for the job's ready flag; a one-lane kernel on the call's stream
 // releases the flag once the slot may be read or overwritten.  A library
 // thread waits for the jobs' completions in order and publishes the number
-// of completed jobs.  A stream that needs copies done is held by a host
-// function (hipLaunchHostFunc) that returns once the count is reached: the
-// command processor holds the stream, and no wave stays resident.  (A wave
-// waiting on a compute unit, even asleep, makes a full-chip kernel such as a
-// 256-tile GEMM run a second round of tiles; the runtime's own stream wait
-// on memory is such a kernel.)
+// of completed jobs in signal memory; a stream that needs copies done waits
+// on that count (hipStreamWaitValue64).
+//
+// Why this is deadlock-free: a job's release is enqueued when the job is
+// submitted, and a stream wait only ever waits for jobs submitted before it,
+// so every wait depends only on work enqueued before it, in any queue.  (A
+// host function holding the stream would not do: the runtime runs host
+// functions one at a time on one thread, so a held stream could keep another
+// stream from reaching the release of a job queued ahead on the engine.)
+//
+// The runtime holds a stream waiting on memory in the command processor when
+// GPU_STREAMOPS_CP_WAIT=1 is set before it starts; otherwise with a one-wave
+// kernel, which is correct but keeps a compute unit partly occupied, enough
+// to make a kernel that fills every compute unit once (a 256-tile GEMM) run a
+// second round of tiles.
 //
 // The engine runs its queue in order.  Everything in it, this library's
 // copies and any other user's, was queued after the work it depends on, so
@@ -29,11 +38,9 @@
 #include <hsa/hsa.h>
 
 #include <atomic>
-#include <chrono>
 #include <condition_variable>
 #include <cstdint>
 #include <deque>
-#include <memory>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -53,24 +60,15 @@ void link_release();
 
 // Engines for the two directions when the caller names none: the HSA
 // runtime's preferred engine for the direction if it names one, else the
-// lowest-numbered available engine, the two directions on different engines
-// where possible.  -1 where no engine is available.
+// lowest-numbered free engine among those that carry the host link at its
+// rate, else one of those shared with its other users; the two directions on
+// different engines where possible (pick_link_engines).
 void link_auto_engines(const LinkAgents& a, int32_t* d2h, int32_t* h2d);
 
 // Enqueues one lane that stores 0, with system-scope release ordering, to
 // each non-null flag (a job's ready flag from LinkEngine::submit): the
 // stores are ordered after everything enqueued on `stream` before it.
 hipError_t launch_release_flags(int64_t* a, int64_t* b, hipStream_t stream);
-
-// Completed-job count of a LinkEngine.
-struct LinkProgress {
-    std::mutex mu;
-    std::condition_variable cv;
-    uint64_t completed = 0;
-    std::atomic<bool> gave_up{false};  // a wait hit its time limit
-    // Blocks until `completed` >= count; false (and gave_up set) after `limit`.
-    bool wait_for(uint64_t count, std::chrono::seconds limit);
-};
 
 struct LinkPiece {
     void* dst;
@@ -98,8 +96,7 @@ class LinkEngine {
     // On failure the job still counts as submitted and is published, with
     // the error kept for error().
     uint64_t submit(const std::vector<LinkPiece>& pieces, int64_t** flag);
-    // Makes `stream` wait until `count` jobs have completed (a host function
-    // that gives up after the job time limit; error() reports it).
+    // Makes `stream` wait until `count` jobs have completed.
     hipError_t stream_wait(hipStream_t stream, uint64_t count);
 
     // First failure (hipSuccess if none).  A failed job is still published,
@@ -122,9 +119,8 @@ class LinkEngine {
     int device_ = 0;
     int32_t engine_ = -1;
     hsa_agent_t dst_agent_{}, src_agent_{};
-    // Shared with the host functions holding streams, which may run after
-    // the engine has stopped.
-    std::shared_ptr<LinkProgress> progress_;
+    void* count_ = nullptr;  // signal memory: the completed-job count
+    volatile uint64_t* count_host_ = nullptr;
     uint64_t issued_ = 0;    // jobs submitted (caller's thread)
     std::mutex mu_;
     std::condition_variable cv_;

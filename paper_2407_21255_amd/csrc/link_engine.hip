@@ -2,9 +2,10 @@
 // HIP streams through a completed-job count in signal memory.
 #include "link_engine.h"
 
+#include "aqua_core.h"
+
 #include <hsa/hsa_ext_amd.h>
 
-#include <new>
 
 #include <chrono>
 
@@ -49,13 +50,15 @@ hsa_status_t first_cpu(hsa_agent_t a, void* data) {
     return HSA_STATUS_SUCCESS;
 }
 
-int32_t lowest_bit(uint32_t m) { return m ? (int32_t)__builtin_ctz(m) : -1; }
-
 // A job's copies take milliseconds once its ready flag is released; a job
 // not complete this long after the release is taken as failed.  (Before the
 // release the job waits for earlier work on the call's stream, for as long
 // as that takes.)
 constexpr auto kJobTimeLimit = std::chrono::seconds(60);
+// Engines that carry the host link at its rate on MI355X: engines 0-3 move
+// 55.6-56.0 GB/s each way in staged swaps; engines 4-15 move 7-13 GB/s device
+// to host and 28-50 GB/s host to device.
+constexpr uint32_t kHostLinkEngines = 0xF;
 // Wait slices, in HSA timestamp ticks (nanoseconds to 10 ns each).
 constexpr uint64_t kWaitHint = 10000000ull;
 // Start value of an engine's completion signal, which every copy decrements.
@@ -119,11 +122,7 @@ void link_auto_engines(const LinkAgents& a, int32_t* d2h, int32_t* h2d) {
         pref[0] = 0;
     if (hsa_amd_memory_get_preferred_copy_engine(a.gpu, a.cpu, &pref[1]) != HSA_STATUS_SUCCESS)
         pref[1] = 0;
-    const uint32_t m0 = (pref[0] & av[0]) ? (pref[0] & av[0]) : av[0];
-    *d2h = lowest_bit(m0);
-    const uint32_t m1 = (pref[1] & av[1]) ? (pref[1] & av[1]) : av[1];
-    const uint32_t m1x = *d2h >= 0 ? (m1 & ~(1u << *d2h)) : m1;
-    *h2d = lowest_bit(m1x ? m1x : m1);
+    pick_link_engines(av[0], pref[0], av[1], pref[1], kHostLinkEngines, d2h, h2d);
 }
 
 hipError_t LinkEngine::start(int device, const LinkAgents& a, int dir, int32_t engine) {
@@ -132,9 +131,22 @@ hipError_t LinkEngine::start(int device, const LinkAgents& a, int dir, int32_t e
     engine_ = engine;
     dst_agent_ = dir == 0 ? a.cpu : a.gpu;
     src_agent_ = dir == 0 ? a.gpu : a.cpu;
-    progress_ = std::make_shared<LinkProgress>();
+    hipError_t e = hipExtMallocWithFlags(&count_, sizeof(uint64_t), hipMallocSignalMemory);
+    hipPointerAttribute_t attr{};
+    if (e == hipSuccess) e = hipPointerGetAttributes(&attr, count_);
+    if (e != hipSuccess || !attr.hostPointer) {
+        (void)hipGetLastError();
+        if (count_) (void)hipFree(count_);
+        count_ = nullptr;
+        return e != hipSuccess ? e : hipErrorInvalidValue;
+    }
+    count_host_ = static_cast<volatile uint64_t*>(attr.hostPointer);
+    __atomic_store_n(count_host_, 0ull, __ATOMIC_RELEASE);
     if (hsa_signal_create(kDoneBase, 0, nullptr, &done_) != HSA_STATUS_SUCCESS) {
         done_.handle = 0;
+        (void)hipFree(count_);
+        count_ = nullptr;
+        count_host_ = nullptr;
         return hipErrorOutOfMemory;
     }
     queued_ = 0;
@@ -162,7 +174,9 @@ void LinkEngine::stop(bool abandon) {
     spare_ready_.clear();
     if (done_.handle) hsa_signal_destroy(done_);
     done_.handle = 0;
-    progress_.reset();
+    (void)hipFree(count_);
+    count_ = nullptr;
+    count_host_ = nullptr;
 }
 
 bool LinkEngine::take_ready(hsa_signal_t* ready) {
@@ -220,49 +234,12 @@ uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag
     return index;
 }
 
-bool LinkProgress::wait_for(uint64_t count, std::chrono::seconds limit) {
-    std::unique_lock<std::mutex> lk(mu);
-    if (cv.wait_for(lk, limit, [&] { return completed >= count; })) return true;
-    gave_up.store(true, std::memory_order_release);
-    return false;
-}
-
-namespace {
-
-struct HoldArgs {
-    std::shared_ptr<LinkProgress> progress;  // alive while the function is pending
-    uint64_t count;
-};
-
-// Runs on the runtime's callback thread when the stream reaches it; the
-// stream's later work waits until it returns.  Makes no HIP call.
-void hold_stream(void* arg) {
-    HoldArgs* a = static_cast<HoldArgs*>(arg);
-    (void)a->progress->wait_for(a->count, kJobTimeLimit);
-    delete a;
-}
-
-}  // namespace
-
 hipError_t LinkEngine::stream_wait(hipStream_t stream, uint64_t count) {
-    {
-        std::lock_guard<std::mutex> lk(progress_->mu);
-        if (progress_->completed >= count) return hipSuccess;  // nothing to wait for
-    }
-    HoldArgs* a = new (std::nothrow) HoldArgs{progress_, count};
-    if (!a) return hipErrorOutOfMemory;
-    const hipError_t e = hipLaunchHostFunc(stream, hold_stream, a);
-    if (e != hipSuccess) delete a;
-    return e;
+    if (__atomic_load_n(count_host_, __ATOMIC_ACQUIRE) >= count) return hipSuccess;
+    return hipStreamWaitValue64(stream, count_, count, hipStreamWaitValueGte, ~0ull);
 }
 
-hipError_t LinkEngine::error() const {
-    const int32_t e = err_.load(std::memory_order_acquire);
-    if (e) return (hipError_t)e;
-    if (progress_ && progress_->gave_up.load(std::memory_order_acquire))
-        return hipErrorLaunchTimeOut;
-    return hipSuccess;
-}
+hipError_t LinkEngine::error() const { return (hipError_t)err_.load(std::memory_order_acquire); }
 
 void LinkEngine::fail(hipError_t e) {
     int32_t none = 0;
@@ -270,11 +247,7 @@ void LinkEngine::fail(hipError_t e) {
 }
 
 void LinkEngine::publish(uint64_t completed) {
-    {
-        std::lock_guard<std::mutex> lk(progress_->mu);
-        progress_->completed = completed;
-    }
-    progress_->cv.notify_all();
+    __atomic_store_n(count_host_, completed, __ATOMIC_RELEASE);
 }
 
 void LinkEngine::loop() {

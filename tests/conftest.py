@@ -5,6 +5,10 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# Imported before any test touches the GPU: the package sets a HIP runtime
+# option that must be in place before the runtime starts.
+import paper_2407_21255_amd  # noqa: E402,F401
+
 
 def pytest_configure(config):
     config.addinivalue_line(

@@ -312,6 +312,44 @@ def test_link_carrier_switched_between_calls(monkeypatch):
         kv.close()
 
 
+def test_two_pools_share_the_copy_engines(monkeypatch):
+    """Two pools stage to pinned host memory at the same time, each on its
+    own stream and both on the automatic engines: each pool's threads queue
+    on the same engines, and each pool's bytes equal the oracle's."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    runs = []
+    for seed in (61, 62):
+        shape, ta, tb, owner = _staged_case(seed)
+        pool = device_pool(shape, seed, owner)
+        size = shape.image_bytes(300)
+        runs.append(dict(shape=shape, ta=ta, tb=tb, pool=pool, pool_h=host(pool), size=size,
+                         img=guarded_buffer(size, G, True), stream=torch.cuda.Stream(),
+                         kv=aqua.KVPool(shape.as_tuple(), pool)))
+    try:
+        for r in runs:
+            r["kv"].set_host_path(aqua.AQUA_HOST_STAGED)
+        for kind in ("out", "in"):
+            for r in runs:
+                inner = r["img"][G:G + r["size"]]
+                if kind == "out":
+                    r["kv"].swap_out(r["ta"], inner, stream=r["stream"])
+                else:
+                    r["kv"].swap_in(r["tb"], inner, stream=r["stream"])
+        for r in runs:
+            r["kv"].sync()
+        say("two pools", [[r["kv"].link_engine(0), r["kv"].link_engine(1)] for r in runs])
+        for k, r in enumerate(runs):
+            d = odesc(r["shape"])
+            want = np.full(r["size"] + 2 * G, wl.GUARD_BYTE, dtype=np.uint8)
+            assert oracle.swap_out(d, r["pool_h"], r["ta"], want[G:G + r["size"]]) == 0
+            assert oracle.swap_in(d, r["pool_h"], r["tb"], want[G:G + r["size"]]) == 0
+            assert_bytes_equal(host(r["img"]), want, f"pool {k} image")
+            assert_bytes_equal(host(r["pool"]), r["pool_h"], f"pool {k}")
+    finally:
+        for r in runs:
+            r["kv"].close()
+
+
 def test_link_engine_setter_rejects_bad_arguments():
     shape = wl.KVShape(2, 64, 1, 2, 8, wl.BF16)
     pool = device_pool(shape, 3)
