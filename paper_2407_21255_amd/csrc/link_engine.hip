@@ -6,7 +6,6 @@
 
 #include <hsa/hsa_ext_amd.h>
 
-
 #include <chrono>
 
 namespace aqua {
@@ -275,7 +274,11 @@ void LinkEngine::loop() {
                     // the time limit runs from here as well; a stop after a
                     // failure abandons such jobs at once.
                     released = hsa_signal_load_relaxed(job.ready) == 0;
-                    if (!released && abandon_.load(std::memory_order_acquire)) {
+                    if (released) {
+                        t0 = std::chrono::steady_clock::now();
+                        continue;
+                    }
+                    if (abandon_.load(std::memory_order_acquire)) {
                         recycle = false;
                         break;
                     }
