@@ -156,6 +156,52 @@ def test_preemption_cycle_full():
         torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("path", ["staged", "zero_copy"])
+def test_preemption_cycle_pinned_host(path):
+    """The preemption cycle with the offload region in pinned host memory
+    (17.7 GB): every slice swaps 16 prompts out on one stream and 16 in on
+    another, both directions of the link at once (staged: one copy engine
+    per direction), then the host mutates the residents and the consumed
+    slots.  Pool and region must equal the oracle's replay."""
+    n = int(os.environ.get("AQUA_TEST_HOST_SLICES", "6"))
+    sched = wl.preemption_schedule(n_slices=n)
+    s = sched.shape
+    t0 = time.time()
+    pool = device_pool(s, sched.seed, schedule_owner(sched))
+    region = torch.empty(sched.region_bytes, dtype=torch.uint8, pin_memory=True)
+    staging = region_for(sched)
+    region.copy_(staging)
+    del staging
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    pool_h = host(pool)
+    region_h = region.numpy().copy()
+    say("host cycle inputs ready", path, round(time.time() - t0, 1), "s")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    kv.set_host_path({"staged": aqua.AQUA_HOST_STAGED,
+                      "zero_copy": aqua.AQUA_HOST_ZERO_COPY}[path])
+    try:
+        prepared = [slice_tables(sched, k) for k in range(n)]
+        run_slices(kv, region, sched, 0, n, sa, sb,
+                   between=lambda k: apply_mutations_device(sched, k, pool, region),
+                   prepared=prepared)
+        torch.cuda.synchronize()
+        st = kv.stats()
+        say("host cycle on GPU done", path, round(time.time() - t0, 1), "s",
+            [kv.link_engine(0), kv.link_engine(1)], st)
+        oracle_replay(sched, pool_h, region_h, 0, n)
+        say("oracle replay done", round(time.time() - t0, 1), "s")
+        assert_bytes_equal(region.numpy(), region_h, "pinned offload region")
+        del region_h
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["calls_out"] == n and st["calls_in"] == n and st["hip_error"] == 0
+    finally:
+        kv.close()
+        del pool, region
+        torch.cuda.empty_cache()
+
+
 def test_preemption_cycle_without_host_syncs():
     """The same schedule issued slice after slice with no host
     synchronisation (no mutations in between): blocks that one slice frees
