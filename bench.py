@@ -372,8 +372,9 @@ def run_pair(args, res_common):
 
 
 def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
-    """GB/s of the copy engines over the host link: plain 1 GiB copies between
-    pinned host memory and the device (hipMemcpyAsync), each direction."""
+    """GB/s of the runtime's copies over the host link: plain 1 GiB copies
+    between pinned host memory and the device (hipMemcpyAsync), each
+    direction alone, then both at once (total)."""
     import torch
     h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
     d = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -391,6 +392,20 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
         e1.record()
         torch.cuda.synchronize()
         out[name] = round(nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 2)
+    # Both directions at once, on two streams: the link's rate when it is
+    # busy both ways.
+    h2 = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d2 = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        with torch.cuda.stream(s1):
+            h.copy_(d, non_blocking=True)
+        with torch.cuda.stream(s2):
+            d2.copy_(h2, non_blocking=True)
+    torch.cuda.synchronize()
+    out["both_total"] = round(2 * nbytes * reps / (time.perf_counter() - t0) / 1e9, 2)
     return out
 
 
@@ -546,7 +561,10 @@ def run_cycle(args, res_common):
         "offload_target": "pinned_host" if on_host else "hbm",
         "host_path": args.host_path if on_host else None, "parallelism": "single_gpu",
     }
-    return _slice_result(res_common, s, *timed, args.steps, config, host=on_host), s
+    res = _slice_result(res_common, s, *timed, args.steps, config, host=on_host)
+    if on_host:
+        res["link_ceiling"] = link_ceiling()
+    return res, s
 
 
 def run_cfs(args, res_common):
