@@ -74,6 +74,7 @@ WORKLOADS = {
     "prefix_host": "the same prefix cache held in pinned host memory",
     "layered": "Llama-3-70B-shaped KV, one 32768-token prompt swapped in from an HBM region "
                "in 10 layer groups of 8, one ticket each",
+    "layered_host": "the same layer-group swap-in from pinned host memory",
     "migrate": "Llama-3-70B-shaped KV: the 10 GiB image of one 32768-token prompt migrated "
                "from the HBM region to pinned host memory and back",
     "cfs": "fair scheduling (least-served first, rescheduled every 16 iterations or on a "
@@ -634,7 +635,7 @@ def run_next(args, res_common):
         n = m = len(prompt)
     pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
     wl.fill_pool(pool, s, 6, owner)
-    pinned = w == "prefix_host"
+    pinned = w in ("prefix_host", "layered_host")
     nbytes = s.image_bytes(n)
     img = (torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) if pinned
            else torch.empty(nbytes, dtype=torch.uint8, device="cuda"))
@@ -661,7 +662,7 @@ def run_next(args, res_common):
             kv.migrate(back, img, [0], [0], [nbytes], stream=stream)
             e2.record(stream)
             timed_evs.append((e0, e1, e2))
-    elif w == "layered":
+    elif w.startswith("layered"):
         groups = [(l0, 8) for l0 in range(0, s.num_layers, 8)]
         moved = nbytes
         def step(timed_evs):
@@ -717,12 +718,15 @@ def run_next(args, res_common):
                  "hbm_to_host_GBps": round(nbytes / d2h / 1e6, 2),
                  "host_to_hbm_GBps": round(nbytes / h2d / 1e6, 2)}
         bound, peak, dom_ms, alg = "host_link", HOST_LINK_PEAK_GBS, max(d2h, h2d), nbytes
-    elif w == "layered":
+    elif w.startswith("layered"):
         first = np.mean([e[0].elapsed_time(e[1]) for e in evs])
         total = np.mean([e[0].elapsed_time(e[-1]) for e in evs])
         extra = {"first_group_ms": round(float(first), 3), "all_groups_ms": round(float(total), 3),
                  "groups": 10, "layers_per_group": 8}
-        bound, peak, dom_ms, alg = "hbm", HBM_PEAK_GBS, total / 10, 2 * nbytes / 10
+        if pinned:
+            bound, peak, dom_ms, alg = "host_link", HOST_LINK_PEAK_GBS, total / 10, nbytes / 10
+        else:
+            bound, peak, dom_ms, alg = "hbm", HBM_PEAK_GBS, total / 10, 2 * nbytes / 10
     else:
         ms = np.mean([a.elapsed_time(b) for a, b in evs])
         extra = {"prefix_tokens": m * s.block_tokens, "cached_tokens": 100000,
@@ -814,7 +818,7 @@ def main():
         res, shape = run_cycle(args, common)
     elif args.workload == "cfs":
         res, shape = run_cfs(args, common)
-    elif args.workload in ("prefix", "prefix_host", "layered", "migrate"):
+    elif args.workload in ("prefix", "prefix_host", "layered", "layered_host", "migrate"):
         res, shape = run_next(args, common)
     else:
         res, shape = run_pair(args, common)
