@@ -68,6 +68,65 @@ def test_prefix_swap_in_from_cached_image(where):
 
 
 @pytest.mark.parametrize("where", ["hbm", "staged"])
+def test_prefix_swap_in_beside_other_traffic(where):
+    """Prefix loads at a 10 % rate while other swaps continue: a cached
+    700-block image is swapped back in (prefixes of 684, 1 and 333 blocks)
+    into the same fresh blocks every tenth iteration, on its own stream,
+    while two other prompts swap out and back in, between two block sets, on
+    two more streams, with no host sync.  Pool and images equal the oracle's
+    replay in issue order."""
+    shape = wl.KVShape(8, 2048, 4, 16, 64, wl.BF16)     # 16 KiB chunks
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 57)
+    n = 700
+    prompt, fresh = perm[:n], perm[n:2 * n]
+    bg_a = [perm[1400 + 100 * k:1500 + 100 * k] for k in range(2)]
+    bg_b = [perm[1600 + 100 * k:1700 + 100 * k] for k in range(2)]
+    owner = {b: (0, i) for i, b in enumerate(prompt)}
+    owner.update({b: (1 + k, i) for k, t in enumerate(bg_a) for i, b in enumerate(t)})
+    pool = device_pool(shape, 23, owner)
+    pool_h = host(pool)
+    img_p = _buf(shape.image_bytes(n), where)
+    img_bg = _buf(shape.image_bytes(200), where)
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    if HOST_PATHS[where] is not None:
+        kv.set_host_path(HOST_PATHS[where])
+    try:
+        kv.swap_out([prompt], img_p, stream=sc)
+        calls = []
+        m_of = {0: n - 16, 10: 1, 20: 333}
+        for i in range(30):
+            if i in m_of:
+                m = m_of[i]
+                kv.swap_in([fresh[:m]], img_p, img_blocks=[n], stream=sc)
+                calls.append(("prefix", m))
+            src, dst = (bg_a, bg_b) if i % 2 == 0 else (bg_b, bg_a)
+            kv.swap_out(src, img_bg, stream=sa)
+            kv.swap_in(dst, img_bg, stream=sb)
+            calls.append(("bg", i))
+        kv.sync()
+        st = kv.stats()
+        say("prefix beside traffic", where, st["waits_inserted"], st["calls_in"])
+        img_p_h = np.zeros(img_p.numel(), dtype=np.uint8)
+        img_bg_h = np.zeros(img_bg.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [prompt], img_p_h) == 0
+        for kind, x in calls:
+            if kind == "prefix":
+                assert oracle.swap_in_ex(d, pool_h, [fresh[:x]], img_p_h, None, [n]) == 0
+            else:
+                src, dst = (bg_a, bg_b) if x % 2 == 0 else (bg_b, bg_a)
+                assert oracle.swap_out(d, pool_h, src, img_bg_h) == 0
+                assert oracle.swap_in(d, pool_h, dst, img_bg_h) == 0
+        assert_bytes_equal(host(img_p), img_p_h, "cached prefix image")
+        assert_bytes_equal(host(img_bg), img_bg_h, "background image")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert st["waits_inserted"] > 0
+    finally:
+        kv.close()
+
+
+@pytest.mark.parametrize("where", ["hbm", "staged"])
 def test_layer_groups_pipelined_swap_in(where):
     """Swap-in issued as one call per layer group; a consumer stream waits
     on each group's ticket and snapshots that group's layers, which must
