@@ -72,6 +72,9 @@ WORKLOADS = {
               "region; each step swaps its prefix (all but the last 256 tokens) back in "
               "from the cached image",
     "prefix_host": "the same prefix cache held in pinned host memory",
+    "prefix_mixed": "the same prefix loaded (from HBM) once per ten iterations of other swap "
+                    "traffic on the same pool: two prompts of 448 blocks swapped out and back "
+                    "into another block set each iteration, on two more streams",
     "layered": "Llama-3-70B-shaped KV, one 32768-token prompt swapped in from an HBM region "
                "in 10 layer groups of 8, one ticket each",
     "layered_host": "the same layer-group swap-in from pinned host memory",
@@ -662,6 +665,33 @@ def run_next(args, res_common):
             kv.migrate(back, img, [0], [0], [nbytes], stream=stream)
             e2.record(stream)
             timed_evs.append((e0, e1, e2))
+    elif w == "prefix_mixed":
+        # Background swaps on blocks the prefix loads do not touch.
+        bg_a = [perm[0:448], perm[448:896]]
+        bg_b = [perm[896:1344], perm[1344:1792]]
+        bg_bytes = s.image_bytes(896)
+        img_bg = torch.empty(bg_bytes, dtype=torch.uint8, device="cuda")
+        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        ta, tb = aqua._csr(bg_a), aqua._csr(bg_b)
+        moved = s.image_bytes(m) + 20 * bg_bytes
+
+        def prefix_load():
+            e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
+            e0.record(stream)
+            kv.swap_in(tf, img, stream=stream, img_blocks=[n])
+            e1.record(stream)
+            return e0, e1
+
+        def step(timed_evs):
+            p0, p1 = prefix_load()
+            b0, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
+            b0.record(sa)
+            for j in range(10):
+                src, dst = (ta, tb) if j % 2 == 0 else (tb, ta)
+                kv.swap_out(src, img_bg, stream=sa)
+                kv.swap_in(dst, img_bg, stream=sb)
+            b1.record(sb)
+            timed_evs.append((p0, p1, b0, b1))
     elif w.startswith("layered"):
         groups = [(l0, 8) for l0 in range(0, s.num_layers, 8)]
         moved = nbytes
@@ -696,6 +726,12 @@ def run_next(args, res_common):
     torch.cuda.synchronize()
     n_warm = max(args.warmup, 2) if args.gemm else args.warmup
     step_s = (time.perf_counter() - tw) / (n_warm - 1) if tw is not None else 0.0
+    if w == "prefix_mixed":
+        # The same prefix load with nothing else running, for comparison.
+        alone = [prefix_load() for _ in range(3)]
+        kv.sync(0)
+        torch.cuda.synchronize()
+        alone_ms = float(np.mean([a.elapsed_time(b) for a, b in alone]))
     comp = GemmCompanion(step_s, args.steps) if args.gemm else None
     evs = []
     st0 = kv.stats()
@@ -718,6 +754,15 @@ def run_next(args, res_common):
                  "hbm_to_host_GBps": round(nbytes / d2h / 1e6, 2),
                  "host_to_hbm_GBps": round(nbytes / h2d / 1e6, 2)}
         bound, peak, dom_ms, alg = "host_link", HOST_LINK_PEAK_GBS, max(d2h, h2d), nbytes
+    elif w == "prefix_mixed":
+        beside = float(np.mean([a.elapsed_time(b) for a, b, _, _ in evs]))
+        bg_ms = float(np.mean([c.elapsed_time(d) for _, _, c, d in evs]))
+        extra = {"prefix_tokens": m * s.block_tokens, "cached_tokens": 100000,
+                 "prefix_alone_ms": round(alone_ms, 3),
+                 "prefix_beside_traffic_ms": round(beside, 3),
+                 "background_ms_per_10_iterations": round(bg_ms, 3),
+                 "background_GBps": round(20 * bg_bytes / bg_ms / 1e6, 1)}
+        bound, peak, dom_ms, alg = "hbm", HBM_PEAK_GBS, wall * 1e3 / args.steps, 2 * moved
     elif w.startswith("layered"):
         first = np.mean([e[0].elapsed_time(e[1]) for e in evs])
         total = np.mean([e[0].elapsed_time(e[-1]) for e in evs])
@@ -818,7 +863,8 @@ def main():
         res, shape = run_cycle(args, common)
     elif args.workload == "cfs":
         res, shape = run_cfs(args, common)
-    elif args.workload in ("prefix", "prefix_host", "layered", "layered_host", "migrate"):
+    elif args.workload in ("prefix", "prefix_host", "prefix_mixed", "layered", "layered_host",
+                           "migrate"):
         res, shape = run_next(args, common)
     else:
         res, shape = run_pair(args, common)
