@@ -80,6 +80,11 @@ WORKLOADS = {
     "layered_host": "the same layer-group swap-in from pinned host memory",
     "migrate": "Llama-3-70B-shaped KV: the 10 GiB image of one 32768-token prompt migrated "
                "from the HBM region to pinned host memory and back",
+    "elastic": "the first 30 reschedules of the fair-scheduling burst with every prompt's "
+               "image in its own swap-space tensor (58 prompts, 25.3 GB): reschedules 0-19 "
+               "with the tensors in the device region, then the region reclaimed (tensors "
+               "moved to pinned host memory), reschedules 20-24 over the host link, the "
+               "region restored, reschedules 25-29",
     "cfs": "fair scheduling (least-served first, rescheduled every 16 iterations or on a "
            "completion) of a 192-request burst on a Llama-3-8B-shaped bf16 pool (16384 "
            "blocks, 2x oversubscribed): each reschedule swaps the prompts leaving the batch "
@@ -571,6 +576,94 @@ def run_cycle(args, res_common):
     return res, s
 
 
+def run_elastic(args, res_common):
+    """Reclaim and restore of a swap space in the middle of a fair-scheduling
+    run: per-phase reschedule times and the link rate of the moves."""
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import aqua, cfs
+    from paper_2407_21255_amd import workload as wl
+    from paper_2407_21255_amd.cycle import run_slices_in_space
+
+    cfg = wl.CFS_LLAMA8B
+    s = cfg.shape
+    tr = cfg.trace()
+    log, _ = cfs.run_trace(tr, s.num_blocks, s.block_tokens, cfg.batch_tokens,
+                           cfg.decode_slots(tr), cfg.k)
+    sched = wl.cfs_swap_schedule(s, cfg.seed, tr, log)
+    n1, n2, n3 = 20, 25, 30
+    prompts = sorted({p for sl in sched.slices[:n3] for p in sl.out_prompts + sl.in_prompts})
+    sizes = {p: s.image_bytes(sched.nblocks[p]) for p in prompts}
+    room = sum((b + 255) // 256 * 256 for b in sizes.values())
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, cfg.seed)
+    torch.cuda.synchronize()
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    _configure_host(kv, "staged")
+    space = aqua.SwapSpace(kv, room, room)
+    tensors = {p: space.alloc(sizes[p]) for p in prompts}
+    assert space.usage()["host_tensors"] == 0
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+
+    def payload(a, b):
+        return sum(s.image_bytes(len(t)) for sl in sched.slices[a:b]
+                   for t in sl.out_tables + sl.in_tables)
+
+    def phase(a, b):
+        per = []
+        for k in range(a, b):
+            t0 = time.perf_counter()
+            run_slices_in_space(kv, space, tensors, sched, k, 1, sa, sb)
+            per.append(time.perf_counter() - t0)
+        moved = payload(a, b)
+        return {"reschedules": [a, b], "ms_per_reschedule": round(float(np.mean(per)) * 1e3, 3),
+                "payload_bytes": moved, "GBps": round(moved / sum(per) / 1e9, 2)}
+
+    def move(fn):
+        before = space.usage()
+        t0 = time.perf_counter()
+        fn(stream=sc)
+        kv.sync(0)
+        dt = time.perf_counter() - t0
+        after = space.usage()
+        moved = abs(after["device_free"] - before["device_free"])
+        return {"bytes": moved, "ms": round(dt * 1e3, 3), "GBps": round(moved / dt / 1e9, 2),
+                "tensors_moved": abs(after["host_tensors"] - before["host_tensors"])}
+
+    wall0 = time.perf_counter()
+    ph = [phase(0, n1)]
+    rec = move(space.reclaim)
+    ph.append(phase(n1, n2))
+    res_ = move(space.restore)
+    ph.append(phase(n2, n3))
+    wall = time.perf_counter() - wall0
+    carrier = [kv.link_engine(0), kv.link_engine(1)]
+    space.close()
+    kv.close()
+    moved = sum(p["payload_bytes"] for p in ph) + rec["bytes"] + res_["bytes"]
+    res = dict(res_common)
+    res.update({
+        "value": round(moved / wall / 1e9, 2),
+        "ms_per_step": round(wall * 1e3 / n3, 4),
+        "dtype": wl.DTYPE_NAME[s.dtype],
+        "config": {"workload": WORKLOADS["elastic"], "layers": s.num_layers,
+                   "kv_heads": s.num_kv_heads, "head_dim": s.head_dim,
+                   "block_tokens": s.block_tokens, "pool_blocks": s.num_blocks,
+                   "chunk_bytes": s.chunk_bytes, "prompts": len(prompts),
+                   "swap_space_bytes": room, "link_carrier": carrier,
+                   "parallelism": "single_gpu"},
+        "phases": {"device_region": ph[0], "host_after_reclaim": ph[1],
+                   "device_after_restore": ph[2]},
+        "reclaim": rec, "restore": res_,
+        "roofline": {"bound": "host_link", "kernel": "reclaim (engine copies to host)",
+                     "achieved": rec["GBps"], "peak": HOST_LINK_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(rec["GBps"] / HOST_LINK_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": rec["bytes"]},
+    })
+    return res, s
+
+
 def run_cfs(args, res_common):
     """Fair scheduling of a burst on the 8B-shaped pool: the rescheduler's
     page-outs and page-ins, slice by slice, for the slices that swap."""
@@ -863,6 +956,8 @@ def main():
         res, shape = run_cycle(args, common)
     elif args.workload == "cfs":
         res, shape = run_cfs(args, common)
+    elif args.workload == "elastic":
+        res, shape = run_elastic(args, common)
     elif args.workload in ("prefix", "prefix_host", "prefix_mixed", "layered", "layered_host",
                            "migrate"):
         res, shape = run_next(args, common)
