@@ -48,7 +48,12 @@
  * AQUA_ERR_HIP and every later swap call returns AQUA_ERR_STATE.
  *
  * Threads: a pool handle is used from one thread at a time.  Separate pools
- * are independent (but do not order against each other).
+ * are independent (but do not order against each other).  A pool whose
+ * host-link copies run on an SDMA engine (aqua_kv_pool_set_link_engine)
+ * owns one library thread per direction in use, started on the first call
+ * that needs it and joined by aqua_kv_pool_destroy; it only waits for the
+ * engine's copies and publishes their completion, and calls back into no
+ * caller code.
  */
 #ifndef AQUA_H
 #define AQUA_H
