@@ -644,6 +644,8 @@ def run_elastic(args, res_common):
     moved = sum(p["payload_bytes"] for p in ph) + rec["bytes"] + res_["bytes"]
     res = dict(res_common)
     res.update({
+        # a fixed sequence: 30 reschedules, a reclaim and a restore, no warm-up
+        "steps": n3, "warmup": 0,
         "value": round(moved / wall / 1e9, 2),
         "ms_per_step": round(wall * 1e3 / n3, 4),
         "dtype": wl.DTYPE_NAME[s.dtype],
