@@ -44,8 +44,11 @@
  *
  * Errors: argument errors are found before anything is enqueued, so a
  * failing call has no side effect and issues no ticket.  A HIP runtime
- * failure after enqueueing is latched on the pool: aqua_sync returns
- * AQUA_ERR_HIP and every later swap call returns AQUA_ERR_STATE.
+ * failure after enqueueing is latched on the pool: the failing call returns
+ * AQUA_ERR_HIP once the work it had enqueued has ended (its destination
+ * bytes are then undefined), aqua_sync returns AQUA_ERR_HIP and every later
+ * swap call returns AQUA_ERR_STATE.  Copy-engine work of the failed call is
+ * never left waiting on the engine, whose queue other pools may share.
  *
  * Threads: a pool handle is used from one thread at a time.  Separate pools
  * are independent (but do not order against each other).  A pool whose

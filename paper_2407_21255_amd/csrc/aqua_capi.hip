@@ -97,6 +97,11 @@ struct aqua_kv_pool {
     uint8_t* staging[2] = {nullptr, nullptr};
     uint64_t staging_bytes[2] = {0, 0};
     uint64_t slot_target = kDefaultSlotBytes;
+    // Launches of the kernel that releases engine jobs, and the one (from 0)
+    // to report as failed without making it (AQUA_FAIL_RELEASE_AT: tests of
+    // the failure path force it from the host, every kernel still ending).
+    uint64_t releases = 0;
+    uint64_t fail_release_at = ~0ull;
     std::vector<StagedSeq> sseq;
     std::vector<uint64_t> slot_offsets;  // per sequence, in a slot
 
@@ -152,6 +157,34 @@ aqua_status latch(aqua_kv_pool* p, hipError_t e) {
         p->stats.hip_error = (int32_t)e;
     }
     return AQUA_ERR_HIP;
+}
+
+// A call that fails after enqueueing work returns once that work has ended
+// (or the device has failed), so that nothing it enqueued outlives the error
+// it reports.
+aqua_status fail_enqueued(hipStream_t stream, aqua_status st) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipGetLastError();
+    return st;
+}
+
+// Enqueues the release of up to two engine jobs' ready flags on `stream`.
+hipError_t release_flags(aqua_kv_pool* p, int64_t* a, int64_t* b, hipStream_t stream) {
+    if (!a) std::swap(a, b);
+    if (!a) return hipSuccess;
+    if (p->releases++ == p->fail_release_at) return hipErrorLaunchFailure;
+    return aqua::launch_release_flags(a, b, stream);
+}
+
+// After a failure between submitting engine jobs and enqueueing their
+// release: once the stream's earlier work has ended, the held flags are
+// released from the host, so that the engine's queue drains.
+aqua_status fail_held(aqua_kv_pool* p, aqua::LinkEngine& w, hipStream_t stream,
+                      int64_t* const* held, int n, hipError_t e) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipGetLastError();
+    for (int i = 0; i < n; ++i) w.release_on_host(held[i]);
+    return latch(p, e);
 }
 
 uint32_t lane_for(aqua_kv_pool* p, hipStream_t s) {
@@ -581,10 +614,8 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
         (void)hipGetLastError();
         return aqua::launch_swap(slot_launch(p, is_in, s, descs, ndesc, l0, nl), stream);
     };
-    auto release = [&](int64_t* a, int64_t* b) -> hipError_t {
-        if (!a) std::swap(a, b);
-        return a ? aqua::launch_release_flags(a, b, stream) : hipSuccess;
-    };
+    // A flag is held from its job's submission until its release kernel is
+    // enqueued; a failure in between hands it to fail_held.
     hipError_t e = hipSuccess;
     if (!is_in) {
         uint64_t first = 0, job = 0;
@@ -595,22 +626,24 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
             int64_t* flag = nullptr;
             job = submit(k, &flag);
             if (k == 0) first = job;
-            if ((e = release(flag, nullptr)) != hipSuccess) return latch(p, e);
+            if ((e = release_flags(p, flag, nullptr, stream)) != hipSuccess)
+                return fail_held(p, w, stream, &flag, 1, e);
         }
         if ((e = w.stream_wait(stream, job + 1)) != hipSuccess) return latch(p, e);
     } else {
-        int64_t* f0 = nullptr;
-        int64_t* f1 = nullptr;
-        const uint64_t first = submit(0, &f0);
-        if (K > 1) (void)submit(1, &f1);
-        if ((e = release(f0, f1)) != hipSuccess) return latch(p, e);
+        int64_t* held[2] = {nullptr, nullptr};
+        const uint64_t first = submit(0, &held[0]);
+        if (K > 1) (void)submit(1, &held[1]);
+        if ((e = release_flags(p, held[0], held[1], stream)) != hipSuccess)
+            return fail_held(p, w, stream, held, 2, e);
         for (uint32_t k = 0; k < K; ++k) {
             if ((e = w.stream_wait(stream, first + k + 1)) != hipSuccess) return latch(p, e);
             if ((e = kernel(k)) != hipSuccess) return latch(p, e);
             if (k + 2 < K) {
                 int64_t* flag = nullptr;
                 (void)submit(k + 2, &flag);
-                if ((e = release(flag, nullptr)) != hipSuccess) return latch(p, e);
+                if ((e = release_flags(p, flag, nullptr, stream)) != hipSuccess)
+                    return fail_held(p, w, stream, &flag, 1, e);
             }
         }
     }
@@ -757,7 +790,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         hipEvent_t ev = event_of(p, d.ticket);
         if (!ev) continue;
         const hipError_t e = hipStreamWaitEvent(stream, ev, 0);
-        if (e != hipSuccess) return latch(p, e);
+        if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         p->stats.waits_inserted++;
     }
 
@@ -770,12 +803,12 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
             descs = p->ring_dev + ring_off;
             e = upload_descs(p, ring_off, dbytes, stream);
         }
-        if (e != hipSuccess) return latch(p, e);
+        if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         if (staged) {
             st = enqueue_staged(p, is_in, buf, stream, reinterpret_cast<const RunDesc*>(descs),
                                 (uint32_t)p->plan.size(), slot, G, l_begin, l_begin + l_count,
                                 &rec);
-            if (st != AQUA_OK) return st;
+            if (st != AQUA_OK) return fail_enqueued(stream, st);
         } else {
             aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
@@ -784,13 +817,13 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
             L.num_layers = l_count;
             (void)hipGetLastError();
             e = aqua::launch_swap(L, stream);
-            if (e != hipSuccess) return latch(p, e);
+            if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         }
     }
 
     hipError_t e = take_event(p, &rec.ev);
     if (e == hipSuccess) e = hipEventRecord(rec.ev, stream);
-    if (e != hipSuccess) return latch(p, e);
+    if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
     p->outstanding[lane].push_back(std::move(rec));
     if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
 
@@ -895,7 +928,7 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
         hipEvent_t ev = event_of(p, d.ticket);
         if (!ev) continue;
         const hipError_t e = hipStreamWaitEvent(stream, ev, 0);
-        if (e != hipSuccess) return latch(p, e);
+        if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         p->stats.waits_inserted++;
     }
     Outstanding rec{ticket, nullptr, {}};
@@ -907,16 +940,17 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
         aqua::LinkEngine& w = p->link[link_dir];
         int64_t* flag = nullptr;
         const uint64_t job = w.submit(copies, &flag);
-        hipError_t e = flag ? aqua::launch_release_flags(flag, nullptr, stream) : hipSuccess;
-        if (e == hipSuccess) e = w.stream_wait(stream, job + 1);
-        if (e != hipSuccess) return latch(p, e);
+        hipError_t e = release_flags(p, flag, nullptr, stream);
+        if (e != hipSuccess) return fail_held(p, w, stream, &flag, 1, e);
+        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess)
+            return fail_enqueued(stream, latch(p, e));
     }
     if (dbytes) {
         // Descriptors go to the device ring: a migration touching host
         // memory keeps the link busy.
         std::memcpy(p->ring_host + ring_off, pieces.data(), dbytes);
         hipError_t e = upload_descs(p, ring_off, dbytes, stream);
-        if (e != hipSuccess) return latch(p, e);
+        if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         const bool host_side = src_target == AQUA_TARGET_HOST || dst_target == AQUA_TARGET_HOST;
         (void)hipGetLastError();
         e = aqua::launch_copy(dsrc, ddst,
@@ -924,11 +958,11 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
                               (uint32_t)pieces.size(),
                               host_side ? p->max_wg[AQUA_TARGET_HOST] : p->max_wg[AQUA_TARGET_DEVICE],
                               stream);
-        if (e != hipSuccess) return latch(p, e);
+        if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
     }
     hipError_t e = take_event(p, &rec.ev);
     if (e == hipSuccess) e = hipEventRecord(rec.ev, stream);
-    if (e != hipSuccess) return latch(p, e);
+    if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
     p->outstanding[lane].push_back(std::move(rec));
     if (dbytes) p->ring_uses.push_back({ring_off, ring_off + ((dbytes + 255) & ~255ull), ticket});
     p->stats.calls_migrate++;
@@ -1023,6 +1057,7 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     if (!p->unit_bytes) p->unit_bytes = kDefaultUnitBytes;
     if (p->unit_bytes > aqua::kMaxChunkBytes) p->unit_bytes = aqua::kMaxChunkBytes;
     p->slot_target = env_u64("AQUA_STAGE_SLOT_BYTES", kDefaultSlotBytes);
+    p->fail_release_at = env_u64("AQUA_FAIL_RELEASE_AT", ~0ull);
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
     if (st != AQUA_OK) {
         delete p;
@@ -1038,7 +1073,16 @@ aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
     {
         DeviceGuard dg(p->device);
         if (p->sticky == hipSuccess) st = wait_all(p);
-        // The link threads may still wait for jobs of calls that failed.
+        if (p->sticky != hipSuccess) {
+            // Calls issued before the failure may still run: let them end
+            // before their slots, rings and events are freed.  (The failed
+            // call itself waited for its own work before returning.)
+            for (auto& q : p->outstanding)
+                for (const Outstanding& o : q) (void)hipEventSynchronize(o.ev);
+            (void)hipGetLastError();
+        }
+        // After a failure a link thread may find a job whose flag is still
+        // held; it releases it from the host so that the engine drains.
         for (int dir = 0; dir < 2; ++dir) p->link[dir].stop(p->sticky != hipSuccess);
         if (p->hsa_up) aqua::link_release();
         p->hsa_up = false;

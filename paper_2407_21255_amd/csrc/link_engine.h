@@ -86,8 +86,11 @@ class LinkEngine {
     // dir 0: device memory to pinned host memory; 1: the reverse.
     hipError_t start(int device, const LinkAgents& a, int dir, int32_t engine);
     // Waits for every submitted job, then ends the thread.  With `abandon`
-    // (after a failure), jobs whose ready flag was never released are
-    // given up at once instead of after the job time limit.
+    // (after a failure), a job whose ready flag is still held is released
+    // from the host, so that its copies and every copy queued behind them
+    // on the engine still run.  If a job stays incomplete past the job time
+    // limit, the engine may still wait on or write this object's signals:
+    // they stay allocated for the life of the process.
     void stop(bool abandon = false);
 
     // Queues the copies of the next job on the engine, to run once the
@@ -96,6 +99,12 @@ class LinkEngine {
     // On failure the job still counts as submitted and is published, with
     // the error kept for error().
     uint64_t submit(const std::vector<LinkPiece>& pieces, int64_t** flag);
+    // Releases from the host the ready flag of a submitted job whose
+    // release kernel was never enqueued (its call failed first), so that the
+    // engine's queue, which every later copy on the engine shares, does not
+    // hold a copy that waits forever.  The caller first waits for the work
+    // that the job's copies were to follow.
+    void release_on_host(int64_t* flag);
     // Makes `stream` wait until `count` jobs have completed.
     hipError_t stream_wait(hipStream_t stream, uint64_t count);
 
@@ -110,6 +119,7 @@ class LinkEngine {
         uint64_t index;
         uint64_t end;        // copies queued on the engine up to and including this job
         hsa_signal_t ready;  // the copies' dependency, released by a kernel
+        int64_t* flag;       // the address of ready's value, as handed out
     };
     void loop();
     void fail(hipError_t e);
@@ -132,6 +142,7 @@ class LinkEngine {
     std::atomic<bool> stopping_{false};
     std::atomic<bool> abandon_{false};
     std::atomic<int32_t> err_{0};
+    bool stuck_ = false;     // a job timed out (loop thread; read after join)
     std::thread th_;
 };
 

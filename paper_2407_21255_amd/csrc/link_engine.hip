@@ -168,6 +168,17 @@ void LinkEngine::stop(bool abandon) {
     th_.join();
     stopping_.store(false);
     abandon_.store(false);
+    if (stuck_) {
+        // The engine may still wait on a ready flag or decrement done_, and a
+        // stream wait may still read the count: keep them all allocated.
+        stuck_ = false;
+        all_.clear();
+        spare_ready_.clear();
+        done_.handle = 0;
+        count_ = nullptr;
+        count_host_ = nullptr;
+        return;
+    }
     for (hsa_signal_t sg : all_) hsa_signal_destroy(sg);
     all_.clear();
     spare_ready_.clear();
@@ -197,7 +208,7 @@ bool LinkEngine::take_ready(hsa_signal_t* ready) {
 uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag) {
     *flag = nullptr;
     const uint64_t index = issued_++;
-    Job job{index, queued_, {0}};
+    Job job{index, queued_, {0}, nullptr};
     volatile hsa_signal_value_t* value = nullptr;
     if (err_.load(std::memory_order_acquire) == 0) {
         if (!take_ready(&job.ready)) {
@@ -223,7 +234,8 @@ uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag
         job.end = queued_;
         // Copies already queued wait for the flag, so it is handed out even
         // when some failed to queue.
-        *flag = const_cast<int64_t*>(value);
+        job.flag = const_cast<int64_t*>(value);
+        *flag = job.flag;
     }
     {
         std::lock_guard<std::mutex> lk(mu_);
@@ -231,6 +243,17 @@ uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag
     }
     cv_.notify_one();
     return index;
+}
+
+void LinkEngine::release_on_host(int64_t* flag) {
+    if (!flag) return;
+    // A held job cannot have completed, so it is still queued here.
+    std::lock_guard<std::mutex> lk(mu_);
+    for (const Job& j : q_)
+        if (j.flag == flag) {
+            hsa_signal_store_screlease(j.ready, 0);
+            return;
+        }
 }
 
 hipError_t LinkEngine::stream_wait(hipStream_t stream, uint64_t count) {
@@ -262,41 +285,45 @@ void LinkEngine::loop() {
         // done_ once: the job is complete when done_ has dropped by the
         // number of copies queued up to and including it.
         const hsa_signal_value_t target = kDoneBase - (hsa_signal_value_t)job.end;
-        bool recycle = job.ready.handle != 0;
-        if (job.ready.handle) {
-            auto t0 = std::chrono::steady_clock::now();
-            bool released = false;
+        // Behind a job that timed out, the engine completes nothing more:
+        // later jobs are published failed at once.
+        bool recycle = job.ready.handle != 0 && !stuck_;
+        if (recycle) {
+            // The time limit runs from the flag's release, or from the stop
+            // for a flag still held then; before either, the job waits for
+            // earlier work on its call's stream for as long as that takes.
+            auto since = std::chrono::steady_clock::now();
+            bool released = false, timed = false;
             while (hsa_signal_wait_scacquire(done_, HSA_SIGNAL_CONDITION_LT, target + 1,
                                              kWaitHint, HSA_WAIT_STATE_BLOCKED) > target) {
-                if (!released && stopping_.load(std::memory_order_acquire)) {
-                    // Stopping: a flag not released by now may never be (a
-                    // call that failed before launching its release), so
-                    // the time limit runs from here as well; a stop after a
-                    // failure abandons such jobs at once.
+                const auto now = std::chrono::steady_clock::now();
+                if (!released) {
                     released = hsa_signal_load_relaxed(job.ready) == 0;
+                    if (!released && stopping_.load(std::memory_order_acquire)) {
+                        if (abandon_.load(std::memory_order_acquire)) {
+                            // The pool failed: its release kernel may never run.
+                            hsa_signal_store_screlease(job.ready, 0);
+                            released = true;
+                        } else if (!timed) {
+                            timed = true;
+                            since = now;
+                        }
+                    }
                     if (released) {
-                        t0 = std::chrono::steady_clock::now();
+                        since = now;
                         continue;
                     }
-                    if (abandon_.load(std::memory_order_acquire)) {
-                        recycle = false;
-                        break;
-                    }
-                    if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
-                        fail(hipErrorLaunchTimeOut);
-                        recycle = false;
-                        break;
-                    }
-                } else if (!released) {
-                    released = hsa_signal_load_relaxed(job.ready) == 0;
-                    t0 = std::chrono::steady_clock::now();
-                } else if (std::chrono::steady_clock::now() - t0 > kJobTimeLimit) {
-                    // The engine may still wait on this flag: never reuse it.
+                    if (!timed) continue;
+                }
+                if (now - since > kJobTimeLimit) {
                     fail(hipErrorLaunchTimeOut);
+                    stuck_ = true;
                     recycle = false;
                     break;
                 }
             }
+        } else if (job.ready.handle) {
+            fail(hipErrorLaunchTimeOut);
         }
         publish(job.index + 1);
         std::lock_guard<std::mutex> lk(mu_);

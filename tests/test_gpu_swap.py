@@ -2,6 +2,8 @@
 byte, through the C ABI.  Every input comes from the seeded generator; every
 expected value from the oracle run on a host copy of the same input."""
 
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -348,6 +350,79 @@ def test_two_pools_share_the_copy_engines(monkeypatch):
     finally:
         for r in runs:
             r["kv"].close()
+
+
+@pytest.mark.parametrize("kind,fail_at", [("out", 3), ("in", 0), ("in", 3), ("migrate", 0)])
+def test_failed_release_leaves_the_shared_engine_usable(monkeypatch, kind, fail_at):
+    """A call that fails after queueing a job on a copy engine but before
+    enqueueing the kernel that releases it (forced from the host with
+    AQUA_FAIL_RELEASE_AT; every kernel still runs to its end) returns
+    AQUA_ERR_HIP once its own work has ended, and the job still drains: a
+    second pool on the same engine then moves its bytes as the oracle does,
+    and the failed pool refuses further calls and closes promptly."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(1 << 20))
+    engine = 3
+    shape, ta, tb, owner = _staged_case(71)
+    size = shape.image_bytes(300)
+    pool_a = device_pool(shape, 71, owner)
+    monkeypatch.setenv("AQUA_FAIL_RELEASE_AT", str(fail_at))
+    kva = aqua.KVPool(shape.as_tuple(), pool_a)
+    monkeypatch.delenv("AQUA_FAIL_RELEASE_AT")
+    pool_b = device_pool(shape, 72, owner)
+    pool_bh = host(pool_b)
+    kvb = aqua.KVPool(shape.as_tuple(), pool_b)
+    img_a = torch.zeros(size, dtype=torch.uint8, pin_memory=True)
+    img_b = guarded_buffer(size, G, True)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    closed_a = False
+    try:
+        for kv in (kva, kvb):
+            kv.set_host_path(aqua.AQUA_HOST_STAGED)
+            kv.set_link_engine(0, engine)
+            kv.set_link_engine(1, engine)
+        say("forced release failure", kind, fail_at, "engine", engine)
+        with pytest.raises(aqua.AquaError) as ei:
+            if kind == "out":
+                kva.swap_out(ta, img_a, stream=sa)
+            elif kind == "in":
+                kva.swap_in(tb, img_a, stream=sa)
+            else:
+                region = torch.zeros(size, dtype=torch.uint8, device="cuda")
+                kva.migrate(region, img_a, [0], [0], [size], stream=sa)
+        assert ei.value.status == aqua.AQUA_ERR_HIP
+        assert kva.stats()["hip_error"] != 0
+        with pytest.raises(aqua.AquaError) as ei:
+            kva.swap_out(ta, img_a, stream=sa)
+        assert ei.value.status == aqua.AQUA_ERR_STATE
+
+        # The second pool queues behind the failed call's jobs on the engine.
+        t0 = time.perf_counter()
+        inner = img_b[G:G + size]
+        kvb.swap_out(ta, inner, stream=sb)
+        kvb.swap_in(tb, inner, stream=sb)
+        kvb.sync()
+        say("second pool done in", round(time.perf_counter() - t0, 3), "s")
+        assert [kvb.link_engine(0), kvb.link_engine(1)] == [engine, engine]
+        d = odesc(shape)
+        want = np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8)
+        assert oracle.swap_out(d, pool_bh, ta, want[G:G + size]) == 0
+        assert oracle.swap_in(d, pool_bh, tb, want[G:G + size]) == 0
+        assert_bytes_equal(host(img_b), want, "second pool image")
+        assert_bytes_equal(host(pool_b), pool_bh, "second pool")
+
+        t0 = time.perf_counter()
+        closed_a = True
+        with pytest.raises(aqua.AquaError) as ei:
+            kva.close()
+        assert ei.value.status == aqua.AQUA_ERR_HIP
+        assert time.perf_counter() - t0 < 10.0
+    finally:
+        if not closed_a:
+            try:
+                kva.close()
+            except aqua.AquaError:
+                pass
+        kvb.close()
 
 
 def test_link_engine_setter_rejects_bad_arguments():
