@@ -4,6 +4,8 @@
 * ``libaqua_core.so``  -- the host core alone, with test entry points, built
                           by the system C++ compiler so that CPU-only tests
                           can drive validation, planning and hazard tracking.
+* ``tests/c_abi_client`` -- a plain C program (gcc) that uses ``libaqua.so``
+                          through ``include/aqua.h`` alone; a GPU test runs it.
 
 Run ``python -m paper_2407_21255_amd.build``.
 """
@@ -18,6 +20,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 HIP_LIB = os.path.join(PKG, "libaqua.so")
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c_abi_client.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c_abi_client")
 CORE_LIB = os.path.join(PKG, "libaqua_core.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -64,9 +68,21 @@ def build_core(out: str = CORE_LIB) -> str:
     return out
 
 
+def build_c_client(out: str = C_CLIENT) -> str:
+    """C11, the HIP runtime's C API and libaqua.so: nothing else."""
+    tmp = out + ".tmp"
+    _run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+          "-I", INCLUDE, "-I/opt/rocm/include", C_CLIENT_SRC, "-o", tmp,
+          "-L", PKG, "-laqua", "-L/opt/rocm/lib", "-lamdhip64",
+          "-Wl,-rpath,$ORIGIN/../paper_2407_21255_amd", "-Wl,-rpath,/opt/rocm/lib"])
+    os.replace(tmp, out)
+    return out
+
+
 def build_all() -> None:
     build_core()
     build_hip()
+    build_c_client()
 
 
 if __name__ == "__main__":
@@ -77,3 +93,5 @@ if __name__ == "__main__":
         build_core()
     if "hip" in what:
         build_hip()
+    if "client" in what:
+        build_c_client()

@@ -66,3 +66,18 @@ def test_null_handles_are_rejected_without_a_gpu():
     assert lib.aqua_sync(None, 0) == -1
     lib.aqua_kv_pool_create.restype = ctypes.c_int32
     assert lib.aqua_kv_pool_create(None, None, ctypes.c_uint64(0), None) == -1
+
+
+def test_c_client_links_the_library_and_the_hip_runtime_only():
+    """The C program that a GPU test runs uses the boundary with no Python
+    or torch: its dynamic dependencies name neither."""
+    import subprocess
+    client = os.path.join(ROOT, "tests", "c_abi_client")
+    if not os.path.exists(client):
+        from paper_2407_21255_amd import build
+        if not os.path.exists(LIB):
+            build.build_hip()
+        build.build_c_client()
+    out = subprocess.run(["ldd", client], capture_output=True, text=True, check=True).stdout
+    assert "libaqua.so" in out and "libamdhip64" in out
+    assert "python" not in out and "torch" not in out
