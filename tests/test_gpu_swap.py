@@ -97,11 +97,13 @@ def test_tiny_config_round_trip():
 
 
 RAGGED = [
-    # (L, N, H, T, D, dtype): 48-byte chunks, 8 KiB chunks, 32 KiB fp8, 64 KiB.
+    # (L, N, H, T, D, dtype): 48-byte chunks, 8 KiB chunks, 32 KiB fp8, 64 KiB, and 1 MiB
+    # chunks that the plan splits into 16 units of 64 KiB each.
     wl.KVShape(3, 300, 1, 3, 8, wl.FP8_E4M3),
     wl.KVShape(2, 64, 2, 16, 64, wl.BF16),
     wl.KVShape(2, 96, 8, 16, 128, wl.FP8_E4M3),
     wl.KVShape(3, 64, 8, 16, 128, wl.F16),
+    wl.KVShape(2, 48, 32, 32, 256, wl.F16),
 ]
 
 
