@@ -377,6 +377,17 @@ class KVPool:
             raise AquaError(st, "aqua_kv_pool_create")
         self.handle = h
         self._spaces = []      # swap spaces on this pool, closed before it
+        self._held = {}        # ticket -> the tensors its call names, until it completes
+
+    def _hold(self, ticket: int, *tensors) -> None:
+        """Keeps the tensors that a call reads or writes alive until the call
+        completes: the library only borrows their memory, and a tensor freed
+        early could be handed out again while a kernel or a copy engine still
+        uses it."""
+        done = [t for t in self._held if aqua_query(self.handle, t) == 1]
+        for t in done:
+            del self._held[t]
+        self._held[ticket] = tensors
 
     def _swap(self, is_in, tables, buf, img_offsets, stream, target, img_blocks, layers):
         ids, offs = _csr(tables)
@@ -399,6 +410,7 @@ class KVPool:
             st, ticket = fn(*args, ctypes.byref(rng), tgt, _stream_handle(stream))
         if st != AQUA_OK:
             raise AquaError(st, name)
+        self._hold(ticket, buf)
         return ticket
 
     def swap_out(self, tables, dst: torch.Tensor, img_offsets=None, stream=None,
@@ -423,12 +435,17 @@ class KVPool:
                                   _stream_handle(stream))
         if st != AQUA_OK:
             raise AquaError(st, "aqua_migrate")
+        self._hold(ticket, src, dst)
         return ticket
 
     def sync(self, ticket: int = 0) -> None:
         st = aqua_sync(self.handle, ticket)
         if st != AQUA_OK:
             raise AquaError(st, "aqua_sync")
+        if ticket == 0:
+            self._held.clear()
+        else:
+            self._held.pop(ticket, None)
 
     def stream_wait(self, ticket: int, stream=None) -> None:
         st = aqua_stream_wait(self.handle, ticket, _stream_handle(stream))
@@ -477,6 +494,7 @@ class KVPool:
         if getattr(self, "handle", None):
             st = aqua_kv_pool_destroy(self.handle)
             self.handle = None
+            self._held.clear()   # destroy waited for every call
             if st != AQUA_OK:
                 raise AquaError(st, "aqua_kv_pool_destroy")
 

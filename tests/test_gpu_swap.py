@@ -578,3 +578,31 @@ def test_stream_wait_orders_caller_work():
         assert kv.query(t)
     finally:
         kv.close()
+
+
+def test_binding_keeps_call_buffers_alive_until_complete():
+    """The binding holds the tensors a call names until the library reports
+    the call complete, so that a caller may drop a temporary buffer right
+    after the call; the hold ends with the call."""
+    import gc
+    import weakref
+
+    shape = wl.KVShape(2, 64, 2, 16, 64, wl.BF16)
+    pool = device_pool(shape, 5)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    s = torch.cuda.Stream()
+    try:
+        with torch.cuda.stream(s):
+            torch.cuda._sleep(200_000_000)            # a bounded spin: the call stays pending
+        buf = torch.empty(shape.image_bytes(8), dtype=torch.uint8, device="cuda")
+        ref = weakref.ref(buf)
+        t = kv.swap_out([list(range(8))], buf, stream=s)
+        assert not kv.query(t)
+        del buf
+        gc.collect()
+        assert ref() is not None
+        kv.sync(t)
+        gc.collect()
+        assert ref() is None
+    finally:
+        kv.close()
