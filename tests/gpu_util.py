@@ -2,7 +2,9 @@
 copies for the oracle, and the oracle's replay of a preemption schedule."""
 from __future__ import annotations
 
+import ctypes
 import sys
+import threading
 
 import numpy as np
 import torch
@@ -105,3 +107,68 @@ def oracle_replay(sched, pool_np, region_np, first, count, mutate=True, grow=Tru
             apply_mutations_host(sched, s, pool_np, region_np)
         elif mutate:
             apply_pool_mutations_host(sched, s, pool_np)
+
+
+class _PointerAttributes(ctypes.Structure):
+    _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int),
+                ("devicePointer", ctypes.c_void_p), ("hostPointer", ctypes.c_void_p),
+                ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+
+
+def _hip_runtime() -> ctypes.CDLL:
+    """The HIP runtime that torch has loaded (the library binds to it too)."""
+    for line in open("/proc/self/maps"):
+        path = line.split()[-1]
+        if "libamdhip64" in path:
+            lib = ctypes.CDLL(path)
+            break
+    else:
+        raise RuntimeError("the HIP runtime is not loaded")
+    P = ctypes.c_void_p
+    lib.hipExtMallocWithFlags.argtypes = [ctypes.POINTER(P), ctypes.c_size_t, ctypes.c_uint]
+    lib.hipPointerGetAttributes.argtypes = [ctypes.POINTER(_PointerAttributes), P]
+    lib.hipFree.argtypes = [P]
+    lib.hipStreamWaitValue32.argtypes = [P, P, ctypes.c_uint32, ctypes.c_uint, ctypes.c_uint32]
+    for f in (lib.hipExtMallocWithFlags, lib.hipPointerGetAttributes, lib.hipFree,
+              lib.hipStreamWaitValue32):
+        f.restype = ctypes.c_int
+    return lib
+
+
+class HostGate:
+    """A 32-bit flag in the runtime's signal memory that holds a stream
+    (hipStreamWaitValue32 until it equals 1) until the host opens it: the
+    host decides when the held stream goes on.  A timer opens it after
+    `failsafe` seconds whatever the test does, and close() opens it and waits
+    for the device before freeing it, so no stream is left waiting."""
+
+    SIGNAL_MEMORY = 0x2      # hipMallocSignalMemory
+    WAIT_EQ = 0x1            # hipStreamWaitValueEq
+
+    def __init__(self, failsafe: float = 30.0):
+        self.hip = _hip_runtime()
+        p = ctypes.c_void_p()
+        assert self.hip.hipExtMallocWithFlags(ctypes.byref(p), 8, self.SIGNAL_MEMORY) == 0
+        self.ptr = p.value
+        attr = _PointerAttributes()
+        assert self.hip.hipPointerGetAttributes(ctypes.byref(attr), self.ptr) == 0
+        assert attr.hostPointer, "signal memory without a host address"
+        self.flag = ctypes.c_uint32.from_address(attr.hostPointer)
+        self.flag.value = 0
+        self.timer = threading.Timer(failsafe, self.open)
+        self.timer.start()
+
+    def hold(self, stream: torch.cuda.Stream) -> None:
+        rc = self.hip.hipStreamWaitValue32(ctypes.c_void_p(stream.cuda_stream),
+                                           ctypes.c_void_p(self.ptr), 1, self.WAIT_EQ,
+                                           0xFFFFFFFF)
+        assert rc == 0, rc
+
+    def open(self) -> None:
+        self.flag.value = 1
+
+    def close(self) -> None:
+        self.open()
+        self.timer.cancel()
+        torch.cuda.synchronize()
+        self.hip.hipFree(ctypes.c_void_p(self.ptr))

@@ -606,3 +606,72 @@ def test_binding_keeps_call_buffers_alive_until_complete():
         assert ref() is None
     finally:
         kv.close()
+
+
+def test_host_gated_stream_forces_each_hazard_order():
+    """Forced interleavings from the host.  Stream A is held by a wait on a
+    host flag ahead of a swap-out, so that swap-out stays pending until the
+    host opens the flag, after every later call has been issued.  Each later
+    call on another stream that conflicts with it gets a device-side wait
+    (counted by the library, none elided since A cannot have completed): a
+    swap-in reading its image (read after write), a swap-in writing the
+    blocks it reads (write after read), a swap-out writing the same image
+    bytes again (write after write, and after the first swap-in's read).  A
+    call that touches none of them gets no wait.  Once the host opens the
+    gate, pool and images equal the oracle run in issue order.  (Whether an
+    unrelated stream progresses meanwhile is the runtime's business: streams
+    share a few hardware queues.)"""
+    from tests.gpu_util import HostGate
+
+    shape = wl.KVShape(4, 512, 8, 16, 128, wl.BF16)
+    C = shape.chunk_bytes
+    d = odesc(shape)
+    pool = device_pool(shape, 19)
+    pool_h = host(pool)
+    perm = wl.permutation(shape.num_blocks, 17)
+    X, Y, W, Z = perm[:32], perm[32:64], perm[64:96], perm[96:128]
+    img = torch.zeros(shape.image_bytes(32), dtype=torch.uint8, device="cuda")
+    img_e = torch.zeros_like(img)
+    other = torch.empty(shape.image_bytes(16), dtype=torch.uint8, device="cuda")
+    wl.fill_chunks(other.view(-1, C), torch.arange(4 * 16, dtype=torch.int64) * 104729 + 11,
+                   C, shape.dtype)
+    other_h = host(other)
+    streams = [torch.cuda.Stream() for _ in range(5)]
+    torch.cuda.synchronize()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    gate = HostGate()
+    try:
+        gate.hold(streams[0])
+        calls = [("A", lambda s: kv.swap_out([X], img, stream=s)),
+                 ("B", lambda s: kv.swap_in([Y], img, stream=s)),           # reads A's image
+                 ("C", lambda s: kv.swap_in([X[:16]], other, stream=s)),    # writes what A reads
+                 ("D", lambda s: kv.swap_out([W], img, stream=s)),          # rewrites A's image
+                 ("E", lambda s: kv.swap_out([Z], img_e, stream=s))]        # independent
+        waits, elided, tickets = {}, {}, {}
+        for (name, call), s in zip(calls, streams):
+            before = kv.stats()
+            tickets[name] = call(s)
+            after = kv.stats()
+            waits[name] = after["waits_inserted"] - before["waits_inserted"]
+            elided[name] = after["waits_elided"] - before["waits_elided"]
+        pending_a = not kv.query(tickets["A"])
+        say("waits per call while the gate is shut:", waits, "elided:", elided)
+        assert pending_a
+        assert waits["A"] == 0 and waits["E"] == 0 and elided["E"] == 0
+        assert waits["B"] == 1 and waits["C"] == 1 and waits["D"] >= 1
+        assert sum(elided.values()) == 0
+        gate.open()
+        kv.sync()
+    finally:
+        gate.close()
+        kv.close()
+    want_img = np.zeros(img.numel(), dtype=np.uint8)
+    want_e = np.zeros(img.numel(), dtype=np.uint8)
+    assert oracle.swap_out(d, pool_h, [X], want_img) == 0
+    assert oracle.swap_in(d, pool_h, [Y], want_img) == 0
+    assert oracle.swap_in(d, pool_h, [X[:16]], other_h) == 0
+    assert oracle.swap_out(d, pool_h, [W], want_img) == 0
+    assert oracle.swap_out(d, pool_h, [Z], want_e) == 0
+    assert_bytes_equal(host(img), want_img, "image rewritten last")
+    assert_bytes_equal(host(img_e), want_e, "independent image")
+    assert_bytes_equal(host(pool), pool_h, "pool")
