@@ -104,6 +104,7 @@ struct aqua_kv_pool {
     uint64_t fail_release_at = ~0ull;
     std::vector<StagedSeq> sseq;
     std::vector<uint64_t> slot_offsets;  // per sequence, in a slot
+    uint64_t call_blocks = 0;            // table entries of the call being enqueued
 
     uint64_t next_ticket = 1;
     uint64_t unit_bytes = kDefaultUnitBytes;
@@ -454,8 +455,9 @@ aqua_status resolve_buffer(aqua_kv_pool* p, const void* ptr, uint64_t bytes,
     return AQUA_OK;
 }
 
+// One launch over layers [l0, l0 + nl) of the call being enqueued.
 aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const RunDesc* descs,
-                             uint32_t ndesc, int32_t target) {
+                             uint32_t ndesc, int32_t target, uint32_t l0, uint32_t nl) {
     aqua::SwapLaunch L;
     L.out = !is_in;
     L.pool = p->base;
@@ -463,12 +465,12 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     L.img_l0 = 0;
     L.descs = descs;
     L.ndesc = ndesc;
-    L.first_layer = 0;
-    L.num_layers = p->shape.L;
+    L.first_layer = l0;
+    L.num_layers = nl;
     L.chunk_bytes = p->shape.C;
     L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
     L.max_workgroups = p->max_wg[target];
-    L.nt_pool_store = p->shape.C >= aqua::kNtPoolStoreMinChunk;
+    L.nt_pool_store = aqua::nt_pool_store(p->shape.C, (uint64_t)nl * p->call_blocks * p->shape.C);
     return L;
 }
 
@@ -509,9 +511,7 @@ void stage_pieces(aqua_kv_pool* p, bool to_host, const void* buf, uint8_t* slot,
 aqua::SwapLaunch slot_launch(aqua_kv_pool* p, bool is_in, uint8_t* slot, const RunDesc* descs,
                              uint32_t ndesc, uint32_t l0, uint32_t nl) {
     // The kernels only touch HBM here: no host-link grid cap.
-    aqua::SwapLaunch L = make_launch(p, is_in, slot, descs, ndesc, AQUA_TARGET_DEVICE);
-    L.first_layer = l0;
-    L.num_layers = nl;
+    aqua::SwapLaunch L = make_launch(p, is_in, slot, descs, ndesc, AQUA_TARGET_DEVICE, l0, nl);
     L.img_l0 = l0;
     return L;
 }
@@ -687,6 +687,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                          : AQUA_ERR_INVALID;
     if (st == AQUA_ERR_INVALID) return st;
     const uint64_t total = num_seqs ? offs[num_seqs] : 0;
+    p->call_blocks = total;
 
     DeviceGuard dg(p->device);
     if (!dg.ok) {
@@ -810,11 +811,9 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                                 &rec);
             if (st != AQUA_OK) return fail_enqueued(stream, st);
         } else {
-            aqua::SwapLaunch L =
+            const aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
-                            (uint32_t)p->plan.size(), target);
-            L.first_layer = l_begin;
-            L.num_layers = l_count;
+                            (uint32_t)p->plan.size(), target, l_begin, l_count);
             (void)hipGetLastError();
             e = aqua::launch_swap(L, stream);
             if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));

@@ -24,10 +24,18 @@ struct SwapLaunch {
     bool nt_pool_store;       // scatter: nontemporal stores into the pool
 };
 
-// Scatter store hint for a pool of chunk_bytes-sized chunks: measured on
-// MI355X, nontemporal pool stores shorten the scatter by up to 5 % for 64 KiB
-// chunks and lengthen it by 10 % for the 32 KiB chunks of an fp8 pool.
+// Scatter store hint, measured on MI355X.  Nontemporal pool stores pay for
+// large chunks and for launches that write much more than the 256 MB
+// last-level cache holds.  A smaller launch of smaller chunks ends sooner with
+// ordinary stores, which L2 and that cache partly absorb:
+//   64 KiB chunks: 0-7 % shorter with nontemporal stores, 2 to 10 GiB launches;
+//   32 KiB chunks: 10 % longer at 1 GiB per launch, 0.5-2 % shorter at 4.4-5 GiB;
+//   16 KiB chunks: 20 % longer at 512 MiB per launch, 7 % shorter at 2.5 GiB.
 constexpr uint64_t kNtPoolStoreMinChunk = 64ull << 10;
+constexpr uint64_t kNtPoolStoreMinBytes = 2ull << 30;
+inline bool nt_pool_store(uint64_t chunk_bytes, uint64_t launch_bytes) {
+    return chunk_bytes >= kNtPoolStoreMinChunk || launch_bytes >= kNtPoolStoreMinBytes;
+}
 
 // Enqueues the copy on `stream`; returns the first launch error.
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream);
