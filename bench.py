@@ -498,20 +498,28 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     in_b = np.array([e[5] for e in evs], dtype=np.float64) * unit
     out_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     in_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
-    return wall, st, out_b, in_b, out_ms, in_ms
+    # Union of the two calls' intervals in each slice, from the swap-out's start.
+    both_ms = np.array([max(e[0].elapsed_time(e[1]), e[0].elapsed_time(e[3]))
+                        - min(0.0, e[0].elapsed_time(e[2])) for e in evs])
+    return wall, st, out_b, in_b, out_ms, in_ms, both_ms
 
 
-def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, config,
+def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, both_ms, steps, config,
                   host=False):
     from paper_2407_21255_amd import workload as wl
 
     moved = float(out_b.sum() + in_b.sum())
     ok = out_b > 0
-    # Gather rate of each slice: its bytes are read and written once in HBM,
-    # or cross the host link once.
+    # A slice's swap-out and swap-in run on two streams (at once, unless the
+    # library orders them) and share the bound: every payload byte is read and
+    # written once in HBM, or crosses one direction of the host link once
+    # (both directions busy: twice the per-direction peak).  Rate of each slice
+    # over the union of the two calls' intervals.
     per = 1 if host else 2
-    achieved = float((per * out_b[ok] / (out_ms[ok] * 1e-3)).mean()) / 1e9 if ok.any() else 0.0
-    peak = HOST_LINK_PEAK_GBS if host else HBM_PEAK_GBS
+    both = (out_b + in_b) > 0
+    achieved = (float((per * (out_b + in_b)[both] / (both_ms[both] * 1e-3)).mean()) / 1e9
+                if both.any() else 0.0)
+    peak = 2 * HOST_LINK_PEAK_GBS if host else HBM_PEAK_GBS
     res = dict(res_common)
     res.update({
         "value": round(moved / wall / 1e9, 2),
@@ -520,11 +528,12 @@ def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, steps, co
         "config": config,
         "roofline": {
             "bound": "host_link" if host else "hbm",
-            "kernel": "gather (swap-out), concurrent with the scatter",
+            "kernel": "gather and scatter of a slice, on two streams"
+                      + (" (one link direction each)" if host else " (sharing HBM)"),
             "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
             "frac": round(achieved / peak, 4), "traffic": None,
-            "algorithmic_bytes_per_launch": round(float(per * out_b[ok].mean())) if ok.any()
-            else 0,
+            "algorithmic_bytes_per_launch": round(float(per * (out_b + in_b)[both].mean()))
+            if both.any() else 0,
         },
         "kernel_ms": {"swap_out_mean": round(float(out_ms[ok].mean()), 4) if ok.any() else 0,
                       "swap_in_mean": round(float(in_ms[in_b > 0].mean()), 4)
