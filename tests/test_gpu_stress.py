@@ -6,6 +6,8 @@ every call is several copy-engine jobs, or swapped zero-copy; or it is in
 HBM.  The library must behave as if the calls ran in issue order: pool,
 arena and region at the end equal the oracle run call by call in that
 order."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -18,6 +20,7 @@ from tests.gpu_util import device_pool, host, odesc, say
 
 ARENA = 4 << 20
 REGION = 4 << 20
+OPS = int(os.environ.get("AQUA_TEST_STRESS_OPS", "150"))   # calls per run
 
 
 def _ops(shape, rng, count):
@@ -75,7 +78,7 @@ def test_random_calls_on_four_streams(monkeypatch, path, seed):
         arena.copy_(fill)
     region = torch.from_numpy(rng.integers(0, 256, size=REGION, dtype=np.uint8)).cuda()
     pool_h, arena_h, region_h = host(pool), host(arena).copy(), host(region)
-    ops = _ops(shape, rng, 150)
+    ops = _ops(shape, rng, OPS)
     say("stress", path, seed, {k: sum(1 for o in ops if o[0] == k)
                                for k in ("out", "in", "to_host", "to_device")})
     streams = [torch.cuda.Stream() for _ in range(4)]
