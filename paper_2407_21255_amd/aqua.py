@@ -378,15 +378,19 @@ class KVPool:
         self.handle = h
         self._spaces = []      # swap spaces on this pool, closed before it
         self._held = {}        # ticket -> the tensors its call names, until it completes
+        self._prune_at = 64    # prune completed entries when this many are held
 
     def _hold(self, ticket: int, *tensors) -> None:
         """Keeps the tensors that a call reads or writes alive until the call
         completes: the library only borrows their memory, and a tensor freed
         early could be handed out again while a kernel or a copy engine still
         uses it."""
-        done = [t for t in self._held if aqua_query(self.handle, t) == 1]
-        for t in done:
-            del self._held[t]
+        if len(self._held) >= self._prune_at:
+            done = [t for t in self._held if aqua_query(self.handle, t) == 1]
+            for t in done:
+                del self._held[t]
+            # Amortised: the next pass waits until the held set has doubled.
+            self._prune_at = max(64, 2 * len(self._held))
         self._held[ticket] = tensors
 
     def _swap(self, is_in, tables, buf, img_offsets, stream, target, img_blocks, layers):
