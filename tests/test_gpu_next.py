@@ -33,6 +33,56 @@ def _buf(nbytes, where):
 
 
 @pytest.mark.parametrize("where", ["hbm", "staged", "zero_copy"])
+def test_ex_forms_multi_sequence_placed_images(where, monkeypatch):
+    """Both extensions in one call, for several sequences: images longer
+    than their tables (m_s >= n_s, a different m_s per sequence, one table
+    empty), placed at chosen offsets with gaps, over all layers or a layer
+    subset.  Swap-out and swap-in equal the oracle's extended forms byte for
+    byte, guard bytes included.  Staged calls go through 128 KiB slots, so a
+    call is several jobs with one piece per layer and sequence."""
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(128 << 10))
+    shape = wl.KVShape(6, 128, 2, 16, 64, wl.BF16)              # 8 KiB chunks
+    C, L = shape.chunk_bytes, shape.num_layers
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 77)
+    out_t = [perm[0:5], perm[5:5], perm[5:17], perm[17:18]]
+    in_t = [perm[40:45], perm[45:45], perm[45:57], perm[57:58]]
+    m = [9, 3, 12, 1]
+    offs, pos = [], 0
+    for ms in m:
+        pos += 4096 + 48
+        pos = (pos + 15) // 16 * 16
+        offs.append(pos)
+        pos += L * ms * C
+    G = 4096
+    total = pos + 4096
+    pool = device_pool(shape, 77)
+    pool_h = host(pool)
+    rng = np.random.default_rng(77)
+    start = rng.integers(0, 256, size=total + 2 * G, dtype=np.uint8)
+    buf = _buf(total + 2 * G, where)
+    buf.copy_(torch.from_numpy(start))
+    want = start.copy()
+    inner, want_inner = buf[G:G + total], want[G:G + total]
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        if HOST_PATHS[where] is not None:
+            kv.set_host_path(HOST_PATHS[where])
+        for l0, nl in [(0, 0), (2, 3), (5, 1)]:
+            layers = None if nl == 0 else (l0, nl)
+            say("ex forms", where, "layers", layers)
+            kv.swap_out(out_t, inner, offs, img_blocks=m, layers=layers)
+            kv.swap_in(in_t, inner, offs, img_blocks=m, layers=layers)
+            kv.sync()
+            assert oracle.swap_out_ex(d, pool_h, out_t, want_inner, offs, m, l0, nl) == 0
+            assert oracle.swap_in_ex(d, pool_h, in_t, want_inner, offs, m, l0, nl) == 0
+            assert_bytes_equal(host(buf), want, f"buffer after layers {layers}")
+            assert_bytes_equal(host(pool), pool_h, f"pool after layers {layers}")
+    finally:
+        kv.close()
+
+
+@pytest.mark.parametrize("where", ["hbm", "staged", "zero_copy"])
 def test_prefix_swap_in_from_cached_image(where):
     """A long prompt's image is cached once; prefixes of it are swapped back
     in, several times, into fresh blocks (the table covers the first m of
