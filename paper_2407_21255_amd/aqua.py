@@ -333,6 +333,7 @@ class RawBuffer:
     def element_size(self) -> int:
         return 1
 
+
 def _csr(tables):
     """(int32 ids, uint64 offsets) from a list of tables or an (ids, offs) pair."""
     if isinstance(tables, tuple) and len(tables) == 2 and isinstance(tables[0], np.ndarray):

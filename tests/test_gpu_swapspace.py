@@ -227,3 +227,68 @@ def test_fair_scheduling_images_in_a_swap_space_with_reclaim_and_restore():
     finally:
         space.close()
         kv.close()
+
+
+def test_partial_reclaim_and_restore_follow_handle_order():
+    """reclaim(bytes) moves the oldest device tensors until that much of the
+    region is free; restore moves host tensors back, oldest first, skipping
+    those that do not fit.  Tensors allocated and freed in between reuse the
+    vacated ranges, all without host syncs.  Placements follow that rule,
+    and every tensor's bytes and the pool after swap-ins from wherever the
+    tensors are equal the oracle's."""
+    shape = wl.KVShape(2, 256, 1, 2, 8, wl.BF16)         # 64-byte chunks, 128 B per block
+    d = odesc(shape)
+    unit = shape.num_layers * shape.chunk_bytes
+    pool = device_pool(shape, 23)
+    pool_h = host(pool)
+    perm = wl.permutation(shape.num_blocks, 23)
+    # Image sizes (blocks): 2, 1, 3, 2 KiB fill the 8 KiB device region; the
+    # fifth (2 KiB) falls back to host memory.
+    sizes = [16, 8, 24, 16, 16]
+    tables, k = [], 0
+    for n in sizes:
+        tables.append(perm[k:k + n])
+        k += n
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    space = aqua.SwapSpace(kv, 8192, 65536)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    D, H = aqua.AQUA_TARGET_DEVICE, aqua.AQUA_TARGET_HOST
+    try:
+        hs = [space.alloc(n * unit) for n in sizes]
+        assert [space.locate(h)[2] for h in hs] == [D, D, D, D, H]
+        for h, t in zip(hs, tables):
+            kv.swap_out([t], space.buffer(h), stream=sa)
+        assert space.reclaim(2560, stream=sb) > 0        # 2 KiB is not enough: two move
+        assert [space.locate(h)[2] for h in hs] == [H, H, D, D, H]
+        t6 = perm[k:k + 24]
+        k += 24
+        h6 = space.alloc(24 * unit)                      # takes the vacated 3 KiB
+        assert space.locate(h6)[2] == D
+        kv.swap_out([t6], space.buffer(h6), stream=sa)
+        assert space.restore(stream=sb) == 0             # nothing fits
+        space.free(hs[2])                                # 3 KiB free again
+        assert space.restore(stream=sb) > 0              # 2 KiB + 1 KiB fit, 2 KiB does not
+        assert [space.locate(h)[2] for h in hs if h != hs[2]] == [D, D, D, H]
+        live = [(h, t) for h, t in zip(hs, tables) if h != hs[2]] + [(h6, t6)]
+        images = {h: space.locate(h) for h, _ in live}
+        fresh = perm[k:]
+        ins, j = [], 0
+        for h, t in live:
+            ins.append((h, fresh[j:j + len(t)]))
+            j += len(t)
+        for h, t in ins:
+            kv.swap_in([t], space.buffer(h), stream=sb)
+        kv.sync()
+        got = {h: _read(images[h][0], images[h][1]) for h, _ in live}
+    finally:
+        space.close()
+        kv.close()
+    want = {}
+    for h, t in live:
+        want[h] = np.zeros(len(t) * unit, dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [t], want[h]) == 0
+    for h, t in ins:
+        assert oracle.swap_in(d, pool_h, [t], want[h]) == 0
+    for h, _ in live:
+        assert_bytes_equal(got[h], want[h], f"tensor {h}")
+    assert_bytes_equal(host(pool), pool_h, "pool")
