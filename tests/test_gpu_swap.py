@@ -675,3 +675,53 @@ def test_host_gated_stream_forces_each_hazard_order():
     assert_bytes_equal(host(img), want_img, "image rewritten last")
     assert_bytes_equal(host(img_e), want_e, "independent image")
     assert_bytes_equal(host(pool), pool_h, "pool")
+
+
+@pytest.mark.parametrize("where", ["hbm", "staged"])
+def test_descriptor_ring_wraps_and_grows(monkeypatch, where):
+    """A 4 KiB descriptor ring (128 runs): calls of 100 runs wrap it and wait
+    for the calls that used the space last, a call of 1000 runs makes it
+    grow, and later calls use the grown ring.  No host sync between calls;
+    every image and the pool equal the oracle run in issue order."""
+    monkeypatch.setenv("AQUA_RING_BYTES", "4096")
+    monkeypatch.setenv("AQUA_STAGE_SLOT_BYTES", str(256 << 10))
+    shape = wl.KVShape(2, 4096, 1, 4, 16, wl.BF16)            # 256-byte chunks
+    d = odesc(shape)
+    pool = device_pool(shape, 31)
+    pool_h = host(pool)
+    perm = wl.permutation(shape.num_blocks, 31)
+    sizes = [100, 100, 100, 1000, 100, 100]
+    tables, k = [], 0
+    for n in sizes:
+        tables.append(perm[k:k + n])
+        k += n
+    fresh = perm[k:]
+    pinned = where == "staged"
+    imgs = [torch.zeros(shape.image_bytes(n), dtype=torch.uint8,
+                        **({"pin_memory": True} if pinned else {"device": "cuda"}))
+            for n in sizes]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        kv.set_host_path(aqua.AQUA_HOST_STAGED)
+        ins, j = [], 0
+        for i, (t, img) in enumerate(zip(tables, imgs)):
+            kv.swap_out([t], img, stream=streams[i % 2])
+            dst = fresh[j:j + len(t)]
+            j += len(t)
+            kv.swap_in([dst], img, stream=streams[(i + 1) % 2])
+            ins.append(dst)
+        st = kv.stats()
+        kv.sync()
+        say("ring", where, "waits inserted", st["waits_inserted"],
+            "host wait ms", round(st["wait_ns"] / 1e6, 3), "descriptors", st["descriptors"])
+        # Random tables: almost every block is a run of its own.
+        assert 1.9 * sum(sizes) <= st["descriptors"] <= 2 * sum(sizes)
+    finally:
+        kv.close()
+    for t, dst, img in zip(tables, ins, imgs):
+        want = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, [t], want) == 0
+        assert_bytes_equal(host(img), want, "image")
+        assert oracle.swap_in(d, pool_h, [dst], want) == 0
+    assert_bytes_equal(host(pool), pool_h, "pool")
