@@ -30,7 +30,7 @@ def _gpu():
 
 def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
                buf_bytes=None, pinned=False, sentinel=True, stream=None, host_path=None,
-               carrier=None):
+               carrier=None, max_workgroups=None):
     """swap_out(out_tables) then swap_in(in_tables) on the GPU and in the
     oracle; compares the image, guards and the whole pool."""
     C = shape.chunk_bytes
@@ -50,6 +50,9 @@ def _roundtrip(shape, seed, out_tables, in_tables, owner, img_offsets=None,
     kv = aqua.KVPool(shape.as_tuple(), pool)
     if host_path is not None:
         kv.set_host_path(host_path)
+    if max_workgroups is not None:
+        kv.set_max_workgroups(aqua.AQUA_TARGET_HOST if pinned else aqua.AQUA_TARGET_DEVICE,
+                              max_workgroups)
     if carrier is not None:
         for direction in (0, 1):
             kv.set_link_engine(direction, carrier)
@@ -147,6 +150,19 @@ def test_unit_size_extremes(unit, monkeypatch):
     in_tables = [list(range(400, 700)), list(range(700, 750))]
     say("unit", unit)
     _roundtrip(shape, 9, out_tables, in_tables, None)
+
+
+@pytest.mark.parametrize("cap,pinned", [(1, False), (7, False), (300, False), (3, True)])
+def test_capped_grids_loop_over_every_unit(cap, pinned):
+    """A grid capped below the number of (layer, run) units: each workgroup
+    loops over units a grid apart, and every byte still moves once."""
+    shape = wl.KVShape(3, 512, 2, 16, 64, wl.BF16)            # 8 KiB chunks
+    perm = wl.permutation(shape.num_blocks, 61)
+    out_tables = [perm[:150], perm[150:151], perm[151:233]]
+    in_tables = [perm[233:383], perm[383:384], perm[384:466]]
+    say("cap", cap, "pinned", pinned)
+    _roundtrip(shape, 61, out_tables, in_tables, None, pinned=pinned,
+               host_path=aqua.AQUA_HOST_ZERO_COPY if pinned else None, max_workgroups=cap)
 
 
 def test_pinned_host_zero_copy_round_trip():
