@@ -179,12 +179,15 @@ hipError_t release_flags(aqua_kv_pool* p, int64_t* a, int64_t* b, hipStream_t st
 
 // After a failure between submitting engine jobs and enqueueing their
 // release: once the stream's earlier work has ended, the held flags are
-// released from the host, so that the engine's queue drains.
+// released from the host, so that the engine's queue drains, and the call
+// returns once those jobs' copies have ended too.
 aqua_status fail_held(aqua_kv_pool* p, aqua::LinkEngine& w, hipStream_t stream,
                       int64_t* const* held, int n, hipError_t e) {
     (void)hipStreamSynchronize(stream);
     (void)hipGetLastError();
-    for (int i = 0; i < n; ++i) w.release_on_host(held[i]);
+    uint64_t upto = 0;
+    for (int i = 0; i < n; ++i) upto = std::max(upto, w.release_on_host(held[i]));
+    w.wait_published(upto);
     return latch(p, e);
 }
 

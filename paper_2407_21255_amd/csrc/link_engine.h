@@ -103,8 +103,12 @@ class LinkEngine {
     // release kernel was never enqueued (its call failed first), so that the
     // engine's queue, which every later copy on the engine shares, does not
     // hold a copy that waits forever.  The caller first waits for the work
-    // that the job's copies were to follow.
-    void release_on_host(int64_t* flag);
+    // that the job's copies were to follow.  Returns the completed-job count
+    // that covers the job (0 if no held job has this flag).
+    uint64_t release_on_host(int64_t* flag);
+    // Blocks the calling thread until `count` jobs are published (complete,
+    // or failed after the job time limit).
+    void wait_published(uint64_t count) const;
     // Makes `stream` wait until `count` jobs have completed.
     hipError_t stream_wait(hipStream_t stream, uint64_t count);
 

@@ -245,15 +245,23 @@ uint64_t LinkEngine::submit(const std::vector<LinkPiece>& pieces, int64_t** flag
     return index;
 }
 
-void LinkEngine::release_on_host(int64_t* flag) {
-    if (!flag) return;
+uint64_t LinkEngine::release_on_host(int64_t* flag) {
+    if (!flag) return 0;
     // A held job cannot have completed, so it is still queued here.
     std::lock_guard<std::mutex> lk(mu_);
     for (const Job& j : q_)
         if (j.flag == flag) {
             hsa_signal_store_screlease(j.ready, 0);
-            return;
+            return j.index + 1;
         }
+    return 0;
+}
+
+void LinkEngine::wait_published(uint64_t count) const {
+    // The library thread publishes every job, at the latest once the job
+    // time limit has passed, so this ends.
+    while (count_host_ && __atomic_load_n(count_host_, __ATOMIC_ACQUIRE) < count)
+        std::this_thread::sleep_for(std::chrono::microseconds(50));
 }
 
 hipError_t LinkEngine::stream_wait(hipStream_t stream, uint64_t count) {
