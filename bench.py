@@ -15,7 +15,9 @@ of 16 fragmented 2048-token prompts preempted to an HBM offload region.
 from __future__ import annotations
 
 import argparse
+import contextlib
 import ctypes
+import gc
 import hashlib
 import json
 import os
@@ -132,22 +134,33 @@ def cpu_baseline(shape, target_seconds: float):
     img = np.zeros(small.image_bytes(128), dtype=np.uint8)
     assert oracle.swap_out(d, pool, [a], img) == 0  # touch every page once
     assert oracle.swap_in(d, pool, [b], img) == 0
+    # One core for the timing (this thread only), restored afterwards.
+    try:
+        prev = os.sched_getaffinity(0)
+        os.sched_setaffinity(0, {min(prev)})
+        pinned = f"pinned to core {min(prev)}"
+    except (AttributeError, OSError):
+        prev, pinned = None, "not pinned"
     reps, moved = 0, 0
-    t0 = time.perf_counter()
-    while True:
-        src, dst = (a, b) if reps % 2 == 0 else (b, a)
-        assert oracle.swap_out(d, pool, [src], img) == 0
-        assert oracle.swap_in(d, pool, [dst], img) == 0
-        reps += 1
-        moved += 2 * img.nbytes
-        el = time.perf_counter() - t0
-        if el >= target_seconds:
-            break
+    try:
+        t0 = time.perf_counter()
+        while True:
+            src, dst = (a, b) if reps % 2 == 0 else (b, a)
+            assert oracle.swap_out(d, pool, [src], img) == 0
+            assert oracle.swap_in(d, pool, [dst], img) == 0
+            reps += 1
+            moved += 2 * img.nbytes
+            el = time.perf_counter() - t0
+            if el >= target_seconds:
+                break
+    finally:
+        if prev is not None:
+            os.sched_setaffinity(0, prev)
     return {
         "value": round(moved / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
         "sample": f"{L}-layer chunks of {small.chunk_bytes} B on a 512-block pool: one "
                   f"128-block prompt ({img.nbytes >> 20} MiB per direction) out and back in, "
-                  f"{reps} round trips in {el:.1f} s, single thread",
+                  f"{reps} round trips in {el:.1f} s, single thread {pinned}",
     }
 
 
@@ -300,15 +313,16 @@ def run_pair(args, res_common):
     # GEMMs enqueued step by step beside the swaps, so that both streams
     # start together.
     comp = GemmCompanion(step_s, args.steps) if args.gemm else None
-    t0 = time.perf_counter()
-    st0 = kv.stats()
-    for i in range(args.steps):
-        if comp:
-            comp.step()
-        step(args.warmup + i, True)
-    kv.sync(0)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    with _no_gc():
+        t0 = time.perf_counter()
+        st0 = kv.stats()
+        for i in range(args.steps):
+            if comp:
+                comp.step()
+            step(args.warmup + i, True)
+        kv.sync(0)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
     st = _since(kv.stats(), st0)
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
                if pinned and args.host_path == "staged" else None)
@@ -415,7 +429,40 @@ def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
             d2.copy_(h2, non_blocking=True)
     torch.cuda.synchronize()
     out["both_total"] = round(2 * nbytes * reps / (time.perf_counter() - t0) / 1e9, 2)
+    out["pcie"] = pcie_link()
     return out
+
+
+def pcie_link():
+    """The trained PCIe link of the (single) AMD GPU, from sysfs, e.g.
+    "32.0 GT/s PCIe x16"; None where sysfs does not say."""
+    import glob
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        try:
+            if open(os.path.join(dev, "vendor")).read().strip() != "0x1002":
+                continue
+            speed = open(os.path.join(dev, "current_link_speed")).read().strip()
+            width = open(os.path.join(dev, "current_link_width")).read().strip()
+            return f"{speed} x{width}"
+        except OSError:
+            continue
+    return None
+
+
+@contextlib.contextmanager
+def _no_gc():
+    """Python's cyclic collector paused over a timed region, after one
+    collection: a full pass over a process that holds torch stalls the host
+    for tens of milliseconds, long enough for the GPU to drain its queue and
+    idle.  (The collector is Python's, not part of the measured path.)"""
+    gc.collect()
+    was = gc.isenabled()
+    gc.disable()
+    try:
+        yield
+    finally:
+        if was:
+            gc.enable()
 
 
 def _since(after: dict, before: dict) -> dict:
@@ -485,12 +532,13 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     kv.sync(0)
     torch.cuda.synchronize()
     st0 = kv.stats()
-    t0 = time.perf_counter()
-    for k in ids[warmup:]:
-        one(k, True)
-    kv.sync(0)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    with _no_gc():
+        t0 = time.perf_counter()
+        for k in ids[warmup:]:
+            one(k, True)
+        kv.sync(0)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
     st = _since(kv.stats(), st0)
     kv.close()
     unit = s.num_layers * s.chunk_bytes
@@ -640,13 +688,14 @@ def run_elastic(args, res_common):
         return {"bytes": moved, "ms": round(dt * 1e3, 3), "GBps": round(moved / dt / 1e9, 2),
                 "tensors_moved": abs(after["host_tensors"] - before["host_tensors"])}
 
-    wall0 = time.perf_counter()
-    ph = [phase(0, n1)]
-    rec = move(space.reclaim)
-    ph.append(phase(n1, n2))
-    res_ = move(space.restore)
-    ph.append(phase(n2, n3))
-    wall = time.perf_counter() - wall0
+    with _no_gc():
+        wall0 = time.perf_counter()
+        ph = [phase(0, n1)]
+        rec = move(space.reclaim)
+        ph.append(phase(n1, n2))
+        res_ = move(space.restore)
+        ph.append(phase(n2, n3))
+        wall = time.perf_counter() - wall0
     carrier = [kv.link_engine(0), kv.link_engine(1)]
     space.close()
     kv.close()
@@ -839,14 +888,15 @@ def run_next(args, res_common):
     comp = GemmCompanion(step_s, args.steps) if args.gemm else None
     evs = []
     st0 = kv.stats()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        if comp:
-            comp.step()
-        step(evs)
-    kv.sync(0)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    with _no_gc():
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            if comp:
+                comp.step()
+            step(evs)
+        kv.sync(0)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
     st = _since(kv.stats(), st0)
     carrier = ([kv.link_engine(0), kv.link_engine(1)]
                if (pinned and args.host_path == "staged") or w == "migrate" else None)
