@@ -95,8 +95,10 @@ enum { AQUA_F16 = 1, AQUA_BF16 = 2, AQUA_FP8_E4M3 = 3 };
 
 /* Offload targets.  DEVICE: device memory on the pool's GPU (a carved-out
  * HBM region standing in for a scale-up peer's memory).  HOST: page-locked
- * host memory from hipHostMalloc (torch pin_memory), written and read by
- * the kernels directly over the host link (zero copy). */
+ * host memory from hipHostMalloc (torch pin_memory), reached over the host
+ * link as aqua_kv_pool_set_host_path chooses: staged through HBM slots and
+ * moved by a copy engine (the default), or read and written by the kernels
+ * directly (zero copy). */
 enum { AQUA_TARGET_DEVICE = 0, AQUA_TARGET_HOST = 1 };
 
 typedef struct {
