@@ -297,9 +297,11 @@ AQUA_API aqua_status aqua_kv_pool_set_host_path(aqua_kv_pool_t pool, int32_t pat
  *                       fraction of the link rate.
  *   AQUA_LINK_AUTO      (default) the HSA runtime's preferred engine for the
  *                       direction if it names one, else the lowest-numbered
- *                       available engine, the two directions on different
- *                       engines where possible; the runtime's copies if no
- *                       engine can be used.
+ *                       free engine among those that carry the host link at
+ *                       its rate (engines 0-3 on MI355X), else one of those
+ *                       shared with its other users; the two directions on
+ *                       different engines where possible; the runtime's
+ *                       copies if no engine can be used.
  * The choice is made on the direction's next staged call.  Waits for every
  * outstanding call first.  dir other than 0 or 1, or another engine value:
  * AQUA_ERR_INVALID.
@@ -325,7 +327,7 @@ AQUA_API const char* aqua_status_str(aqua_status s);
  * region lent for offloading (the stand-in for a producer GPU's HBM) while a
  * range of it fits, else in pinned host memory (the DRAM fallback).  Reclaim
  * moves device tensors to host memory to hand device memory back; restore
- * moves host tensors back into the device region while they fit.  A handle
+ * moves host tensors back into the device region where they fit.  A handle
  * keeps its identity when its tensor moves; aqua_swap_locate gives the
  * current pointer and target, which the swap calls take.  Moves are
  * migrations on the space's pool (aqua_migrate), so calls on that pool issued
@@ -369,8 +371,10 @@ AQUA_API aqua_status aqua_swap_locate(aqua_swap_space_t space, uint64_t handle, 
 AQUA_API aqua_status aqua_swap_reclaim(aqua_swap_space_t space, uint64_t bytes, void* stream,
                                        uint64_t* ticket);
 
-/* Restore: moves host tensors (oldest handles first) into the device region
- * while they fit, as one migration on `stream`; *ticket as for reclaim. */
+/* Restore: moves host tensors into the device region, oldest handle first,
+ * each that a free range of the region fits at its turn (one that does not
+ * fit stays in host memory and later ones are still tried), as one
+ * migration on `stream`; *ticket as for reclaim. */
 AQUA_API aqua_status aqua_swap_restore(aqua_swap_space_t space, void* stream, uint64_t* ticket);
 
 /* Free bytes of each region and the number of live tensors in each. */
