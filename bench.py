@@ -391,7 +391,32 @@ def run_pair(args, res_common):
             "swap_out_vs_copy_engine": round(res["swap_out_GBps"] / res["link_ceiling"]["d2h"], 4),
             "swap_in_vs_copy_engine": round(res["swap_in_GBps"] / res["link_ceiling"]["h2d"], 4),
         }
+    elif not two_step:
+        copy_gbs = runtime_copy_rate(img, pool[:payload])
+        res["hbm_runtime_copy"] = {
+            "GBps_traffic": copy_gbs,
+            "swap_out_vs_runtime_copy": round(2 * res["swap_out_GBps"] / copy_gbs, 4),
+            "swap_in_vs_runtime_copy": round(2 * res["swap_in_GBps"] / copy_gbs, 4),
+        }
     return res, s
+
+
+def runtime_copy_rate(dst, src, reps: int = 5) -> float:
+    """HBM traffic rate (read + write, GB/s) of the runtime's own contiguous
+    device-to-device copy of the payload size (torch ``copy_``), timed with
+    HIP events after one untimed copy: the same-run yardstick for the swap
+    kernels' rates."""
+    import torch
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        dst.copy_(src)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            dst.copy_(src)
+        e1.record(stream)
+    stream.synchronize()
+    return round(2 * src.numel() * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
 
 
 def link_ceiling(nbytes: int = 1 << 30, reps: int = 5):
