@@ -1,0 +1,57 @@
+"""bench.py's host logic, without a GPU: the one-GPU guard, argument
+checks, the garbage-collector pause around timed regions and the CPU
+baseline record."""
+import gc
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+BENCH = os.path.join(ROOT, "bench.py")
+
+
+def _run(args, env_extra=None):
+    env = dict(os.environ)
+    env.update(env_extra or {})
+    return subprocess.run([sys.executable, BENCH, *args], capture_output=True, text=True,
+                          timeout=300, env=env)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = _run(["--gpus", "2"])
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+    r = _run([], {"WORLD_SIZE": "4"})
+    assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_bad_link_engine_is_an_argument_error():
+    r = _run(["--link-engine", "16"])
+    assert r.returncode == 2 and "--link-engine" in r.stderr
+
+
+def test_gc_pause_restores_the_collector():
+    sys.path.insert(0, ROOT)
+    import bench
+    assert gc.isenabled()
+    with bench._no_gc():
+        assert not gc.isenabled()
+    assert gc.isenabled()
+    gc.disable()
+    try:
+        with bench._no_gc():
+            pass
+        assert not gc.isenabled()        # left as the caller had it
+    finally:
+        gc.enable()
+
+
+def test_cpu_baseline_record():
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2407_21255_amd import workload as wl
+    affinity = os.sched_getaffinity(0)
+    rec = bench.cpu_baseline(wl.KVShape(4, 256, 8, 16, 128, wl.F16), 0.2)
+    assert rec["kind"] == "oracle" and rec["cores"] == 1 and rec["unit"] == "GB/s"
+    assert rec["value"] > 0 and "round trips" in rec["sample"]
+    assert os.sched_getaffinity(0) == affinity        # pinning undone
