@@ -605,11 +605,22 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
         *nl = std::min<uint32_t>(G, l_end - *l0);
         return p->staging[is_in] + (k % 2) * slot;
     };
+    uint64_t submitted = 0;  // completed-job count that covers this call's jobs so far
     auto submit = [&](uint32_t k, int64_t** flag) {
         uint32_t l0, nl;
         uint8_t* s = group(k, &l0, &nl);
         stage_pieces(p, !is_in, buf, s, G, l0, nl, &pieces);
-        return w.submit(pieces, flag);
+        const uint64_t job = w.submit(pieces, flag);
+        submitted = job + 1;
+        return job;
+    };
+    // A later step failed with no flag held: the jobs already released still
+    // run, and the call returns once they and the stream's work have ended.
+    auto fail = [&](hipError_t e) {
+        (void)hipStreamSynchronize(stream);
+        (void)hipGetLastError();
+        w.wait_published(submitted);
+        return latch(p, e);
     };
     auto kernel = [&](uint32_t k) {
         uint32_t l0, nl;
@@ -624,15 +635,15 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
         uint64_t first = 0, job = 0;
         for (uint32_t k = 0; k < K; ++k) {
             if (k >= 2 && (e = w.stream_wait(stream, first + k - 1)) != hipSuccess)
-                return latch(p, e);
-            if ((e = kernel(k)) != hipSuccess) return latch(p, e);
+                return fail(e);
+            if ((e = kernel(k)) != hipSuccess) return fail(e);
             int64_t* flag = nullptr;
             job = submit(k, &flag);
             if (k == 0) first = job;
             if ((e = release_flags(p, flag, nullptr, stream)) != hipSuccess)
                 return fail_held(p, w, stream, &flag, 1, e);
         }
-        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess) return latch(p, e);
+        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess) return fail(e);
     } else {
         int64_t* held[2] = {nullptr, nullptr};
         const uint64_t first = submit(0, &held[0]);
@@ -640,8 +651,8 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
         if ((e = release_flags(p, held[0], held[1], stream)) != hipSuccess)
             return fail_held(p, w, stream, held, 2, e);
         for (uint32_t k = 0; k < K; ++k) {
-            if ((e = w.stream_wait(stream, first + k + 1)) != hipSuccess) return latch(p, e);
-            if ((e = kernel(k)) != hipSuccess) return latch(p, e);
+            if ((e = w.stream_wait(stream, first + k + 1)) != hipSuccess) return fail(e);
+            if ((e = kernel(k)) != hipSuccess) return fail(e);
             if (k + 2 < K) {
                 int64_t* flag = nullptr;
                 (void)submit(k + 2, &flag);
@@ -944,8 +955,11 @@ aqua_status do_migrate(aqua_kv_pool* p, const void* src, uint64_t src_bytes, int
         const uint64_t job = w.submit(copies, &flag);
         hipError_t e = release_flags(p, flag, nullptr, stream);
         if (e != hipSuccess) return fail_held(p, w, stream, &flag, 1, e);
-        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess)
-            return fail_enqueued(stream, latch(p, e));
+        if ((e = w.stream_wait(stream, job + 1)) != hipSuccess) {
+            const aqua_status st = fail_enqueued(stream, latch(p, e));
+            w.wait_published(job + 1);  // the released copies end before the call returns
+            return st;
+        }
     }
     if (dbytes) {
         // Descriptors go to the device ring: a migration touching host
