@@ -823,7 +823,11 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
             st = enqueue_staged(p, is_in, buf, stream, reinterpret_cast<const RunDesc*>(descs),
                                 (uint32_t)p->plan.size(), slot, G, l_begin, l_begin + l_count,
                                 &rec);
-            if (st != AQUA_OK) return fail_enqueued(stream, st);
+            if (st != AQUA_OK) {
+                // The runtime carrier's copies run on the library's copy stream.
+                if (p->copy[is_in]) (void)hipStreamSynchronize(p->copy[is_in]);
+                return fail_enqueued(stream, st);
+            }
         } else {
             const aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
