@@ -134,7 +134,11 @@ typedef struct {
  *              [pool_base, pool_base + pool_bytes) inside one allocation.
  *   pool_bytes >= L*N*C, else AQUA_ERR_CAPACITY.
  *   out        receives the handle; untouched on failure.
- * Allocates the library's own descriptor rings and events. */
+ * Allocates the library's own descriptor rings and events.  The first pool
+ * of a process on a device also launches each of the library's kernels once,
+ * with nothing to copy, on a private stream, and waits for them: the runtime
+ * loads the library's device code then (about 80 ms once), not at the first
+ * swap. */
 AQUA_API aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
                                 uint64_t pool_bytes, aqua_kv_pool_t* out);
 
@@ -265,11 +269,11 @@ AQUA_API aqua_status aqua_kv_pool_set_max_workgroups(aqua_kv_pool_t pool,
  *     aqua_kv_pool_set_link_engine), so a swap-out and a swap-in on
  *     different streams use both directions of the link at once.  The
  *     compute units are busy only for the short gathers and scatters, so
- *     concurrent kernels keep running.  A pool's first staged call also
- *     starts its carrier and allocates the slots: about 160 ms of host time
- *     on MI355X, against well under 1 ms later; a caller that cannot take
- *     that at its first preemption issues one small staged swap-out and
- *     swap-in when it starts.
+ *     concurrent kernels keep running.  A pool's first staged call in each
+ *     direction also sets up that direction's carrier and slots: about 6 ms
+ *     of host time on MI355X, against well under 1 ms later; a caller that
+ *     cannot take that at its first preemption issues one small staged
+ *     swap-out and swap-in when it starts.
  *   AQUA_HOST_ZERO_COPY: the gather and scatter kernels read and write the
  *     host image directly over the link, with no HBM staging.  Their
  *     workgroups stay resident for the whole transfer, so the library caps

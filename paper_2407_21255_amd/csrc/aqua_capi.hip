@@ -9,7 +9,9 @@
 #include <cstring>
 #include <deque>
 #include <map>
+#include <mutex>
 #include <new>
+#include <set>
 #include <vector>
 
 #include "aqua.h"
@@ -388,6 +390,54 @@ hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipS
                        reinterpret_cast<const uint4*>(p->ring_host_dev + ring_off),
                        reinterpret_cast<uint4*>(p->ring_dev + ring_off), n);
     return hipGetLastError();
+}
+
+// Launches each of the library's kernels once with nothing to copy, on a
+// private stream, so that the runtime loads their device code when the
+// first pool of a process is created rather than at its first swap (the
+// first launch in a process took 76 ms, and the first staged call's other
+// kernels 7 ms more).  The one run descriptor and the one range descriptor
+// have no chunks and no bytes, so the swap and range-copy kernels read the
+// descriptor and nothing else; the flag kernel and the upload write only
+// the pool's own, still unused, device ring.
+hipError_t warm_kernels(aqua_kv_pool* p) {
+    static std::mutex mu;
+    static std::set<int> warmed;
+    std::lock_guard<std::mutex> lk(mu);
+    if (warmed.count(p->device)) return hipSuccess;
+    std::memset(p->ring_host, 0, 64);  // a zero RunDesc, read also as a zero CopyDesc
+    hipStream_t s = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+    aqua::SwapLaunch L;
+    L.pool = p->base;
+    L.img = p->base;
+    L.img_l0 = 0;
+    L.descs = reinterpret_cast<const RunDesc*>(p->ring_host_dev);
+    L.ndesc = 1;
+    L.first_layer = 0;
+    L.num_layers = 1;
+    L.chunk_bytes = p->shape.C;
+    L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
+    L.max_workgroups = 0;
+    const bool forms[3][2] = {{true, false}, {false, true}, {false, false}};  // out, nt stores
+    for (const auto& f : forms) {
+        L.out = f[0];
+        L.nt_pool_store = f[1];
+        if (e == hipSuccess) e = aqua::launch_swap(L, s);
+    }
+    if (e == hipSuccess)
+        e = aqua::launch_copy(p->base, p->base,
+                              reinterpret_cast<const aqua::CopyDesc*>(p->ring_host_dev), 1, 0, s);
+    if (e == hipSuccess) e = upload_descs(p, 0, 32, s);
+    if (e == hipSuccess)
+        e = aqua::launch_release_flags(reinterpret_cast<int64_t*>(p->ring_dev + 64), nullptr, s);
+    const hipError_t es = hipStreamSynchronize(s);
+    (void)hipStreamDestroy(s);
+    if (e == hipSuccess) e = es;
+    if (e == hipSuccess) warmed.insert(p->device);
+    (void)hipGetLastError();
+    return e;
 }
 
 // Chooses direction dir's carrier for link copies on its first staged call
@@ -1079,6 +1129,10 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     p->slot_target = env_u64("AQUA_STAGE_SLOT_BYTES", kDefaultSlotBytes);
     p->fail_release_at = env_u64("AQUA_FAIL_RELEASE_AT", ~0ull);
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
+    if (st == AQUA_OK && warm_kernels(p) != hipSuccess) {
+        free_rings(p);
+        st = AQUA_ERR_HIP;
+    }
     if (st != AQUA_OK) {
         delete p;
         return st;
