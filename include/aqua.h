@@ -135,10 +135,12 @@ typedef struct {
  *   pool_bytes >= L*N*C, else AQUA_ERR_CAPACITY.
  *   out        receives the handle; untouched on failure.
  * Allocates the library's own descriptor rings and events.  The first pool
- * of a process on a device also launches each of the library's kernels once,
- * with nothing to copy, on a private stream, and waits for them: the runtime
- * loads the library's device code then (about 80 ms once), not at the first
- * swap. */
+ * of a process on a device also launches one kernel of each of the
+ * library's source files once, with nothing to copy, on a private stream,
+ * and waits for them: the runtime loads the library's device code then
+ * (about 80 ms once), not at the first swap.  (Profiles of a process show
+ * those three dispatches of a few microseconds: a range copy, a descriptor
+ * upload and a flag release.) */
 AQUA_API aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
                                 uint64_t pool_bytes, aqua_kv_pool_t* out);
 

@@ -392,42 +392,26 @@ hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipS
     return hipGetLastError();
 }
 
-// Launches each of the library's kernels once with nothing to copy, on a
-// private stream, so that the runtime loads their device code when the
-// first pool of a process is created rather than at its first swap (the
-// first launch in a process took 76 ms, and the first staged call's other
-// kernels 7 ms more).  The one run descriptor and the one range descriptor
-// have no chunks and no bytes, so the swap and range-copy kernels read the
-// descriptor and nothing else; the flag kernel and the upload write only
-// the pool's own, still unused, device ring.
+// Launches one kernel of each of the library's source files once, with
+// nothing to copy, on a private stream, so that the runtime loads their
+// device code (one code object per source file) when the first pool of a
+// process is created rather than at its first swap (the first launch in a
+// process took 76 ms, and the first staged call's other kernels 7 ms more).
+// The range-copy kernel, which shares its file with the swap kernels, gets
+// one range of no bytes and reads only that descriptor; the flag kernel and
+// the upload write only the pool's own, still unused, device ring.  The
+// swap kernels themselves are not launched, so their dispatches are the
+// caller's alone.
 hipError_t warm_kernels(aqua_kv_pool* p) {
     static std::mutex mu;
     static std::set<int> warmed;
     std::lock_guard<std::mutex> lk(mu);
     if (warmed.count(p->device)) return hipSuccess;
-    std::memset(p->ring_host, 0, 64);  // a zero RunDesc, read also as a zero CopyDesc
+    std::memset(p->ring_host, 0, 64);  // a zero CopyDesc: a range of no bytes
     hipStream_t s = nullptr;
     hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
     if (e != hipSuccess) return e;
-    aqua::SwapLaunch L;
-    L.pool = p->base;
-    L.img = p->base;
-    L.img_l0 = 0;
-    L.descs = reinterpret_cast<const RunDesc*>(p->ring_host_dev);
-    L.ndesc = 1;
-    L.first_layer = 0;
-    L.num_layers = 1;
-    L.chunk_bytes = p->shape.C;
-    L.pool_lstride = (uint64_t)p->shape.N * p->shape.C;
-    L.max_workgroups = 0;
-    const bool forms[3][2] = {{true, false}, {false, true}, {false, false}};  // out, nt stores
-    for (const auto& f : forms) {
-        L.out = f[0];
-        L.nt_pool_store = f[1];
-        if (e == hipSuccess) e = aqua::launch_swap(L, s);
-    }
-    if (e == hipSuccess)
-        e = aqua::launch_copy(p->base, p->base,
+    e = aqua::launch_copy(p->base, p->base,
                               reinterpret_cast<const aqua::CopyDesc*>(p->ring_host_dev), 1, 0, s);
     if (e == hipSuccess) e = upload_descs(p, 0, 32, s);
     if (e == hipSuccess)
