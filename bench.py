@@ -8,9 +8,10 @@ alternate between two disjoint block sets, so every step moves the whole
 payload both ways.  The pool and the offload buffer are resident (HBM, or
 pinned host for the host-target workloads) before the timed region starts.
 
-Prints one JSON line.  The default workload is the Llama-3-8B-shaped pool
-(32 layers, 8 KV heads, head_dim 128, block 16, bf16, 16384 blocks) with 8
-of 16 fragmented 2048-token prompts preempted to an HBM offload region.
+Prints one JSON line.  The default workload is the largest single-GPU
+configuration: the Llama-3-70B-shaped pool (80 layers, 8 KV heads, head_dim
+128, block 16, bf16, 4096 blocks) with one 32768-token prompt (10 GiB each
+way) preempted to an HBM offload region, the long-prompt regime.
 """
 from __future__ import annotations
 
@@ -34,18 +35,31 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 --pmc
 # (FETCH_SIZE, WRITE_SIZE), each scaled by the same counters' reading for a
-# plain copy of known size.  Keyed by the hash of the kernel source they
-# were taken on: a changed kernel reports null until measured again.
+# plain copy of known size.  Keyed by _kernel_hash(): a change to the kernels
+# or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama8b_hbm", "9472d306fd77a2a1"): {
-        "gather (swap-out)": 4295907572, "scatter (swap-in)": 4295784269},
 }
 
+# Every source that decides what the swap kernels do and how they are
+# launched: the kernels, the per-launch store rule, the workgroup size and
+# grid rules, the run planning (unit size) and the launch set-up.
+KERNEL_SOURCES = ("swap_kernels.hip", "swap_kernels.h", "aqua_core.h", "aqua_core.cpp",
+                  "aqua_capi.hip")
+# Run-time settings that change the launches.
+KERNEL_ENV = ("AQUA_UNIT_BYTES", "AQUA_RING_BYTES", "AQUA_STAGE_SLOT_BYTES")
 
-def _kernel_hash() -> str:
-    p = os.path.join(ROOT, "paper_2407_21255_amd", "csrc", "swap_kernels.hip")
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+def _kernel_hash(root: str = ROOT, max_workgroups: int = 0) -> str:
+    """Hash of the launch-defining sources and settings (16 hex digits)."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(name.encode() + b"\0")
+        h.update(open(os.path.join(root, "paper_2407_21255_amd", "csrc", name), "rb").read())
+    for name in KERNEL_ENV:
+        h.update(f"{name}={os.environ.get(name, '')}\0".encode())
+    h.update(f"max_workgroups={max_workgroups}".encode())
+    return h.hexdigest()[:16]
 
 
 WORKLOADS = {
@@ -343,7 +357,7 @@ def run_pair(args, res_common):
     else:
         bound, peak, alg = "hbm", HBM_PEAK_GBS, 2 * payload
     achieved = alg / (dom_ms.mean() * 1e-3) / 1e9
-    khash = _kernel_hash()
+    khash = _kernel_hash(max_workgroups=args.max_workgroups)
     res = dict(res_common)
     res.update({
         "value": round(value, 2),
@@ -398,7 +412,38 @@ def run_pair(args, res_common):
             "swap_out_vs_runtime_copy": round(2 * res["swap_out_GBps"] / copy_gbs, 4),
             "swap_in_vs_runtime_copy": round(2 * res["swap_in_GBps"] / copy_gbs, 4),
         }
+        res["hbm_ceiling"] = hbm_ceiling(img, pool[:payload])
+        cp = res["hbm_ceiling"]["copy_GBps"]
+        res["hbm_ceiling"]["swap_out_vs_copy"] = round(2 * res["swap_out_GBps"] / cp, 4)
+        res["hbm_ceiling"]["swap_in_vs_copy"] = round(2 * res["swap_in_GBps"] / cp, 4)
     return res, s
+
+
+def hbm_ceiling(dst, src, reps: int = 5) -> dict:
+    """Same-run HBM yardsticks of the payload's size with the library's own
+    copy loop (aqua_hbm_yardstick): a contiguous copy (GB/s of read + write
+    traffic), a pure read and a pure write, each timed with HIP events on
+    its launch stream after one untimed pass; each as a share of 8 TB/s."""
+    import torch
+
+    from paper_2407_21255_amd import aqua
+    nbytes = src.numel()
+    stream = torch.cuda.Stream()
+    out = {"bytes": nbytes}
+    for name, kind, traffic in (("copy", aqua.AQUA_YARDSTICK_COPY, 2 * nbytes),
+                                ("read", aqua.AQUA_YARDSTICK_READ, nbytes),
+                                ("write", aqua.AQUA_YARDSTICK_WRITE, nbytes)):
+        aqua.hbm_yardstick(kind, dst, src, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            aqua.hbm_yardstick(kind, dst, src, stream=stream)
+        e1.record(stream)
+        stream.synchronize()
+        gbs = traffic * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        out[f"{name}_GBps"] = round(gbs, 1)
+        out[f"{name}_frac"] = round(gbs / HBM_PEAK_GBS, 4)
+    return out
 
 
 def runtime_copy_rate(dst, src, reps: int = 5) -> float:
@@ -994,7 +1039,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama8b_hbm", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="llama70b_hbm", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm", action="store_true",

@@ -329,6 +329,32 @@ AQUA_API aqua_status aqua_pool_stats_get(aqua_kv_pool_t pool, aqua_pool_stats* o
 /* Static text for a status code. */
 AQUA_API const char* aqua_status_str(aqua_status s);
 
+/* ---- HBM yardsticks (measurement helper, no pool).
+ *
+ * The swap kernels' roofline is HBM bandwidth, read plus write (a swap with
+ * an HBM offload target reads and writes every payload byte once).  These
+ * calls run the swap kernels' own copy loop -- 64 KiB per 1024-lane
+ * workgroup, four 16-byte vectors per lane in flight, nontemporal hints --
+ * over one contiguous range, so that a caller can measure, in the same run
+ * and on the same device, what a copy, a pure read and a pure write reach:
+ *   AQUA_YARDSTICK_COPY   copies bytes from src to dst (ranges disjoint);
+ *   AQUA_YARDSTICK_READ   reads bytes of src; dst (16 bytes at least) is
+ *                         not written for any input a caller can give
+ *                         (the loads are folded and stored only if the fold
+ *                         equals an internal key);
+ *   AQUA_YARDSTICK_WRITE  writes bytes of dst: 16-byte vector i holds the
+ *                         32-bit words {i mod 2^32, i / 2^32, 0x9E3779B9,
+ *                         0x61C88646}; src is not read and may be NULL.
+ * src and dst are device memory of the current device, 16-byte aligned,
+ * each range inside one allocation; bytes is a multiple of 16 (0: nothing
+ * is enqueued).  The work is enqueued on `stream` (NULL: the null stream)
+ * and the call returns without waiting.  AQUA_ERR_INVALID for another kind,
+ * a misaligned or foreign pointer, a range outside its allocation or
+ * overlapping copy ranges; AQUA_ERR_HIP if the launch fails. */
+enum { AQUA_YARDSTICK_COPY = 0, AQUA_YARDSTICK_READ = 1, AQUA_YARDSTICK_WRITE = 2 };
+AQUA_API aqua_status aqua_hbm_yardstick(int32_t kind, void* dst, const void* src,
+                                        uint64_t bytes, void* stream);
+
 /* ---- Swap space: offload tensors with a device region and a host fallback
  * (section 6, "Aqua Tensors", "Allocating Aqua Tensors", "Reclaiming Aqua
  * Tensors").

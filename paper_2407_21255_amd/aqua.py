@@ -33,6 +33,7 @@ AQUA_F16, AQUA_BF16, AQUA_FP8_E4M3 = 1, 2, 3
 AQUA_TARGET_DEVICE, AQUA_TARGET_HOST = 0, 1
 AQUA_HOST_ZERO_COPY, AQUA_HOST_STAGED = 0, 1
 AQUA_LINK_RUNTIME, AQUA_LINK_AUTO = -1, -2
+AQUA_YARDSTICK_COPY, AQUA_YARDSTICK_READ, AQUA_YARDSTICK_WRITE = 0, 1, 2
 
 EXPORTS = (
     "aqua_kv_pool_create", "aqua_kv_pool_destroy", "aqua_swap_out",
@@ -43,6 +44,7 @@ EXPORTS = (
     "aqua_pool_stats_get", "aqua_status_str", "aqua_cfs_partition",
     "aqua_swap_space_create", "aqua_swap_space_destroy", "aqua_swap_alloc", "aqua_swap_free",
     "aqua_swap_locate", "aqua_swap_reclaim", "aqua_swap_restore", "aqua_swap_usage",
+    "aqua_hbm_yardstick",
 )
 
 
@@ -133,6 +135,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_swap_reclaim.argtypes = [P, u64, P, ctypes.POINTER(u64)]
     L.aqua_swap_restore.argtypes = [P, P, ctypes.POINTER(u64)]
     L.aqua_swap_usage.argtypes = [P] + [ctypes.POINTER(u64)] * 4
+    L.aqua_hbm_yardstick.argtypes = [i32, P, P, u64, P]
     L.aqua_status_str.argtypes = [i32]
     L.aqua_status_str.restype = ctypes.c_char_p
     for n in EXPORTS:
@@ -229,6 +232,23 @@ def aqua_pool_stats_get(pool):
     s = aqua_pool_stats()
     st = load().aqua_pool_stats_get(pool, ctypes.byref(s))
     return st, s
+
+
+def aqua_hbm_yardstick(kind: int, dst, src, nbytes: int, stream) -> int:
+    return load().aqua_hbm_yardstick(kind, dst, src, nbytes, stream)
+
+
+def hbm_yardstick(kind: int, dst: torch.Tensor, src: Optional[torch.Tensor] = None,
+                  stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueues one HBM yardstick pass (AQUA_YARDSTICK_COPY / _READ / _WRITE)
+    over src's bytes (dst's for a write) on ``stream``; raises AquaError on
+    a failed call."""
+    nbytes = (src if kind != AQUA_YARDSTICK_WRITE else dst).numel() * \
+        (src if kind != AQUA_YARDSTICK_WRITE else dst).element_size()
+    st = aqua_hbm_yardstick(kind, dst.data_ptr(), src.data_ptr() if src is not None else None,
+                            nbytes, stream.cuda_stream if stream is not None else None)
+    if st != AQUA_OK:
+        raise AquaError(st, "aqua_hbm_yardstick")
 
 
 def aqua_status_str(status: int) -> str:

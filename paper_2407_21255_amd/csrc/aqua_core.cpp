@@ -166,6 +166,22 @@ size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
     return out->size() - before;
 }
 
+uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
+    uint32_t lo = 64;
+    while (lo < min_threads && lo < kMaxThreads) lo *= 2;
+    uint32_t t = lo;
+    const uint64_t want = chunk_bytes / (16ull * kUnroll);  // lanes for one pass
+    while (t < kMaxThreads && t < want) t *= 2;
+    return t;
+}
+
+uint32_t launch_grid(uint64_t units, uint32_t max_workgroups) {
+    uint64_t g = units;
+    if (max_workgroups && g > max_workgroups) g = max_workgroups;
+    if (g > kMaxGrid) g = kMaxGrid;
+    return (uint32_t)g;
+}
+
 aqua_status validate_migrate(uintptr_t src, uint64_t src_bytes, uintptr_t dst,
                              uint64_t dst_bytes, uint32_t n, const uint64_t* src_off,
                              const uint64_t* dst_off, const uint64_t* len) {
@@ -218,25 +234,55 @@ void HazardTracker::reset(uint32_t num_blocks) {
     readers_.assign(num_blocks, {});
     ranges_.clear();
     done_.clear();
+    last_.clear();
     dep_.clear();
-    ticket_lane_.assign(1, 0);
+    ticket_lane_.clear();
+    base_ = 1;
     last_ticket_ = 0;
 }
 
 void HazardTracker::ensure_lane(uint32_t lane) {
     if (lane >= done_.size()) {
         done_.resize(lane + 1, 0);
+        last_.resize(lane + 1, 0);
         dep_.resize(lane + 1, 0);
     }
 }
 
+// Drops the lanes of the oldest tickets while they are complete.
+void HazardTracker::prune() {
+    while (!ticket_lane_.empty()) {
+        const uint32_t m = ticket_lane_.front();
+        if (m != kNoLane && base_ > done_[m]) break;
+        ticket_lane_.pop_front();
+        ++base_;
+    }
+}
+
+bool HazardTracker::idle(uint32_t lane) const {
+    return lane >= done_.size() || done_[lane] >= last_[lane];
+}
+
+uint32_t LaneMap::lane_for(uintptr_t stream, const HazardTracker& t) {
+    for (uint32_t m = 0; m < stream_.size(); ++m)
+        if (stream_[m] == stream) return m;
+    for (uint32_t m = 0; m < stream_.size(); ++m)
+        if (t.idle(m)) {
+            stream_[m] = stream;
+            return m;
+        }
+    stream_.push_back(stream);
+    return (uint32_t)(stream_.size() - 1);
+}
+
 uint32_t HazardTracker::lane_of(uint64_t ticket) const {
-    return ticket < ticket_lane_.size() ? ticket_lane_[ticket] : 0;
+    if (ticket < base_ || ticket - base_ >= ticket_lane_.size()) return kNoLane;
+    const uint32_t m = ticket_lane_[ticket - base_];
+    return (m != kNoLane && ticket > done_[m]) ? m : kNoLane;
 }
 
 bool HazardTracker::done(uint64_t ticket) const {
-    const uint32_t m = lane_of(ticket);
-    return ticket <= done_[m];
+    return lane_of(ticket) == kNoLane;
 }
 
 uint64_t HazardTracker::completed(uint32_t lane) const {
@@ -246,15 +292,16 @@ uint64_t HazardTracker::completed(uint32_t lane) const {
 void HazardTracker::complete(uint32_t lane, uint64_t ticket) {
     ensure_lane(lane);
     if (ticket > done_[lane]) done_[lane] = ticket;
+    prune();
 }
 
 void HazardTracker::need(uint64_t ticket, uint32_t lane, uint64_t* elided) {
     if (!ticket) return;
-    if (done(ticket)) {
+    const uint32_t m = lane_of(ticket);
+    if (m == kNoLane) {  // known complete
         ++*elided;
         return;
     }
-    const uint32_t m = lane_of(ticket);
     if (m == lane) return;  // same stream: ordered by the stream itself
     if (ticket > dep_[m]) dep_[m] = ticket;
 }
@@ -264,8 +311,10 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
     ensure_lane(lane);
     deps->clear();
     std::fill(dep_.begin(), dep_.end(), 0);
-    if (ticket_lane_.size() <= ticket) ticket_lane_.resize(ticket + 1, 0);
-    ticket_lane_[ticket] = lane;
+    // Tickets skipped since the last issue were never issued: complete.
+    while (base_ + ticket_lane_.size() < ticket) ticket_lane_.push_back(kNoLane);
+    ticket_lane_.push_back(lane);
+    last_[lane] = ticket;
     last_ticket_ = ticket;
     uint64_t elided = 0;
 

@@ -6,6 +6,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <deque>
 #include <map>
 #include <utility>
 #include <vector>
@@ -91,6 +92,24 @@ struct alignas(16) RunDesc {
 };
 static_assert(sizeof(RunDesc) == 32, "descriptor layout is shared with the kernels");
 
+// Launch geometry of the copy kernels.  Every lane moves kUnroll 16-byte
+// vectors per pass, so a workgroup of `threads` lanes has threads * 64 bytes
+// in flight.  A workgroup is sized to the chunk: 1024 lanes for chunks of
+// 64 KiB and more, fewer for smaller chunks (down to min_threads, a power
+// of two of at least 64), so that every lane still issues kUnroll loads
+// before its first store.
+constexpr uint32_t kUnroll = 4;
+constexpr uint32_t kMaxThreads = 1024;
+uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads);
+
+// Workgroups of one launch over `units` work units: one per unit, at most
+// `max_workgroups` when that is non-zero, and never more than kMaxGrid.  A
+// dispatch counts its work-items in 32 bits, so 1024-lane workgroups allow
+// at most 4 194 303 of them; the kernels loop over units with a grid
+// stride, so a capped grid still covers every unit.
+constexpr uint32_t kMaxGrid = 1u << 21;
+uint32_t launch_grid(uint64_t units, uint32_t max_workgroups);
+
 // Reusable scratch for duplicate detection (epoch-stamped marks, O(n)).
 struct DupMarks {
     std::vector<uint32_t> mark;
@@ -125,6 +144,11 @@ void image_ranges(const Shape& s, const CallArgs& a,
 // writing ticket and, per lane, the newest ticket reading it since that
 // write; per offload byte range it keeps the in-flight readers and writers.
 // Tickets known complete (per-lane watermark) are never waited on.
+//
+// Memory stays bounded however many calls are issued: the lane of a ticket
+// is kept only from the oldest ticket not yet known complete onwards (every
+// older ticket is complete, whatever its lane), and a lane whose tickets
+// have all completed can be handed to another stream (LaneMap).
 class HazardTracker {
 public:
     struct Dep {
@@ -159,9 +183,21 @@ public:
     // Everything on `lane` up to and including `ticket` has completed.
     void complete(uint32_t lane, uint64_t ticket);
     uint64_t completed(uint32_t lane) const;
+    // Lane of an issued ticket that is not yet known complete; kNoLane for a
+    // ticket already known complete (or never issued).
+    static constexpr uint32_t kNoLane = UINT32_MAX;
     uint32_t lane_of(uint64_t ticket) const;
+    // Known complete: below the oldest outstanding ticket, or at or below
+    // its lane's watermark.
+    bool done(uint64_t ticket) const;
+    // Every ticket issued on `lane` is known complete.
+    bool idle(uint32_t lane) const;
     size_t live_ranges() const { return ranges_.size(); }
     uint64_t last_ticket() const { return last_ticket_; }
+    // Tickets whose lane is still kept (from the oldest one not known
+    // complete to the newest) and lanes known to the tracker.
+    size_t tickets_kept() const { return ticket_lane_.size(); }
+    size_t lanes() const { return done_.size(); }
 
 private:
     struct Reader {
@@ -174,16 +210,32 @@ private:
         bool write;
     };
     void ensure_lane(uint32_t lane);
-    bool done(uint64_t ticket) const;
+    void prune();
     void need(uint64_t ticket, uint32_t lane, uint64_t* elided);
 
     std::vector<uint64_t> last_writer_;
     std::vector<std::vector<Reader>> readers_;
     std::vector<RangeRec> ranges_;
     std::vector<uint64_t> done_;        // per lane watermark
+    std::vector<uint64_t> last_;        // per lane, newest ticket issued on it
     std::vector<uint64_t> dep_;         // per lane, scratch of one issue()
-    std::vector<uint32_t> ticket_lane_; // index: ticket
+    std::deque<uint32_t> ticket_lane_;  // lanes of tickets base_, base_ + 1, ...
+    uint64_t base_ = 1;                 // every ticket below is complete
     uint64_t last_ticket_ = 0;
+};
+
+// Stream -> lane map of one pool.  A stream seen before keeps its lane; a
+// new stream takes over the lowest lane that is idle in the tracker (every
+// ticket issued on it complete), else a new lane, so the lane count is at
+// most the number of streams with calls in flight at once, plus one.
+class LaneMap {
+public:
+    uint32_t lane_for(uintptr_t stream, const HazardTracker& t);
+    size_t size() const { return stream_.size(); }
+    uintptr_t stream_of(uint32_t lane) const { return stream_[lane]; }
+
+private:
+    std::vector<uintptr_t> stream_;
 };
 
 // First-fit allocator of byte ranges inside one arena [0, size) (the swap

@@ -1,6 +1,7 @@
 // core_testapi.cpp -- C entry points into the host core for CPU tests.
 // Built into a separate library (libaqua_core.so) with the system C++
 // compiler; the GPU library does not contain these symbols.
+#include <algorithm>
 #include <cstring>
 #include <vector>
 
@@ -174,6 +175,87 @@ void aqua_core_tracker_complete(void* t, uint32_t lane, uint64_t ticket) {
 
 uint64_t aqua_core_tracker_live_ranges(void* t) {
     return static_cast<aqua::HazardTracker*>(t)->live_ranges();
+}
+
+uint64_t aqua_core_tracker_tickets_kept(void* t) {
+    return static_cast<aqua::HazardTracker*>(t)->tickets_kept();
+}
+
+uint64_t aqua_core_tracker_lanes(void* t) {
+    return static_cast<aqua::HazardTracker*>(t)->lanes();
+}
+
+int aqua_core_tracker_done(void* t, uint64_t ticket) {
+    return static_cast<aqua::HazardTracker*>(t)->done(ticket) ? 1 : 0;
+}
+
+void* aqua_core_lanes_new() { return new aqua::LaneMap(); }
+void aqua_core_lanes_free(void* m) { delete static_cast<aqua::LaneMap*>(m); }
+uint32_t aqua_core_lanes_lane_for(void* m, uint64_t stream, void* t) {
+    return static_cast<aqua::LaneMap*>(m)->lane_for(
+        (uintptr_t)stream, *static_cast<aqua::HazardTracker*>(t));
+}
+uint64_t aqua_core_lanes_size(void* m) { return static_cast<aqua::LaneMap*>(m)->size(); }
+
+// A serving loop in miniature, for the memory bound of the tracker: n_calls
+// swaps (alternately out and in, 8 blocks each, of a num_blocks pool) on
+// streams drawn round-robin from a set of `streams` handles that is replaced
+// by new handles every `rotate` calls; at most `depth` calls are in flight
+// (the oldest completes first).  Writes the largest number of tickets whose
+// lane the tracker kept, and of lanes, seen after any call.
+void aqua_core_tracker_soak(uint64_t n_calls, uint32_t num_blocks, uint32_t streams,
+                            uint64_t rotate, uint32_t depth, uint64_t* max_kept,
+                            uint64_t* max_lanes) {
+    aqua::HazardTracker tr(num_blocks);
+    aqua::LaneMap lanes;
+    std::vector<std::pair<uint32_t, uint64_t>> fifo;  // (lane, ticket), oldest first
+    size_t head = 0;
+    std::vector<aqua::HazardTracker::Dep> deps;
+    std::vector<int32_t> blocks(8);
+    const std::pair<uint64_t, uint64_t> range{0, 4096};
+    *max_kept = *max_lanes = 0;
+    for (uint64_t i = 0; i < n_calls; ++i) {
+        const uint64_t ticket = i + 1;
+        const uintptr_t stream = 0x1000 + (i / rotate) * streams + i % streams;
+        const uint32_t lane = lanes.lane_for(stream, tr);
+        for (uint32_t j = 0; j < 8; ++j)
+            blocks[j] = (int32_t)((i * 8 + j) * 2654435761ull % num_blocks);
+        aqua::HazardTracker::Access acc;
+        std::pair<uint64_t, uint64_t> r = range;
+        r.first += (i % 64) * 4096;
+        r.second += (i % 64) * 4096;
+        if (i % 2) {
+            acc.blocks_written = blocks.data();  // distinct: 8 consecutive multiples
+            acc.n_blocks_written = 8;
+            acc.ranges_read = &r;
+            acc.n_ranges_read = 1;
+        } else {
+            acc.blocks_read = blocks.data();
+            acc.n_blocks_read = 8;
+            acc.ranges_written = &r;
+            acc.n_ranges_written = 1;
+        }
+        tr.issue(ticket, lane, acc, &deps);
+        fifo.emplace_back(lane, ticket);
+        while (fifo.size() - head > depth) {
+            tr.complete(fifo[head].first, fifo[head].second);
+            ++head;
+        }
+        if (head > 4096) {
+            fifo.erase(fifo.begin(), fifo.begin() + head);
+            head = 0;
+        }
+        *max_kept = std::max<uint64_t>(*max_kept, tr.tickets_kept());
+        *max_lanes = std::max<uint64_t>(*max_lanes, std::max(tr.lanes(), lanes.size()));
+    }
+}
+
+uint32_t aqua_core_swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
+    return aqua::swap_threads(chunk_bytes, min_threads);
+}
+
+uint32_t aqua_core_launch_grid(uint64_t units, uint32_t max_workgroups) {
+    return aqua::launch_grid(units, max_workgroups);
 }
 
 void aqua_core_pick_link_engines(uint32_t d2h_avail, uint32_t d2h_pref, uint32_t h2d_avail,

@@ -22,6 +22,7 @@ struct SwapLaunch {
     uint64_t pool_lstride;    // N * C
     uint32_t max_workgroups;  // 0: one workgroup per (layer, run)
     bool nt_pool_store;       // scatter: nontemporal stores into the pool
+    uint32_t threads;         // lanes per workgroup: 64, 128, 256, 512 or 1024
 };
 
 // Scatter store hint, measured on MI355X.  Nontemporal pool stores pay for
@@ -39,6 +40,12 @@ inline bool nt_pool_store(uint64_t chunk_bytes, uint64_t launch_bytes) {
 
 // Enqueues the copy on `stream`; returns the first launch error.
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream);
+
+// Enqueues one HBM yardstick over `bytes` (a multiple of 16) of device
+// memory with the swap kernels' copy loop: mode 0 copies src to dst, mode 1
+// reads src only, mode 2 writes dst only (see aqua_hbm_yardstick).
+hipError_t launch_yardstick(int mode, const uint8_t* src, uint8_t* dst, uint64_t bytes,
+                            uint32_t key, hipStream_t stream);
 
 // Enqueues the range copy of `n` pieces (each at most 64 KiB, 16-byte
 // multiples) from `src` to `dst`, both device-accessible addresses.

@@ -2,10 +2,15 @@
 //
 // The work is pure data movement (Aqua, section 7, "Efficient context
 // switching"): no arithmetic on the values, so no MFMA and no LDS.  Each
-// workgroup of 1024 lanes (16 wave64s) copies one run of chunks of one
-// layer; every lane moves 16-byte vectors, a wave covers 1 KiB contiguous
-// per instruction, and UNROLL = 4 independent loads are issued before the
-// first store, so a workgroup has 64 KiB -- one bf16 chunk -- in flight.
+// workgroup copies one run of chunks of one layer at a time; every lane
+// moves 16-byte vectors, a wave covers 1 KiB contiguous per instruction,
+// and kUnroll = 4 independent loads are issued before the first store, so a
+// workgroup of 1024 lanes (16 wave64s) holds one 64 KiB bf16 chunk in flight.
+// The kernels also come in 512, 256, 128 and 64 lanes, so that a launch can
+// size the workgroup to a smaller chunk and keep kUnroll loads in flight
+// per lane; on MI355X that measured no faster for 32 KiB chunks and 4 %
+// slower for 16 KiB ones than 1024 lanes with idle lanes in the last pass,
+// so the library launches 1024 lanes by default (swap_threads).
 // The run descriptor is uniform across the workgroup and is fetched with
 // scalar loads.  The offload side is written (swap-out) or read (swap-in) with
 // nontemporal hints: it is touched once and should not displace the pool's
@@ -26,15 +31,8 @@ namespace {
 
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
-// Launch shape and cache hints.  The defaults are the shipped
-// configuration; the macros exist so that measurement sweeps can build
-// variants.
-#ifndef AQUA_THREADS
-#define AQUA_THREADS 1024
-#endif
-#ifndef AQUA_UNROLL
-#define AQUA_UNROLL 4
-#endif
+// Cache hints.  The defaults are the shipped configuration; the macros
+// exist so that measurement sweeps can build variants.
 #ifndef AQUA_NT_OUT_LD   // swap-out: pool loads
 #define AQUA_NT_OUT_LD 1
 #endif
@@ -46,9 +44,6 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #endif
 // Swap-in pool stores: nontemporal or not is chosen per launch
 // (SwapLaunch::nt_pool_store).
-
-constexpr int kThreads = AQUA_THREADS;
-constexpr int kUnroll = AQUA_UNROLL;
 
 template <bool NT>
 __device__ __forceinline__ v4u ld(const v4u* p) {
@@ -62,30 +57,33 @@ __device__ __forceinline__ void st(v4u* p, v4u v) {
     else *p = v;
 }
 
-// Copies nvec 16-byte vectors from s to d with the whole workgroup.
-template <int UNROLL, bool NT_LD, bool NT_ST>
+// Copies nvec 16-byte vectors from s to d with the whole workgroup of
+// THREADS lanes: full passes of THREADS * kUnroll vectors, then one partial
+// pass in which a lane loads only those of its kUnroll vectors that fall
+// inside the span, all before its first store.
+template <int THREADS, bool NT_LD, bool NT_ST>
 __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
                                           v4u* __restrict__ d, uint32_t nvec) {
     const uint32_t t = threadIdx.x;
-    constexpr uint32_t step = kThreads * UNROLL;
+    constexpr uint32_t step = THREADS * kUnroll;
     uint32_t base = 0;
     for (; base + step <= nvec; base += step) {
-        v4u r[UNROLL];
+        v4u r[kUnroll];
 #pragma unroll
-        for (int j = 0; j < UNROLL; ++j) r[j] = ld<NT_LD>(s + base + j * kThreads + t);
+        for (int j = 0; j < (int)kUnroll; ++j) r[j] = ld<NT_LD>(s + base + j * THREADS + t);
 #pragma unroll
-        for (int j = 0; j < UNROLL; ++j) st<NT_ST>(d + base + j * kThreads + t, r[j]);
+        for (int j = 0; j < (int)kUnroll; ++j) st<NT_ST>(d + base + j * THREADS + t, r[j]);
     }
-    if (base < nvec) {  // ragged tail, still UNROLL loads in flight
-        v4u r[UNROLL];
+    if (base < nvec) {
+        v4u r[kUnroll];
 #pragma unroll
-        for (int j = 0; j < UNROLL; ++j) {
-            const uint32_t i = base + j * kThreads + t;
+        for (int j = 0; j < (int)kUnroll; ++j) {
+            const uint32_t i = base + j * THREADS + t;
             if (i < nvec) r[j] = ld<NT_LD>(s + i);
         }
 #pragma unroll
-        for (int j = 0; j < UNROLL; ++j) {
-            const uint32_t i = base + j * kThreads + t;
+        for (int j = 0; j < (int)kUnroll; ++j) {
+            const uint32_t i = base + j * THREADS + t;
             if (i < nvec) st<NT_ST>(d + i, r[j]);
         }
     }
@@ -98,8 +96,8 @@ __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
 // (0 for whole images, the first staged layer for a staging slot);
 // consecutive workgroups take consecutive runs of one layer, so the image
 // side of a gather is written front to back.
-template <bool OUT, int UNROLL, bool NT_POOL_ST>
-__global__ __launch_bounds__(kThreads) void swap_runs_kernel(
+template <bool OUT, bool NT_POOL_ST, int THREADS>
+__global__ __launch_bounds__(THREADS) void swap_runs_kernel(
     uint8_t* __restrict__ pool, uint8_t* __restrict__ img,
     const RunDesc* __restrict__ descs, uint32_t ndesc, uint32_t l0, uint32_t img_l0,
     uint32_t units, uint64_t chunk_bytes, uint64_t pool_lstride) {
@@ -111,26 +109,82 @@ __global__ __launch_bounds__(kThreads) void swap_runs_kernel(
         uint8_t* m = img + dsc.img_off + (uint64_t)(l - img_l0) * dsc.img_lstride;
         const uint32_t nvec = (uint32_t)((uint64_t)dsc.nchunks * chunk_bytes / 16);
         if constexpr (OUT)
-            copy_span<UNROLL, AQUA_NT_OUT_LD, AQUA_NT_OUT_ST>(
+            copy_span<THREADS, AQUA_NT_OUT_LD, AQUA_NT_OUT_ST>(
                 reinterpret_cast<const v4u*>(p), reinterpret_cast<v4u*>(m), nvec);
         else
-            copy_span<UNROLL, AQUA_NT_IN_LD, NT_POOL_ST>(
+            copy_span<THREADS, AQUA_NT_IN_LD, NT_POOL_ST>(
                 reinterpret_cast<const v4u*>(m), reinterpret_cast<v4u*>(p), nvec);
     }
 }
 
 // Range copy between two offload buffers (image migration): work unit u
 // copies descs[u].len bytes from src + src_off to dst + dst_off.
-template <int UNROLL>
-__global__ __launch_bounds__(kThreads) void copy_ranges_kernel(
+__global__ __launch_bounds__(kMaxThreads) void copy_ranges_kernel(
     const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
     const CopyDesc* __restrict__ descs, uint32_t n) {
     for (uint32_t u = blockIdx.x; u < n; u += gridDim.x) {
         const CopyDesc dsc = descs[u];
-        copy_span<UNROLL, true, true>(reinterpret_cast<const v4u*>(src + dsc.src_off),
-                                      reinterpret_cast<v4u*>(dst + dsc.dst_off),
-                                      (uint32_t)(dsc.len / 16));
+        copy_span<kMaxThreads, true, true>(reinterpret_cast<const v4u*>(src + dsc.src_off),
+                                           reinterpret_cast<v4u*>(dst + dsc.dst_off),
+                                           (uint32_t)(dsc.len / 16));
     }
+}
+
+// HBM yardsticks over nvec contiguous vectors, in 64 KiB pieces with the
+// swap kernels' lane shape and hints.  MODE 0 copies src to dst, MODE 1 only
+// reads src (the vectors are folded together and stored to dst only if the
+// fold equals a key no real input produces, so the loads stay), MODE 2 only
+// writes dst: vector i holds {i low, i high, key, ~key}.
+template <int MODE>
+__global__ __launch_bounds__(kMaxThreads) void yardstick_kernel(
+    const v4u* __restrict__ src, v4u* __restrict__ dst, uint64_t nvec, uint32_t key) {
+    constexpr uint32_t per = kMaxThreads * kUnroll;
+    const uint64_t units = (nvec + per - 1) / per;
+    const uint32_t t = threadIdx.x;
+    v4u acc = {0u, 0u, 0u, 0u};
+    for (uint64_t u = blockIdx.x; u < units; u += gridDim.x) {
+        const uint64_t base = u * per;
+        const uint32_t n = (uint32_t)std::min<uint64_t>(per, nvec - base);
+        if constexpr (MODE == 0) {
+            copy_span<kMaxThreads, true, true>(src + base, dst + base, n);
+        } else if constexpr (MODE == 1) {
+            v4u r[kUnroll];
+#pragma unroll
+            for (int j = 0; j < (int)kUnroll; ++j) {
+                const uint32_t i = j * kMaxThreads + t;
+                r[j] = i < n ? ld<true>(src + base + i) : v4u{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int j = 0; j < (int)kUnroll; ++j) acc ^= r[j];
+        } else {
+#pragma unroll
+            for (int j = 0; j < (int)kUnroll; ++j) {
+                const uint32_t i = j * kMaxThreads + t;
+                const uint64_t g = base + i;
+                if (i < n) st<true>(dst + g, v4u{(uint32_t)g, (uint32_t)(g >> 32), key, ~key});
+            }
+        }
+    }
+    if constexpr (MODE == 1) {
+        if (acc.x == key && acc.y == ~key && acc.z == key && acc.w == ~key) dst[0] = acc;
+    }
+}
+
+template <int THREADS>
+void launch_swap_t(const SwapLaunch& a, uint32_t grid, uint32_t l0, uint32_t units,
+                   hipStream_t stream) {
+    if (a.out)
+        hipLaunchKernelGGL((swap_runs_kernel<true, false, THREADS>), dim3(grid), dim3(THREADS),
+                           0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
+                           a.chunk_bytes, a.pool_lstride);
+    else if (a.nt_pool_store)
+        hipLaunchKernelGGL((swap_runs_kernel<false, true, THREADS>), dim3(grid), dim3(THREADS),
+                           0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
+                           a.chunk_bytes, a.pool_lstride);
+    else
+        hipLaunchKernelGGL((swap_runs_kernel<false, false, THREADS>), dim3(grid), dim3(THREADS),
+                           0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
+                           a.chunk_bytes, a.pool_lstride);
 }
 
 }  // namespace
@@ -138,10 +192,8 @@ __global__ __launch_bounds__(kThreads) void copy_ranges_kernel(
 hipError_t launch_copy(const uint8_t* src, uint8_t* dst, const CopyDesc* descs, uint32_t n,
                        uint32_t max_workgroups, hipStream_t stream) {
     if (!n) return hipSuccess;
-    uint32_t grid = n;
-    if (max_workgroups && grid > max_workgroups) grid = max_workgroups;
-    hipLaunchKernelGGL((copy_ranges_kernel<kUnroll>), dim3(grid), dim3(kThreads), 0, stream,
-                       src, dst, descs, n);
+    hipLaunchKernelGGL(copy_ranges_kernel, dim3(launch_grid(n, max_workgroups)),
+                       dim3(kMaxThreads), 0, stream, src, dst, descs, n);
     return hipGetLastError();
 }
 
@@ -153,24 +205,39 @@ hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
     for (uint32_t l0 = a.first_layer; l0 < end; l0 += per) {
         const uint32_t nl = std::min<uint32_t>(per, end - l0);
         const uint32_t units = nl * a.ndesc;
-        uint32_t grid = units;
-        if (a.max_workgroups && grid > a.max_workgroups) grid = a.max_workgroups;
-        if (a.out)
-            hipLaunchKernelGGL((swap_runs_kernel<true, kUnroll, false>), dim3(grid),
-                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
-                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
-        else if (a.nt_pool_store)
-            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll, true>), dim3(grid),
-                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
-                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
-        else
-            hipLaunchKernelGGL((swap_runs_kernel<false, kUnroll, false>), dim3(grid),
-                               dim3(kThreads), 0, stream, a.pool, a.img, a.descs, a.ndesc, l0,
-                               a.img_l0, units, a.chunk_bytes, a.pool_lstride);
+        const uint32_t grid = launch_grid(units, a.max_workgroups);
+        switch (a.threads) {
+            case 1024: launch_swap_t<1024>(a, grid, l0, units, stream); break;
+            case 512: launch_swap_t<512>(a, grid, l0, units, stream); break;
+            case 256: launch_swap_t<256>(a, grid, l0, units, stream); break;
+            case 128: launch_swap_t<128>(a, grid, l0, units, stream); break;
+            case 64: launch_swap_t<64>(a, grid, l0, units, stream); break;
+            default: return hipErrorInvalidValue;
+        }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_yardstick(int mode, const uint8_t* src, uint8_t* dst, uint64_t bytes,
+                            uint32_t key, hipStream_t stream) {
+    const uint64_t nvec = bytes / 16;
+    if (!nvec) return hipSuccess;
+    const uint64_t per = (uint64_t)kMaxThreads * kUnroll;
+    const uint32_t grid = launch_grid((nvec + per - 1) / per, 0);
+    const v4u* s = reinterpret_cast<const v4u*>(src);
+    v4u* d = reinterpret_cast<v4u*>(dst);
+    switch (mode) {
+        case 0: hipLaunchKernelGGL(yardstick_kernel<0>, dim3(grid), dim3(kMaxThreads), 0, stream,
+                                   s, d, nvec, key); break;
+        case 1: hipLaunchKernelGGL(yardstick_kernel<1>, dim3(grid), dim3(kMaxThreads), 0, stream,
+                                   s, d, nvec, key); break;
+        case 2: hipLaunchKernelGGL(yardstick_kernel<2>, dim3(grid), dim3(kMaxThreads), 0, stream,
+                                   s, d, nvec, key); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace aqua

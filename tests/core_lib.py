@@ -55,6 +55,23 @@ def lib():
         L.aqua_core_tracker_issue_rw.restype = i64
         L.aqua_core_tracker_complete.argtypes = [P, u32, u64]
         L.aqua_core_tracker_live_ranges.argtypes = [P]
+        for n in ("aqua_core_tracker_tickets_kept", "aqua_core_tracker_lanes"):
+            getattr(L, n).argtypes = [P]
+            getattr(L, n).restype = u64
+        L.aqua_core_tracker_done.argtypes = [P, u64]
+        L.aqua_core_tracker_done.restype = i32
+        L.aqua_core_lanes_new.restype = P
+        L.aqua_core_lanes_free.argtypes = [P]
+        L.aqua_core_lanes_lane_for.argtypes = [P, u64, P]
+        L.aqua_core_lanes_lane_for.restype = u32
+        L.aqua_core_lanes_size.argtypes = [P]
+        L.aqua_core_lanes_size.restype = u64
+        L.aqua_core_tracker_soak.argtypes = [u64, u32, u32, u64, u32, ctypes.POINTER(u64),
+                                             ctypes.POINTER(u64)]
+        L.aqua_core_swap_threads.argtypes = [u64, u32]
+        L.aqua_core_swap_threads.restype = u32
+        L.aqua_core_launch_grid.argtypes = [u64, u32]
+        L.aqua_core_launch_grid.restype = u32
         L.aqua_core_tracker_live_ranges.restype = u64
         _lib = L
     return _lib
@@ -150,6 +167,15 @@ class Tracker:
     def live_ranges(self):
         return int(lib().aqua_core_tracker_live_ranges(self.h))
 
+    def tickets_kept(self):
+        return int(lib().aqua_core_tracker_tickets_kept(self.h))
+
+    def lanes(self):
+        return int(lib().aqua_core_tracker_lanes(self.h))
+
+    def done(self, ticket):
+        return bool(lib().aqua_core_tracker_done(self.h, ticket))
+
     def __del__(self):
         if getattr(self, "h", None):
             lib().aqua_core_tracker_free(self.h)
@@ -193,3 +219,38 @@ class Ranges:
         if self.h:
             self.L.aqua_core_ranges_free_all(self.h)
             self.h = None
+
+
+class LaneMap:
+    """The core's stream -> lane map, over a Tracker."""
+
+    def __init__(self):
+        self.h = lib().aqua_core_lanes_new()
+
+    def lane_for(self, stream: int, tracker: "Tracker") -> int:
+        return int(lib().aqua_core_lanes_lane_for(self.h, stream, tracker.h))
+
+    def size(self) -> int:
+        return int(lib().aqua_core_lanes_size(self.h))
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            lib().aqua_core_lanes_free(self.h)
+            self.h = None
+
+
+def swap_threads(chunk_bytes: int, min_threads: int) -> int:
+    return int(lib().aqua_core_swap_threads(chunk_bytes, min_threads))
+
+
+def launch_grid(units: int, max_workgroups: int) -> int:
+    return int(lib().aqua_core_launch_grid(units, max_workgroups))
+
+
+def tracker_soak(n_calls: int, num_blocks: int, streams: int, rotate: int, depth: int):
+    """(largest tickets kept, largest lane count) over a simulated serving
+    loop; see aqua_core_tracker_soak."""
+    kept, lanes = ctypes.c_uint64(0), ctypes.c_uint64(0)
+    lib().aqua_core_tracker_soak(n_calls, num_blocks, streams, rotate, depth,
+                                 ctypes.byref(kept), ctypes.byref(lanes))
+    return int(kept.value), int(lanes.value)

@@ -197,3 +197,60 @@ def test_finished_ranges_are_forgotten():
     tr.complete(0, 100)
     tr.issue(101, 1, False, [0], [(0, 16)])
     assert tr.live_ranges() == 1
+
+
+def test_tracker_memory_stays_bounded_over_a_million_calls():
+    """A serving loop issues 10^6 swaps over streams that are replaced by
+    new handles every 1000 calls, with at most 8 calls in flight: the
+    tracker keeps the lanes of the in-flight tickets only, and the stream
+    map reuses idle lanes instead of growing by one per stream handle."""
+    from tests.core_lib import tracker_soak
+    kept, lanes = tracker_soak(1_000_000, 16384, streams=4, rotate=1000, depth=8)
+    assert kept <= 9            # the in-flight tickets plus the one being issued
+    assert lanes <= 4 + 8 + 1   # the streams in use, plus those still in flight
+
+
+def test_completed_tickets_are_dropped_and_still_done():
+    """Once every ticket up to t is complete its lane is forgotten, and done()
+    still answers for it; a ticket of a lane that is behind keeps the ones
+    after it."""
+    tr = Tracker(64)
+    for t in range(1, 11):
+        tr.issue(t, t % 2, False, [t], [])
+    assert tr.tickets_kept() == 10
+    tr.complete(1, 9)                      # lane 1: tickets 1, 3, ..., 9
+    assert tr.tickets_kept() == 9          # ticket 1 goes; ticket 2 (lane 0) holds the rest
+    assert tr.done(9) and not tr.done(2)
+    tr.complete(0, 6)
+    assert tr.tickets_kept() == 3          # tickets 8..10 are kept
+    assert all(tr.done(t) for t in range(1, 8)) and not tr.done(8)
+    tr.complete(0, 10)
+    assert tr.tickets_kept() == 0 and all(tr.done(t) for t in range(1, 11))
+    # A later call on a forgotten block's ticket is not held back by it.
+    assert tr.issue(11, 2, True, [3], []) == []
+
+
+def test_skipped_tickets_count_as_complete():
+    tr = Tracker(16)
+    tr.issue(5, 0, False, [1], [])
+    assert tr.done(2) and not tr.done(5)
+    assert tr.issue(9, 1, True, [1], []) == [(0, 5)]
+    tr.complete(0, 5)
+    assert tr.tickets_kept() == 1          # ticket 9 only
+
+
+def test_lane_map_reuses_idle_lanes_only():
+    from tests.core_lib import LaneMap
+    tr, lm = Tracker(16), LaneMap()
+    a = lm.lane_for(0xA, tr)
+    tr.issue(1, a, False, [1], [])
+    b = lm.lane_for(0xB, tr)
+    assert b != a                            # lane a is busy
+    tr.issue(2, b, False, [2], [])
+    assert lm.lane_for(0xA, tr) == a         # a stream keeps its lane
+    tr.complete(a, 1)
+    c = lm.lane_for(0xC, tr)
+    assert c == a and lm.size() == 2         # the idle lane is handed over
+    tr.issue(3, c, True, [1], [])
+    assert lm.lane_for(0xA, tr) not in (b, c)  # stream A comes back: a new lane
+    assert lm.size() == 3

@@ -194,3 +194,41 @@ def test_migrate_validation_matches_oracle():
         got = core_lib.validate_migrate(src.ctypes.data, src.nbytes, dst.ctypes.data,
                                         dst.nbytes, so, do, ln)
         assert got == want, (case, so, do, ln, src is dst)
+
+
+def test_launch_grid_stays_within_one_dispatch():
+    """A dispatch counts its work-items in 32 bits: with 1024-lane
+    workgroups at most 4 194 303 fit.  A call of 2^22 units (a fragmented
+    131072-block table of 32 layers) and anything larger get a capped grid
+    that the kernels' grid-stride loop covers."""
+    from tests.core_lib import launch_grid
+    assert launch_grid(1, 0) == 1
+    assert launch_grid(32768, 0) == 32768
+    assert launch_grid(32768, 16) == 16
+    for units in (1 << 22, (1 << 31) - 1, 1 << 40):
+        g = launch_grid(units, 0)
+        assert g == 1 << 21 and g * 1024 < 1 << 32
+    assert launch_grid(1 << 22, 4_000_000) == 1 << 21
+    assert launch_grid(0, 0) == 0
+
+
+def test_workgroup_is_sized_to_the_chunk():
+    """Every lane holds 4 vectors of 16 bytes in flight: a 64 KiB chunk
+    takes 1024 lanes, 32 KiB 512, 16 KiB 256; a larger chunk still 1024,
+    and smaller ones never go below the minimum asked for (a power of two
+    of at least one wave)."""
+    from tests.core_lib import swap_threads
+    assert swap_threads(64 << 10, 64) == 1024
+    assert swap_threads(1 << 20, 64) == 1024
+    assert swap_threads(32 << 10, 64) == 512
+    assert swap_threads(16 << 10, 64) == 256
+    assert swap_threads(4 << 10, 64) == 64
+    assert swap_threads(48 << 10, 64) == 1024   # 768 lanes' worth rounds up
+    assert swap_threads(32, 64) == 64
+    assert swap_threads(16 << 10, 256) == 256
+    assert swap_threads(4 << 10, 256) == 256
+    assert swap_threads(4 << 10, 200) == 256
+    assert swap_threads(32 << 10, 1024) == 1024
+    for c in (16, 32, 4096, 12288, 65536, 1 << 30):
+        t = swap_threads(c, 64)
+        assert t in (64, 128, 256, 512, 1024)

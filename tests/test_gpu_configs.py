@@ -127,7 +127,8 @@ def test_preemption_cycle_full():
     swaps 16 out on one stream and 16 in on another, then the host mutates
     the residents and the consumed slots.  The whole pool and offload region
     must equal the oracle's replay."""
-    n = int(os.environ.get("AQUA_TEST_SLICES", "10"))
+    # The configuration runs 100 slices; AQUA_TEST_SLICES shortens a quick run.
+    n = int(os.environ.get("AQUA_TEST_SLICES", "100"))
     sched = wl.preemption_schedule(n_slices=n)
     s = sched.shape
     t0 = time.time()

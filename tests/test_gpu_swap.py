@@ -165,6 +165,20 @@ def test_capped_grids_loop_over_every_unit(cap, pinned):
                host_path=aqua.AQUA_HOST_ZERO_COPY if pinned else None, max_workgroups=cap)
 
 
+def test_more_units_than_one_dispatch_can_count():
+    """40 layers of a fragmented 131072-block table on a 262144-block pool of
+    32-byte chunks: 5.2 million (layer, run) units, more workgroups than one
+    dispatch can count (its 32-bit work-item count allows 4 194 303 of 1024
+    lanes).  The grid is capped and each workgroup loops over units a grid
+    apart; every byte still matches the oracle."""
+    shape = wl.KVShape(40, 262144, 1, 1, 8, wl.BF16)          # 32-byte chunks
+    perm = wl.permutation(shape.num_blocks, 67)
+    out_tables = [perm[:131072]]
+    in_tables = [perm[131072:]]
+    say("units", shape.num_layers * len(out_tables[0]))
+    _roundtrip(shape, 67, out_tables, in_tables, None)
+
+
 def test_pinned_host_zero_copy_round_trip():
     """The offload image in pinned host memory, written and read zero-copy."""
     case = wl.tiny_case(seed=11)
