@@ -19,7 +19,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "aqua_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# AQUA_ORACLE_LIB names another build of the oracle (the sanitizer build).
+_LIB = os.environ.get("AQUA_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 OK, ERR_INVALID, ERR_RANGE, ERR_DUPLICATE, ERR_CAPACITY = 0, -1, -2, -3, -4
 F16, BF16, FP8_E4M3 = 1, 2, 3

@@ -8,6 +8,9 @@
                           through ``include/aqua.h`` alone; a GPU test runs it.
 
 Run ``python -m paper_2407_21255_amd.build``.
+
+The sanitizer build of the host core and the oracle is
+``python -m paper_2407_21255_amd.sanitize`` (CPU only).
 """
 from __future__ import annotations
 
@@ -95,3 +98,4 @@ if __name__ == "__main__":
         build_hip()
     if "client" in what:
         build_c_client()
+

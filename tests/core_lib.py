@@ -9,7 +9,9 @@ import os
 import numpy as np
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CORE = os.path.join(ROOT, "paper_2407_21255_amd", "libaqua_core.so")
+# AQUA_CORE_LIB names another build of the core (the sanitizer build).
+CORE = os.environ.get("AQUA_CORE_LIB") or os.path.join(ROOT, "paper_2407_21255_amd",
+                                                       "libaqua_core.so")
 
 RUN_DESC = np.dtype([("img_off", "<u8"), ("img_lstride", "<u8"), ("block", "<u4"),
                      ("nchunks", "<u4"), ("r0", "<u4"), ("r1", "<u4")])
