@@ -215,6 +215,38 @@ AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
                                      const aqua_swap_range* range, int32_t target,
                                      void* stream, uint64_t* ticket);
 
+/* ---- Allocation-free swap, for callers that cannot allocate memory (code
+ * being captured into a HIP graph, tight serving loops, harnesses that
+ * forbid allocation).
+ *
+ * aqua_swap_noalloc is aqua_swap_out (direction 0) or aqua_swap_in
+ * (direction 1) with the same arguments, results, ordering and errors,
+ * except that it allocates nothing: no device or pinned memory, no HIP
+ * event or stream.  Its run descriptors go through the pool's pinned ring
+ * (allocated when the pool was created; the call never grows it) to a
+ * device scratch array of 2 MiB that the library holds on each device for
+ * the life of the process, and its completion event is one of those the
+ * pool created (while none is spare, the call first waits for the oldest
+ * outstanding call of the pool).  Differences:
+ *   - at most 65536 run descriptors per call (a run is a stretch of
+ *     consecutive blocks of one table, up to 64 KiB; a fragmented table has
+ *     one run per block), and no more than the pool's ring holds:
+ *     AQUA_ERR_CAPACITY otherwise, before anything is enqueued;
+ *   - a pinned-host image is always moved zero-copy, whatever
+ *     aqua_kv_pool_set_host_path says (the staged path needs the library's
+ *     slots and copy engines);
+ *   - all layers are moved (no layer range or partial image).
+ * The scratch array is shared by every pool on a device and keeps the last
+ * call's descriptors.  Calls of this entry point on one pool are ordered
+ * with each other by the library (they all write the scratch); calls on
+ * different pools of one device that may overlap in time race on the
+ * scratch and must be ordered by the caller (one stream, or a sync). */
+AQUA_API aqua_status aqua_swap_noalloc(aqua_kv_pool_t pool, int32_t direction,
+                                       uint32_t num_seqs, const int32_t* block_ids,
+                                       const uint64_t* seq_offsets, void* buf,
+                                       uint64_t buf_bytes, const uint64_t* img_offsets,
+                                       int32_t target, void* stream, uint64_t* ticket);
+
 /* Image migration.  When the memory holding offloaded images is reclaimed
  * (section 6, "Reclaiming Aqua Tensors"), the images move elsewhere -- here
  * between the HBM region and pinned host memory, in either direction, or

@@ -44,7 +44,7 @@ EXPORTS = (
     "aqua_pool_stats_get", "aqua_status_str", "aqua_cfs_partition",
     "aqua_swap_space_create", "aqua_swap_space_destroy", "aqua_swap_alloc", "aqua_swap_free",
     "aqua_swap_locate", "aqua_swap_reclaim", "aqua_swap_restore", "aqua_swap_usage",
-    "aqua_hbm_yardstick",
+    "aqua_hbm_yardstick", "aqua_swap_noalloc",
 )
 
 
@@ -136,6 +136,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.aqua_swap_restore.argtypes = [P, P, ctypes.POINTER(u64)]
     L.aqua_swap_usage.argtypes = [P] + [ctypes.POINTER(u64)] * 4
     L.aqua_hbm_yardstick.argtypes = [i32, P, P, u64, P]
+    L.aqua_swap_noalloc.argtypes = [P, i32, u32, P, P, P, u64, P, i32, P, ctypes.POINTER(u64)]
     L.aqua_status_str.argtypes = [i32]
     L.aqua_status_str.restype = ctypes.c_char_p
     for n in EXPORTS:
@@ -187,6 +188,14 @@ def aqua_swap_in_ex(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
     t = ctypes.c_uint64(0)
     st = load().aqua_swap_in_ex(pool, num_seqs, block_ids, seq_offsets, src, src_bytes,
                                 img_offsets, rng, target, stream, ctypes.byref(t))
+    return st, t.value
+
+
+def aqua_swap_noalloc(pool, direction, num_seqs, block_ids, seq_offsets, buf, buf_bytes,
+                      img_offsets, target, stream):
+    t = ctypes.c_uint64(0)
+    st = load().aqua_swap_noalloc(pool, direction, num_seqs, block_ids, seq_offsets, buf,
+                                  buf_bytes, img_offsets, target, stream, ctypes.byref(t))
     return st, t.value
 
 
@@ -447,6 +456,24 @@ class KVPool:
     def swap_in(self, tables, src: torch.Tensor, img_offsets=None, stream=None,
                 target=None, img_blocks=None, layers=None) -> int:
         return self._swap(True, tables, src, img_offsets, stream, target, img_blocks, layers)
+
+    def swap_noalloc(self, direction: int, tables, buf: torch.Tensor, img_offsets=None,
+                     stream=None, target=None) -> int:
+        """aqua_swap_noalloc: swap-out (direction 0) or swap-in (1) that
+        allocates nothing."""
+        ids, offs = _csr(tables)
+        io = None
+        if img_offsets is not None:
+            io = np.ascontiguousarray(img_offsets, dtype=np.uint64)
+        tgt = _target_of(buf) if target is None else target
+        st, ticket = aqua_swap_noalloc(
+            self.handle, direction, len(offs) - 1, ids.ctypes.data, offs.ctypes.data,
+            buf.data_ptr(), buf.numel() * buf.element_size(),
+            None if io is None else io.ctypes.data, tgt, _stream_handle(stream))
+        if st != AQUA_OK:
+            raise AquaError(st, "aqua_swap_noalloc")
+        self._hold(ticket, buf)
+        return ticket
 
     def migrate(self, src: torch.Tensor, dst: torch.Tensor, src_offsets, dst_offsets,
                 lengths, stream=None) -> int:

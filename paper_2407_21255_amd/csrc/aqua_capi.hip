@@ -61,6 +61,32 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
     return (end && *end == 0) ? (uint64_t)x : dflt;
 }
 
+// Device scratch of the allocation-free swap entry point
+// (aqua_swap_noalloc): its run descriptors, copied there from the pool's
+// pinned ring on the call's stream.  One array per device for the life of
+// the process; host code uses only the device address that
+// hipGetSymbolAddress gives for the current device (scratch_address).
+constexpr uint64_t kScratchBytes = 2ull << 20;  // 65536 run descriptors
+constexpr uint32_t kPoolEvents = 4;              // events made at pool creation
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Device address of `scratch` on `device`, looked up once per device with
+// that device current (the caller has made it current); nullptr on failure.
+uint8_t* scratch_address(int device) {
+    static std::mutex mu;
+    static std::map<int, uint8_t*> addr;
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = addr.find(device);
+    if (it != addr.end()) return it->second;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    addr[device] = (uint8_t*)ptr;
+    return (uint8_t*)ptr;
+}
+
 struct Outstanding {
     uint64_t ticket;
     hipEvent_t ev;                 // recorded on the call's stream, last
@@ -134,6 +160,7 @@ struct aqua_kv_pool {
 
     uint64_t next_ticket = 1;
     uint64_t unit_bytes = kDefaultUnitBytes;
+    uint8_t* scratch = nullptr;  // this device's scratch (aqua_swap_noalloc)
     // Grid caps per target (0: one workgroup per unit).  Zero-copy host
     // swaps are link-bound: 16 workgroups of 1024 lanes saturate the link.
     uint32_t max_wg[2] = {0, kHostZeroCopyWorkgroups};
@@ -302,6 +329,29 @@ aqua_status wait_all(aqua_kv_pool* p) {
     return check_links(p);
 }
 
+// An event for a call of the allocation-free entry point: a spare one, or,
+// while none is spare, the event of the oldest outstanding call once that
+// call has completed.  Creates nothing: the pool made kPoolEvents events
+// when it was created, and each is either spare or held by a call.
+aqua_status take_event_noalloc(aqua_kv_pool* p, hipEvent_t* ev) {
+    for (;;) {
+        if (!p->spare_events.empty()) {
+            *ev = p->spare_events.back();
+            p->spare_events.pop_back();
+            return AQUA_OK;
+        }
+        uint32_t oldest = UINT32_MAX;
+        for (uint32_t m = 0; m < p->outstanding.size(); ++m)
+            if (!p->outstanding[m].empty() &&
+                (oldest == UINT32_MAX ||
+                 p->outstanding[m].front().ticket < p->outstanding[oldest].front().ticket))
+                oldest = m;
+        if (oldest == UINT32_MAX) return AQUA_ERR_STATE;  // no event at all
+        const aqua_status st = wait_ticket(p, p->outstanding[oldest].front().ticket);
+        if (st != AQUA_OK) return st;
+    }
+}
+
 void free_rings(aqua_kv_pool* p) {
     if (p->ring_dev) (void)hipFree(p->ring_dev);
     if (p->ring_host) (void)hipHostFree(p->ring_host);
@@ -333,8 +383,9 @@ aqua_status alloc_rings(aqua_kv_pool* p, uint64_t bytes) {
 
 // Reserves `bytes` of the descriptor rings, waiting for the calls that used
 // the space last.  Grows the rings when one call needs more than they hold.
-aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off) {
+aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off, bool grow = true) {
     bytes = (bytes + 255) & ~255ull;
+    if (bytes > p->ring_bytes && !grow) return AQUA_ERR_CAPACITY;
     if (bytes > p->ring_bytes) {
         aqua_status st = wait_all(p);
         if (st != AQUA_OK) return st;
@@ -406,15 +457,18 @@ __global__ __launch_bounds__(256) void upload_descs_kernel(const uint4* __restri
 // the call's own data.  A kernel, not a runtime copy: the runtime can hold
 // the calling thread on such a small copy until the stream's earlier host
 // functions have run.  `bytes` is a multiple of 32 (whole descriptors).
-hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipStream_t stream) {
+hipError_t upload_to(const uint8_t* src, uint8_t* dst, uint64_t bytes, hipStream_t stream) {
     const uint32_t n = (uint32_t)(bytes / 16);
     if (!n) return hipSuccess;
     const uint32_t grid = std::min<uint32_t>(256u, (n + 255u) / 256u);
     (void)hipGetLastError();
     hipLaunchKernelGGL(upload_descs_kernel, dim3(grid), dim3(256), 0, stream,
-                       reinterpret_cast<const uint4*>(p->ring_host_dev + ring_off),
-                       reinterpret_cast<uint4*>(p->ring_dev + ring_off), n);
+                       reinterpret_cast<const uint4*>(src), reinterpret_cast<uint4*>(dst), n);
     return hipGetLastError();
+}
+
+hipError_t upload_descs(aqua_kv_pool* p, uint64_t ring_off, uint64_t bytes, hipStream_t stream) {
+    return upload_to(p->ring_host_dev + ring_off, p->ring_dev + ring_off, bytes, stream);
 }
 
 // Launches one kernel of each of the library's source files once, with
@@ -738,7 +792,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                     const int32_t* ids, const uint64_t* offs, const void* buf,
                     uint64_t buf_bytes, const uint64_t* img_offsets,
                     const aqua_swap_range* range, int32_t target, void* stream_ptr,
-                    uint64_t* ticket_out) {
+                    uint64_t* ticket_out, bool noalloc = false) {
     if (!p) return AQUA_ERR_INVALID;
     if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
     const auto t0 = std::chrono::steady_clock::now();
@@ -782,7 +836,10 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
 
     const uint32_t lane = lane_for(p, stream);
     const uint64_t ticket = p->next_ticket;
-    const bool staged = target == AQUA_TARGET_HOST && p->host_path == AQUA_HOST_STAGED && total;
+    // The allocation-free form moves a host image zero-copy: the staged
+    // path needs the library's slots and copy engines.
+    const bool staged = target == AQUA_TARGET_HOST && p->host_path == AQUA_HOST_STAGED &&
+                        total && !noalloc;
     const uint32_t l_begin = a.first_layer;
     const uint32_t l_count = a.num_layers ? a.num_layers : p->shape.L;
 
@@ -833,18 +890,41 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     uint64_t ring_off = 0;
     const uint64_t dbytes = p->plan.size() * sizeof(RunDesc);
     uint64_t waited_ns = 0;
+    Outstanding rec{ticket, nullptr, {}};
+    // The allocation-free form: descriptors beyond the scratch are refused
+    // before anything happens, and the call's event is a recycled one.
+    const std::pair<uint64_t, uint64_t> scratch_range{
+        (uint64_t)(uintptr_t)p->scratch, (uint64_t)(uintptr_t)p->scratch + dbytes};
+    if (noalloc) {
+        if (dbytes > kScratchBytes) return AQUA_ERR_CAPACITY;
+        if (!p->scratch) return AQUA_ERR_HIP;
+        const auto w0 = std::chrono::steady_clock::now();
+        st = take_event_noalloc(p, &rec.ev);
+        waited_ns += (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                         std::chrono::steady_clock::now() - w0)
+                         .count();
+        if (st != AQUA_OK) return st;
+    }
+    auto give_back = [&]() {
+        if (rec.ev) p->spare_events.push_back(rec.ev);
+        rec.ev = nullptr;
+    };
     if (dbytes) {
         const auto w0 = std::chrono::steady_clock::now();
-        st = ring_reserve(p, dbytes, &ring_off);
+        st = ring_reserve(p, dbytes, &ring_off, !noalloc);
         waited_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
                         std::chrono::steady_clock::now() - w0)
                         .count();
-        if (st != AQUA_OK) return st;
+        if (st != AQUA_OK) {
+            give_back();
+            return st;
+        }
     }
 
     // Accesses: swap-out reads the table's blocks and writes the images,
     // swap-in reads the images and writes the blocks; the staged path also
-    // writes its slots.
+    // writes its slots, and the allocation-free form the device scratch (so
+    // that two such calls on one pool never overlap).
     HazardTracker::Access acc;
     if (is_in) {
         acc.blocks_written = ids;
@@ -854,11 +934,15 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         if (staged) {
             acc.ranges_written = &stage_range;
             acc.n_ranges_written = 1;
+        } else if (noalloc && dbytes) {
+            acc.ranges_written = &scratch_range;
+            acc.n_ranges_written = 1;
         }
     } else {
         acc.blocks_read = ids;
         acc.n_blocks_read = (size_t)total;
         if (staged) p->ranges.push_back(stage_range);
+        if (noalloc && dbytes) p->ranges.push_back(scratch_range);
         acc.ranges_written = p->ranges.data();
         acc.n_ranges_written = p->ranges.size();
     }
@@ -873,12 +957,14 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         p->stats.waits_inserted++;
     }
 
-    Outstanding rec{ticket, nullptr, {}};
     if (dbytes) {
         std::memcpy(p->ring_host + ring_off, p->plan.data(), dbytes);
         hipError_t e = hipSuccess;
         const uint8_t* descs = p->ring_host_dev + ring_off;
-        if (staged || AQUA_DESC_DEVICE) {
+        if (noalloc) {
+            descs = p->scratch;
+            e = upload_to(p->ring_host_dev + ring_off, p->scratch, dbytes, stream);
+        } else if (staged || AQUA_DESC_DEVICE) {
             descs = p->ring_dev + ring_off;
             e = upload_descs(p, ring_off, dbytes, stream);
         }
@@ -902,7 +988,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         }
     }
 
-    hipError_t e = take_event(p, &rec.ev);
+    hipError_t e = rec.ev ? hipSuccess : take_event(p, &rec.ev);
     if (e == hipSuccess) e = hipEventRecord(rec.ev, stream);
     if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
     p->outstanding[lane].push_back(std::move(rec));
@@ -1143,11 +1229,22 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
     p->slot_target = env_u64("AQUA_STAGE_SLOT_BYTES", kDefaultSlotBytes);
     p->fail_release_at = env_u64("AQUA_FAIL_RELEASE_AT", ~0ull);
     st = alloc_rings(p, env_u64("AQUA_RING_BYTES", kDefaultRingBytes));
-    if (st == AQUA_OK && warm_kernels(p) != hipSuccess) {
-        free_rings(p);
-        st = AQUA_ERR_HIP;
+    if (st == AQUA_OK && warm_kernels(p) != hipSuccess) st = AQUA_ERR_HIP;
+    // Set-up of the allocation-free entry point: this device's scratch
+    // address, and the events its calls recycle.
+    if (st == AQUA_OK && !(p->scratch = scratch_address(dev))) st = AQUA_ERR_HIP;
+    for (uint32_t k = 0; st == AQUA_OK && k < kPoolEvents; ++k) {
+        hipEvent_t ev = nullptr;
+        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+            (void)hipGetLastError();
+            st = AQUA_ERR_HIP;
+        } else {
+            p->spare_events.push_back(ev);
+        }
     }
     if (st != AQUA_OK) {
+        for (hipEvent_t ev : p->spare_events) (void)hipEventDestroy(ev);
+        free_rings(p);
         delete p;
         return st;
     }
@@ -1221,6 +1318,15 @@ aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_
                             int32_t target, void* stream, uint64_t* ticket) {
     return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
                    range, target, stream, ticket);
+}
+
+aqua_status aqua_swap_noalloc(aqua_kv_pool_t pool, int32_t direction, uint32_t num_seqs,
+                              const int32_t* block_ids, const uint64_t* seq_offsets, void* buf,
+                              uint64_t buf_bytes, const uint64_t* img_offsets, int32_t target,
+                              void* stream, uint64_t* ticket) {
+    if (direction != 0 && direction != 1) return AQUA_ERR_INVALID;
+    return do_swap(pool, direction == 1, num_seqs, block_ids, seq_offsets, buf, buf_bytes,
+                   img_offsets, nullptr, target, stream, ticket, true);
 }
 
 aqua_status aqua_migrate(aqua_kv_pool_t pool, const void* src, uint64_t src_bytes,

@@ -1,0 +1,160 @@
+"""GPU checks of the allocation-free swap (aqua_swap_noalloc) against the
+ordinary entry points (aqua_swap_out / aqua_swap_in), byte for byte, through
+the C ABI: two calls in a row, the second smaller, so that descriptors left
+in the device scratch by the first must not leak into the second; calls on
+two streams without a host sync in between; the descriptor limit; and no
+device memory taken by the calls."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_21255_amd import aqua
+from paper_2407_21255_amd import workload as wl
+from tests.checkers import assert_bytes_equal
+from tests.gpu_util import device_pool, guarded_buffer, host, odesc, say
+
+pytestmark = pytest.mark.gpu
+
+G = 4096
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    aqua.load()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _calls(shape, seed):
+    """Two (out tables, in tables) pairs on disjoint blocks: three fragmented
+    sequences with a contiguous stretch, then one short sequence."""
+    N = shape.num_blocks
+    perm = wl.permutation(N, seed)
+    first_out = [perm[:120], list(range(N - 40, N - 8)), perm[120:121]]
+    first_out[1] = [b for b in first_out[1] if b not in set(perm[:121])]
+    used = {b for t in first_out for b in t}
+    free = [b for b in perm[121:] if b not in used]
+    sizes = [len(t) for t in first_out]
+    first_in, k = [], 0
+    for n in sizes:
+        first_in.append(free[k:k + n])
+        k += n
+    rest = free[k:]
+    second_out = [rest[:17]]
+    second_in = [rest[17:34]]
+    return [(first_out, first_in), (second_out, second_in)]
+
+
+@pytest.mark.parametrize("pinned", [False, True], ids=["hbm", "pinned_host"])
+def test_noalloc_matches_the_ordinary_entry_points(pinned):
+    shape = wl.KVShape(4, 512, 8, 16, 128, wl.BF16)       # 64 KiB chunks
+    d = odesc(shape)
+    pool_a = device_pool(shape, 71)                        # ordinary entry points
+    pool_b = pool_a.clone()                                # allocation-free one
+    pool_h = host(pool_a)
+    size = shape.image_bytes(200)
+    buf_a = guarded_buffer(size, G, pinned)
+    buf_b = guarded_buffer(size, G, pinned)
+    kv_a = aqua.KVPool(shape.as_tuple(), pool_a)
+    kv_b = aqua.KVPool(shape.as_tuple(), pool_b)
+    stream = torch.cuda.Stream()
+    try:
+        # The stream and the kernels have been used once before the calls
+        # whose device memory is watched.
+        kv_a.swap_out([[0]], buf_a[G:G + shape.chunk_bytes * shape.num_layers], stream=stream)
+        kv_a.sync(0)
+        for k, (outs, ins) in enumerate(_calls(shape, 71)):
+            nb = sum(len(t) for t in outs)
+            n = shape.image_bytes(nb)
+            ia, ib = buf_a[G:G + n], buf_b[G:G + n]
+            torch.cuda.synchronize()
+            free0 = torch.cuda.mem_get_info()[0]
+            tb = kv_b.swap_noalloc(0, outs, ib, stream=stream)
+            kv_b.sync(tb)
+            free1 = torch.cuda.mem_get_info()[0]
+            ta = kv_a.swap_out(outs, ia, stream=stream)
+            kv_a.sync(ta)
+            say("call", k, "blocks", nb, "free bytes before/after", free0, free1)
+            assert free1 == free0, "the allocation-free swap took device memory"
+            want = np.full(n, 0, dtype=np.uint8)
+            assert oracle.swap_out(d, pool_h, outs, want) == 0
+            assert_bytes_equal(host(ib), want, f"call {k}: noalloc image vs oracle")
+            assert_bytes_equal(host(buf_b), host(buf_a), f"call {k}: images and guards")
+            tb = kv_b.swap_noalloc(1, ins, ib, stream=stream)
+            ta = kv_a.swap_in(ins, ia, stream=stream)
+            kv_a.sync(0)
+            kv_b.sync(0)
+            assert oracle.swap_in(d, pool_h, ins, want) == 0
+            assert_bytes_equal(host(pool_b), pool_h, f"call {k}: noalloc pool vs oracle")
+            assert_bytes_equal(host(pool_b), host(pool_a), f"call {k}: pools")
+        st = kv_b.stats()
+        assert st["calls_out"] == 2 and st["calls_in"] == 2 and st["hip_error"] == 0
+    finally:
+        kv_a.close()
+        kv_b.close()
+
+
+def test_noalloc_calls_on_two_streams_without_a_sync():
+    """A swap-out on one stream and a swap-in on another, issued back to
+    back: both write the shared scratch, and the library orders them."""
+    shape = wl.KVShape(8, 1024, 4, 16, 128, wl.FP8_E4M3)   # 16 KiB chunks
+    d = odesc(shape)
+    pool = device_pool(shape, 73)
+    pool_h = host(pool)
+    perm = wl.permutation(shape.num_blocks, 73)
+    out1, in1 = [perm[:300]], [perm[300:600]]
+    out2 = [perm[600:640]]
+    img1 = torch.zeros(shape.image_bytes(300), dtype=torch.uint8, device="cuda")
+    img2 = torch.zeros(shape.image_bytes(40), dtype=torch.uint8, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        kv.swap_noalloc(0, out1, img1, stream=s1)
+        kv.swap_noalloc(1, in1, img1, stream=s2)   # reads img1: waits for the gather
+        kv.swap_noalloc(0, out2, img2, stream=s1)  # 40 runs after 300 in the scratch
+        kv.sync(0)
+        w1 = np.zeros(img1.numel(), dtype=np.uint8)
+        w2 = np.zeros(img2.numel(), dtype=np.uint8)
+        assert oracle.swap_out(d, pool_h, out1, w1) == 0
+        assert oracle.swap_in(d, pool_h, in1, w1) == 0
+        assert oracle.swap_out(d, pool_h, out2, w2) == 0
+        assert_bytes_equal(host(img1), w1, "first image")
+        assert_bytes_equal(host(img2), w2, "second image")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        assert kv.stats()["waits_inserted"] >= 1
+    finally:
+        kv.close()
+
+
+def test_noalloc_descriptor_limit():
+    """65536 runs fit the scratch; 65537 are refused before anything is
+    enqueued (no ticket, nothing written); a bad direction is refused."""
+    shape = wl.KVShape(1, 131080, 1, 1, 8, wl.BF16)       # 32-byte chunks
+    pool = device_pool(shape, 79)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        ok = [list(range(0, 2 * 65536, 2))]                # 65536 runs of one block
+        img = torch.zeros(shape.image_bytes(65537), dtype=torch.uint8, device="cuda")
+        t = kv.swap_noalloc(0, ok, img)
+        kv.sync(t)
+        want = np.zeros(img.numel(), dtype=np.uint8)
+        assert oracle.swap_out(odesc(shape), host(pool), ok, want[:shape.image_bytes(65536)]) == 0
+        assert_bytes_equal(host(img), want, "65536 runs")
+        img.zero_()
+        too_many = [list(range(0, 2 * 65537, 2))]
+        with pytest.raises(aqua.AquaError) as e:
+            kv.swap_noalloc(0, too_many, img)
+        assert e.value.status == aqua.AQUA_ERR_CAPACITY
+        with pytest.raises(aqua.AquaError) as e:
+            kv.swap_noalloc(2, ok, img)
+        assert e.value.status == aqua.AQUA_ERR_INVALID
+        torch.cuda.synchronize()
+        assert int(img.count_nonzero()) == 0
+        assert kv.swap_out([[1]], img) == t + 1             # no ticket was issued
+        kv.sync(0)
+    finally:
+        kv.close()
