@@ -39,6 +39,10 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
+    ("llama70b_hbm", "a097bbe9bee95f11"): {
+        "gather (swap-out)": 21477180002, "scatter (swap-in)": 21476717771},
+    ("llama70b_tp2_hbm", "a097bbe9bee95f11"): {
+        "gather (swap-out)": 10739790225, "scatter (swap-in)": 10739333115},
 }
 
 # Every source that decides what the swap kernels do and how they are
@@ -412,10 +416,11 @@ def run_pair(args, res_common):
             "swap_out_vs_runtime_copy": round(2 * res["swap_out_GBps"] / copy_gbs, 4),
             "swap_in_vs_runtime_copy": round(2 * res["swap_in_GBps"] / copy_gbs, 4),
         }
-        res["hbm_ceiling"] = hbm_ceiling(img, pool[:payload])
-        cp = res["hbm_ceiling"]["copy_GBps"]
-        res["hbm_ceiling"]["swap_out_vs_copy"] = round(2 * res["swap_out_GBps"] / cp, 4)
-        res["hbm_ceiling"]["swap_in_vs_copy"] = round(2 * res["swap_in_GBps"] / cp, 4)
+        res["hbm_ceiling"] = ceil = hbm_ceiling(img, pool[:payload])
+        for ref in ("copy", "serial"):
+            for d in ("out", "in"):
+                ceil[f"swap_{d}_vs_{ref}"] = round(2 * res[f"swap_{d}_GBps"] /
+                                                   ceil[f"{ref}_GBps"], 4)
     return res, s
 
 
@@ -423,7 +428,11 @@ def hbm_ceiling(dst, src, reps: int = 5) -> dict:
     """Same-run HBM yardsticks of the payload's size with the library's own
     copy loop (aqua_hbm_yardstick): a contiguous copy (GB/s of read + write
     traffic), a pure read and a pure write, each timed with HIP events on
-    its launch stream after one untimed pass; each as a share of 8 TB/s."""
+    its launch stream after one untimed pass; each as a share of 8 TB/s.
+    ``serial`` is the rate of reading the payload and then writing it, one
+    after the other (2 * bytes over the sum of the read and write times):
+    the rate of a copy in which the memory serves reads and writes in turn
+    and never both at once."""
     import torch
 
     from paper_2407_21255_amd import aqua
@@ -443,6 +452,9 @@ def hbm_ceiling(dst, src, reps: int = 5) -> dict:
         gbs = traffic * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
         out[f"{name}_GBps"] = round(gbs, 1)
         out[f"{name}_frac"] = round(gbs / HBM_PEAK_GBS, 4)
+    serial = 2.0 / (1.0 / out["read_GBps"] + 1.0 / out["write_GBps"])
+    out["serial_GBps"] = round(serial, 1)
+    out["serial_frac"] = round(serial / HBM_PEAK_GBS, 4)
     return out
 
 

@@ -43,14 +43,9 @@ constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 #ifndef AQUA_DESC_DEVICE
 #define AQUA_DESC_DEVICE 0
 #endif
-// A swap-in's runs are sorted by destination block when the call writes at
-// least this share of the pool's blocks, in thousandths (0: never): the
-// pool writes then go nearly in address order.  Measured on MI355X with
-// every swap-in sorted: the 70B scatter (half the pool) 3.3 % shorter, one
-// TP2 rank's 1.6 %, and no gain where the call writes a sixteenth of the
-// pool (the 8B and fp8 8B scatters, within +-0.5 %).
-#ifndef AQUA_SORT_IN_PERMILLE
-#define AQUA_SORT_IN_PERMILLE 400
+// 0: runs stay in table order (see aqua::sort_runs for the shipped rule).
+#ifndef AQUA_SORT_RUNS
+#define AQUA_SORT_RUNS 1
 #endif
 
 uint64_t env_u64(const char* name, uint64_t dflt) {
@@ -872,8 +867,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
     }
-    if (is_in && AQUA_SORT_IN_PERMILLE &&
-        total * 1000 >= (uint64_t)AQUA_SORT_IN_PERMILLE * p->shape.N)
+    if (AQUA_SORT_RUNS && aqua::sort_runs(is_in, p->shape.C, total, p->shape.N))
         std::sort(p->plan.begin(), p->plan.end(),
                   [](const RunDesc& x, const RunDesc& y) { return x.block < y.block; });
     aqua::image_ranges(p->shape, a, &p->ranges);

@@ -175,6 +175,11 @@ uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
     return t;
 }
 
+bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
+    if (!num_blocks || blocks * 1000 < kSortMinPermille * num_blocks) return false;
+    return is_in || chunk_bytes >= kSortOutMinChunk;
+}
+
 uint32_t launch_grid(uint64_t units, uint32_t max_workgroups) {
     uint64_t g = units;
     if (max_workgroups && g > max_workgroups) g = max_workgroups;

@@ -254,6 +254,10 @@ uint32_t aqua_core_swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
     return aqua::swap_threads(chunk_bytes, min_threads);
 }
 
+int aqua_core_sort_runs(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
+    return aqua::sort_runs(is_in != 0, chunk_bytes, blocks, num_blocks) ? 1 : 0;
+}
+
 uint32_t aqua_core_launch_grid(uint64_t units, uint32_t max_workgroups) {
     return aqua::launch_grid(units, max_workgroups);
 }

@@ -44,6 +44,9 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #endif
 // Swap-in pool stores: nontemporal or not is chosen per launch
 // (SwapLaunch::nt_pool_store).
+#ifndef AQUA_YS_NT       // yardsticks: nontemporal loads and stores
+#define AQUA_YS_NT 1
+#endif
 
 template <bool NT>
 __device__ __forceinline__ v4u ld(const v4u* p) {
@@ -146,13 +149,13 @@ __global__ __launch_bounds__(kMaxThreads) void yardstick_kernel(
         const uint64_t base = u * per;
         const uint32_t n = (uint32_t)std::min<uint64_t>(per, nvec - base);
         if constexpr (MODE == 0) {
-            copy_span<kMaxThreads, true, true>(src + base, dst + base, n);
+            copy_span<kMaxThreads, AQUA_YS_NT, AQUA_YS_NT>(src + base, dst + base, n);
         } else if constexpr (MODE == 1) {
             v4u r[kUnroll];
 #pragma unroll
             for (int j = 0; j < (int)kUnroll; ++j) {
                 const uint32_t i = j * kMaxThreads + t;
-                r[j] = i < n ? ld<true>(src + base + i) : v4u{0u, 0u, 0u, 0u};
+                r[j] = i < n ? ld<AQUA_YS_NT>(src + base + i) : v4u{0u, 0u, 0u, 0u};
             }
 #pragma unroll
             for (int j = 0; j < (int)kUnroll; ++j) acc ^= r[j];
@@ -161,7 +164,8 @@ __global__ __launch_bounds__(kMaxThreads) void yardstick_kernel(
             for (int j = 0; j < (int)kUnroll; ++j) {
                 const uint32_t i = j * kMaxThreads + t;
                 const uint64_t g = base + i;
-                if (i < n) st<true>(dst + g, v4u{(uint32_t)g, (uint32_t)(g >> 32), key, ~key});
+                if (i < n)
+                    st<AQUA_YS_NT>(dst + g, v4u{(uint32_t)g, (uint32_t)(g >> 32), key, ~key});
             }
         }
     }

@@ -72,6 +72,8 @@ def lib():
                                              ctypes.POINTER(u64)]
         L.aqua_core_swap_threads.argtypes = [u64, u32]
         L.aqua_core_swap_threads.restype = u32
+        L.aqua_core_sort_runs.argtypes = [i32, u64, u64, u32]
+        L.aqua_core_sort_runs.restype = i32
         L.aqua_core_launch_grid.argtypes = [u64, u32]
         L.aqua_core_launch_grid.restype = u32
         L.aqua_core_tracker_live_ranges.restype = u64
@@ -256,3 +258,7 @@ def tracker_soak(n_calls: int, num_blocks: int, streams: int, rotate: int, depth
     lib().aqua_core_tracker_soak(n_calls, num_blocks, streams, rotate, depth,
                                  ctypes.byref(kept), ctypes.byref(lanes))
     return int(kept.value), int(lanes.value)
+
+
+def sort_runs(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int) -> bool:
+    return bool(lib().aqua_core_sort_runs(int(is_in), chunk_bytes, blocks, num_blocks))

@@ -55,3 +55,31 @@ def test_cpu_baseline_record():
     assert rec["kind"] == "oracle" and rec["cores"] == 1 and rec["unit"] == "GB/s"
     assert rec["value"] > 0 and "round trips" in rec["sample"]
     assert os.sched_getaffinity(0) == affinity        # pinning undone
+
+
+def test_traffic_follows_what_the_kernels_run(tmp_path, monkeypatch):
+    """The measured traffic is keyed to every source and setting that
+    decides the swap launches: a changed store rule, a changed launch
+    setting or a grid cap each give another key, so the bench line reports
+    traffic as null until the counters are taken again."""
+    import shutil
+    sys.path.insert(0, ROOT)
+    import bench
+    csrc = os.path.join(ROOT, "paper_2407_21255_amd", "csrc")
+    copy = tmp_path / "paper_2407_21255_amd" / "csrc"
+    shutil.copytree(csrc, copy)
+    base = bench._kernel_hash()
+    assert bench._kernel_hash(str(tmp_path)) == base
+    h = copy / "swap_kernels.h"
+    text = h.read_text()
+    assert "kNtPoolStoreMinBytes = 2ull << 30" in text
+    h.write_text(text.replace("kNtPoolStoreMinBytes = 2ull << 30", "kNtPoolStoreMinBytes = 1ull << 30"))
+    changed = bench._kernel_hash(str(tmp_path))
+    assert changed != base
+    for wl in ("llama70b_hbm", "llama8b_hbm"):
+        assert bench.MEASURED_TRAFFIC.get((wl, changed)) is None
+    monkeypatch.setenv("AQUA_UNIT_BYTES", "32768")
+    assert bench._kernel_hash() != base
+    monkeypatch.delenv("AQUA_UNIT_BYTES")
+    assert bench._kernel_hash(max_workgroups=256) != base
+    assert bench._kernel_hash() == base

@@ -232,3 +232,18 @@ def test_workgroup_is_sized_to_the_chunk():
     for c in (16, 32, 4096, 12288, 65536, 1 << 30):
         t = swap_threads(c, 64)
         assert t in (64, 128, 256, 512, 1024)
+
+
+def test_run_order_rule():
+    """Runs are sorted by pool block for calls that cover at least 40 % of
+    the pool: every swap-in, and swap-outs of chunks of 64 KiB or more."""
+    from tests.core_lib import sort_runs
+    K = 1 << 10
+    assert sort_runs(True, 64 * K, 2048, 4096)          # 70B scatter: half the pool
+    assert sort_runs(True, 16 * K, 2048, 4096)          # TP4 scatter
+    assert sort_runs(False, 64 * K, 2048, 4096)         # 70B gather
+    assert not sort_runs(False, 32 * K, 2048, 4096)     # TP2 gather
+    assert not sort_runs(True, 64 * K, 1024, 16384)     # 8B: a sixteenth of the pool
+    assert not sort_runs(True, 32 * K, 4168, 16384)     # preemption cycle: a quarter
+    assert sort_runs(True, 64 * K, 1639, 4096) and not sort_runs(True, 64 * K, 1638, 4096)
+    assert not sort_runs(True, 64 * K, 0, 0)
