@@ -43,6 +43,12 @@ MEASURED_TRAFFIC = {
         "gather (swap-out)": 21477180002, "scatter (swap-in)": 21476717771},
     ("llama70b_tp2_hbm", "a097bbe9bee95f11"): {
         "gather (swap-out)": 10739790225, "scatter (swap-in)": 10739333115},
+    ("llama70b_tp4_hbm", "a097bbe9bee95f11"): {
+        "gather (swap-out)": 5369635828, "scatter (swap-in)": 5369295660},
+    ("llama8b_hbm", "a097bbe9bee95f11"): {
+        "gather (swap-out)": 4295902813, "scatter (swap-in)": 4295780345},
+    ("llama8b_fp8_hbm", "a097bbe9bee95f11"): {
+        "gather (swap-out)": 2148159784, "scatter (swap-in)": 2148142574},
 }
 
 # Every source that decides what the swap kernels do and how they are
