@@ -1048,6 +1048,39 @@ def run_next(args, res_common):
     return res, s
 
 
+def secondary_legs(args, common) -> dict:
+    """Two shorter legs reported beside the default line, outside its timed
+    region: the same 32768-token prompt swapped out to pinned host memory
+    and back on the library's default host path (staged through HBM, link
+    copies on a copy engine; 2 timed steps), and the fp8 preemption cycle
+    (10 timed slices of 16 out on one stream and 16 in on another)."""
+    import torch
+
+    legs = {}
+    sub = argparse.Namespace(**vars(args))
+    sub.workload, sub.host_path, sub.steps, sub.warmup = "llama70b_host", "staged", 2, 1
+    sub.copy_reference = False
+    r, _ = run_pair(sub, {})
+    legs["llama70b_host_staged"] = {
+        "workload": WORKLOADS["llama70b_host"] + " (staged through HBM)",
+        "steps": sub.steps, "value": r["value"], "unit": "GB/s",
+        "swap_out_GBps": r["swap_out_GBps"], "swap_in_GBps": r["swap_in_GBps"],
+        "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "peak", "frac")},
+        "host_link_frac": r["host_link_frac"], "link_ceiling": r["link_ceiling"],
+        "link_carrier": r["config"]["link_carrier"]}
+    torch.cuda.empty_cache()
+    sub = argparse.Namespace(**vars(args))
+    sub.workload, sub.steps, sub.warmup = "cycle", 10, 2
+    r, _ = run_cycle(sub, {})
+    legs["preemption_cycle"] = {
+        "workload": WORKLOADS["cycle"], "slices_timed": sub.steps, "value": r["value"],
+        "unit": "GB/s", "ms_per_slice": r["ms_per_step"],
+        "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "peak", "frac")},
+        "kernel_ms": r["kernel_ms"], "waits_inserted": r["waits_inserted"]}
+    torch.cuda.empty_cache()
+    return legs
+
+
 def ceil_div_tokens(tokens, block_tokens):
     return -(-tokens // block_tokens)
 
@@ -1078,6 +1111,9 @@ def main():
                          "runtime's copies) or an SDMA engine index 0..15")
     ap.add_argument("--copy-reference", action="store_true",
                     help="one plain device copy of the payload size before timing")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="default workload: skip the two shorter legs reported beside it (the "
+                         "same prompt to pinned host memory, and the preemption cycle)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the swap path runs on a single MI355X "
@@ -1112,6 +1148,9 @@ def main():
         res, shape = run_next(args, common)
     else:
         res, shape = run_pair(args, common)
+    if args.workload == "llama70b_hbm" and not (args.no_secondary or args.gemm or
+                                                args.two_step or args.max_workgroups):
+        res["secondary"] = secondary_legs(args, common)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
     print(json.dumps(res), flush=True)
