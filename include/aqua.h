@@ -225,9 +225,11 @@ AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
  * event or stream.  Its run descriptors go through the pool's pinned ring
  * (allocated when the pool was created; the call never grows it) to a
  * device scratch array of 2 MiB that the library holds on each device for
- * the life of the process, and its completion event is one of those the
- * pool created (while none is spare, the call first waits for the oldest
- * outstanding call of the pool).  Differences:
+ * the life of the process, and its completion event is one of the 16 the
+ * pool created.  While none is spare (16 calls of the pool in flight), the
+ * call first blocks the host until the oldest outstanding call of the pool
+ * has completed; a caller that holds its streams from the host must not
+ * issue it then.  Differences:
  *   - at most 65536 run descriptors per call (a run is a stretch of
  *     consecutive blocks of one table, up to 64 KiB; a fragmented table has
  *     one run per block), and no more than the pool's ring holds:

@@ -62,7 +62,7 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
 // the process; host code uses only the device address that
 // hipGetSymbolAddress gives for the current device (scratch_address).
 constexpr uint64_t kScratchBytes = 2ull << 20;  // 65536 run descriptors
-constexpr uint32_t kPoolEvents = 4;              // events made at pool creation
+constexpr uint32_t kPoolEvents = 16;             // events made at pool creation
 __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 // Device address of `scratch` on `device`, looked up once per device with

@@ -158,3 +158,38 @@ def test_noalloc_descriptor_limit():
         kv.sync(0)
     finally:
         kv.close()
+
+
+def test_noalloc_recycles_its_events_past_the_pool_count():
+    """48 calls in flight on three streams with no host sync: more than the
+    16 events the pool made, so later calls wait for the oldest and reuse
+    its event.  Every byte equals the oracle run in issue order."""
+    shape = wl.KVShape(2, 2048, 2, 16, 64, wl.BF16)        # 8 KiB chunks
+    d = odesc(shape)
+    pool = device_pool(shape, 83)
+    pool_h = host(pool)
+    perm = wl.permutation(shape.num_blocks, 83)
+    img = torch.zeros(shape.image_bytes(24 * 20), dtype=torch.uint8, device="cuda")
+    img_h = np.zeros(img.numel(), dtype=np.uint8)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        calls = []
+        for k in range(24):
+            src = [perm[20 * k:20 * k + 20]]
+            dst = [perm[1024 + 20 * k:1024 + 20 * k + 20]]
+            off = [shape.image_bytes(20) * k]
+            calls.append((0, src, off))
+            calls.append((1, dst, off))
+        for i, (direction, tables, off) in enumerate(calls):
+            kv.swap_noalloc(direction, tables, img, img_offsets=off, stream=streams[i % 3])
+        kv.sync(0)
+        for direction, tables, off in calls:
+            fn = oracle.swap_in if direction else oracle.swap_out
+            assert fn(d, pool_h, tables, img_h, off) == 0
+        assert_bytes_equal(host(img), img_h, "images")
+        assert_bytes_equal(host(pool), pool_h, "pool")
+        st = kv.stats()
+        assert st["calls_out"] == 24 and st["calls_in"] == 24 and st["hip_error"] == 0
+    finally:
+        kv.close()
