@@ -110,6 +110,8 @@ struct aqua_kv_pool {
     aqua::DupMarks marks;
     HazardTracker tracker;
     std::vector<RunDesc> plan;
+    std::vector<uint32_t> sort_counts;  // scratch of aqua::sort_by_block
+    std::vector<RunDesc> sort_tmp;
     std::vector<std::pair<uint64_t, uint64_t>> ranges;
     std::vector<HazardTracker::Dep> deps;
 
@@ -868,8 +870,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
     }
     if (AQUA_SORT_RUNS && aqua::sort_runs(is_in, p->shape.C, total, p->shape.N))
-        std::sort(p->plan.begin(), p->plan.end(),
-                  [](const RunDesc& x, const RunDesc& y) { return x.block < y.block; });
+        aqua::sort_by_block(&p->plan, p->shape.N, &p->sort_counts, &p->sort_tmp);
     aqua::image_ranges(p->shape, a, &p->ranges);
     for (auto& r : p->ranges) {  // tracked by the caller's address of the buffer
         r.first += a.buf;

@@ -180,6 +180,16 @@ bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_b
     return is_in || chunk_bytes >= kSortOutMinChunk;
 }
 
+void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
+                   std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp) {
+    counts->assign((size_t)num_blocks + 1, 0);
+    for (const RunDesc& r : *runs) ++(*counts)[r.block + 1];
+    for (uint32_t b = 0; b < num_blocks; ++b) (*counts)[b + 1] += (*counts)[b];
+    tmp->resize(runs->size());
+    for (const RunDesc& r : *runs) (*tmp)[(*counts)[r.block]++] = r;
+    runs->swap(*tmp);
+}
+
 uint32_t launch_grid(uint64_t units, uint32_t max_workgroups) {
     uint64_t g = units;
     if (max_workgroups && g > max_workgroups) g = max_workgroups;

@@ -127,6 +127,14 @@ constexpr uint64_t kSortMinPermille = 400;      // share of the pool's blocks
 constexpr uint64_t kSortOutMinChunk = 64ull << 10;
 bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks);
 
+// Puts the runs in ascending order of their first block, keeping the table
+// order of runs that start at the same block (a swap-out may name a block
+// twice).  A counting sort over the pool's blocks: O(runs + num_blocks), and
+// sort_runs only asks for it when the runs number at least 40 % of the
+// blocks.  `counts` and `tmp` are reusable scratch.
+void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
+                   std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp);
+
 // Reusable scratch for duplicate detection (epoch-stamped marks, O(n)).
 struct DupMarks {
     std::vector<uint32_t> mark;

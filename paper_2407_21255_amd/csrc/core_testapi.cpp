@@ -254,6 +254,15 @@ uint32_t aqua_core_swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
     return aqua::swap_threads(chunk_bytes, min_threads);
 }
 
+// Sorts n descriptors (32 bytes each) in place by block with sort_by_block.
+void aqua_core_sort_by_block(void* descs, uint64_t n, uint32_t num_blocks) {
+    std::vector<aqua::RunDesc> v(n), tmp;
+    std::vector<uint32_t> counts;
+    if (n) std::memcpy(v.data(), descs, n * sizeof(aqua::RunDesc));
+    aqua::sort_by_block(&v, num_blocks, &counts, &tmp);
+    if (n) std::memcpy(descs, v.data(), n * sizeof(aqua::RunDesc));
+}
+
 int aqua_core_sort_runs(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
     return aqua::sort_runs(is_in != 0, chunk_bytes, blocks, num_blocks) ? 1 : 0;
 }

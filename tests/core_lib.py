@@ -72,6 +72,7 @@ def lib():
                                              ctypes.POINTER(u64)]
         L.aqua_core_swap_threads.argtypes = [u64, u32]
         L.aqua_core_swap_threads.restype = u32
+        L.aqua_core_sort_by_block.argtypes = [P, u64, u32]
         L.aqua_core_sort_runs.argtypes = [i32, u64, u64, u32]
         L.aqua_core_sort_runs.restype = i32
         L.aqua_core_launch_grid.argtypes = [u64, u32]
@@ -262,3 +263,10 @@ def tracker_soak(n_calls: int, num_blocks: int, streams: int, rotate: int, depth
 
 def sort_runs(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int) -> bool:
     return bool(lib().aqua_core_sort_runs(int(is_in), chunk_bytes, blocks, num_blocks))
+
+
+def sort_by_block(descs: np.ndarray, num_blocks: int) -> np.ndarray:
+    """The core's counting sort of RUN_DESC records by block (a copy)."""
+    out = np.ascontiguousarray(descs.copy())
+    lib().aqua_core_sort_by_block(out.ctypes.data if len(out) else None, len(out), num_blocks)
+    return out

@@ -247,3 +247,23 @@ def test_run_order_rule():
     assert not sort_runs(True, 32 * K, 4168, 16384)     # preemption cycle: a quarter
     assert sort_runs(True, 64 * K, 1639, 4096) and not sort_runs(True, 64 * K, 1638, 4096)
     assert not sort_runs(True, 64 * K, 0, 0)
+
+
+def test_sort_by_block_matches_a_stable_sort():
+    """The counting sort gives the runs in ascending block order and keeps
+    table order among runs that start at the same block (swap-outs may name
+    a block twice), on random plans with and without repeats."""
+    import numpy as np
+    from tests.core_lib import RUN_DESC, sort_by_block
+    rng = np.random.default_rng(5)
+    for trial in range(200):
+        n = int(rng.integers(0, 300))
+        N = int(rng.integers(1, 400))
+        d = np.zeros(n, dtype=RUN_DESC)
+        d["block"] = rng.integers(0, N, n)
+        d["img_off"] = np.arange(n) * 4096            # table order, to check stability
+        d["nchunks"] = rng.integers(1, 5, n)
+        got = sort_by_block(d, N)
+        want = d[np.argsort(d["block"], kind="stable")]
+        assert got.tobytes() == want.tobytes(), trial
+    assert len(sort_by_block(np.zeros(0, dtype=RUN_DESC), 7)) == 0
