@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "0841550f7ec774d2"): {
-        "gather (swap-out)": 21477244003, "scatter (swap-in)": 21476787301},
-    ("llama8b_hbm", "0841550f7ec774d2"): {
-        "gather (swap-out)": 4295911619, "scatter (swap-in)": 4295802976},
-    ("llama70b_tp2_hbm", "0841550f7ec774d2"): {
-        "gather (swap-out)": 10739820638, "scatter (swap-in)": 10739311099},
-    ("llama70b_tp4_hbm", "0841550f7ec774d2"): {
-        "gather (swap-out)": 5369606439, "scatter (swap-in)": 5369285727},
-    ("llama8b_fp8_hbm", "0841550f7ec774d2"): {
-        "gather (swap-out)": 2148158965, "scatter (swap-in)": 2148148615},
+    ("llama70b_hbm", "e25819ab6c849ab9"): {
+        "gather (swap-out)": 21477169353, "scatter (swap-in)": 21476763032},
+    ("llama8b_hbm", "e25819ab6c849ab9"): {
+        "gather (swap-out)": 4295896873, "scatter (swap-in)": 4295758022},
+    ("llama70b_tp2_hbm", "e25819ab6c849ab9"): {
+        "gather (swap-out)": 10739876856, "scatter (swap-in)": 10739503509},
+    ("llama70b_tp4_hbm", "e25819ab6c849ab9"): {
+        "gather (swap-out)": 5369623949, "scatter (swap-in)": 5369285932},
+    ("llama8b_fp8_hbm", "e25819ab6c849ab9"): {
+        "gather (swap-out)": 2148160194, "scatter (swap-in)": 2148143086},
 }
 
 # Every source that decides what the swap kernels do and how they are

@@ -907,9 +907,9 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     if (dbytes) {
         const auto w0 = std::chrono::steady_clock::now();
         st = ring_reserve(p, dbytes, &ring_off, !noalloc);
-        waited_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
-                        std::chrono::steady_clock::now() - w0)
-                        .count();
+        waited_ns += (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                         std::chrono::steady_clock::now() - w0)
+                         .count();
         if (st != AQUA_OK) {
             give_back();
             return st;
