@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "e25819ab6c849ab9"): {
-        "gather (swap-out)": 21477169353, "scatter (swap-in)": 21476763032},
-    ("llama8b_hbm", "e25819ab6c849ab9"): {
-        "gather (swap-out)": 4295896873, "scatter (swap-in)": 4295758022},
-    ("llama70b_tp2_hbm", "e25819ab6c849ab9"): {
-        "gather (swap-out)": 10739876856, "scatter (swap-in)": 10739503509},
-    ("llama70b_tp4_hbm", "e25819ab6c849ab9"): {
-        "gather (swap-out)": 5369623949, "scatter (swap-in)": 5369285932},
-    ("llama8b_fp8_hbm", "e25819ab6c849ab9"): {
-        "gather (swap-out)": 2148160194, "scatter (swap-in)": 2148143086},
+    ("llama70b_hbm", "3422048267d3bf17"): {
+        "gather (swap-out)": 21477213692, "scatter (swap-in)": 21476730776},
+    ("llama8b_hbm", "3422048267d3bf17"): {
+        "gather (swap-out)": 4295931177, "scatter (swap-in)": 4295796729},
+    ("llama70b_tp2_hbm", "3422048267d3bf17"): {
+        "gather (swap-out)": 10739804971, "scatter (swap-in)": 10739346734},
+    ("llama70b_tp4_hbm", "3422048267d3bf17"): {
+        "gather (swap-out)": 5369633473, "scatter (swap-in)": 5369288799},
+    ("llama8b_fp8_hbm", "3422048267d3bf17"): {
+        "gather (swap-out)": 2148165621, "scatter (swap-in)": 2148153121},
 }
 
 # Every source that decides what the swap kernels do and how they are

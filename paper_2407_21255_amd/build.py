@@ -57,7 +57,7 @@ def build_hip(out: str = HIP_LIB, extra=()) -> str:
         srcs += (["-x", "hip", p] if s.endswith(".hip") else ["-x", "c++", p])
     tmp = out + ".tmp"
     _run([HIPCC, *HIP_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp,
-          "-L/opt/rocm/lib", "-lhsa-runtime64"])
+          "-L/opt/rocm/lib", "-lhsa-runtime64", "-lrocprofiler-sdk-roctx"])
     os.replace(tmp, out)
     return out
 

@@ -14,6 +14,8 @@
 #include <set>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "aqua.h"
 #include "aqua_core.h"
 #include "link_engine.h"
@@ -47,6 +49,16 @@ constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 #ifndef AQUA_SORT_RUNS
 #define AQUA_SORT_RUNS 1
 #endif
+
+// Names one library call on the host timeline of a profiler that records
+// markers (rocprofv3 --marker-trace); with none attached a push and a pop
+// cost a function call each.
+struct TraceRange {
+    explicit TraceRange(const char* name) { roctxRangePushA(name); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange&) = delete;
+    TraceRange& operator=(const TraceRange&) = delete;
+};
 
 uint64_t env_u64(const char* name, uint64_t dflt) {
     const char* v = std::getenv(name);
@@ -1182,6 +1194,7 @@ extern "C" {
 
 aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
                                 uint64_t pool_bytes, aqua_kv_pool_t* out) {
+    TraceRange trace("aqua_kv_pool_create");
     if (!out) return AQUA_ERR_INVALID;
     aqua::Shape s;
     aqua_status st = aqua::make_shape(desc, &s);
@@ -1248,6 +1261,7 @@ aqua_status aqua_kv_pool_create(const aqua_kv_desc* desc, void* pool_base,
 }
 
 aqua_status aqua_kv_pool_destroy(aqua_kv_pool_t p) {
+    TraceRange trace("aqua_kv_pool_destroy");
     if (!p) return AQUA_ERR_INVALID;
     aqua_status st = AQUA_OK;
     {
@@ -1287,6 +1301,7 @@ aqua_status aqua_swap_out(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t*
                           const uint64_t* seq_offsets, void* dst, uint64_t dst_bytes,
                           const uint64_t* img_offsets, int32_t target, void* stream,
                           uint64_t* ticket) {
+    TraceRange trace("aqua_swap_out");
     return do_swap(pool, false, num_seqs, block_ids, seq_offsets, dst, dst_bytes, img_offsets,
                    nullptr, target, stream, ticket);
 }
@@ -1295,6 +1310,7 @@ aqua_status aqua_swap_in(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_t* 
                          const uint64_t* seq_offsets, const void* src, uint64_t src_bytes,
                          const uint64_t* img_offsets, int32_t target, void* stream,
                          uint64_t* ticket) {
+    TraceRange trace("aqua_swap_in");
     return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
                    nullptr, target, stream, ticket);
 }
@@ -1303,6 +1319,7 @@ aqua_status aqua_swap_out_ex(aqua_kv_pool_t pool, uint32_t num_seqs, const int32
                              const uint64_t* seq_offsets, void* dst, uint64_t dst_bytes,
                              const uint64_t* img_offsets, const aqua_swap_range* range,
                              int32_t target, void* stream, uint64_t* ticket) {
+    TraceRange trace("aqua_swap_out_ex");
     return do_swap(pool, false, num_seqs, block_ids, seq_offsets, dst, dst_bytes, img_offsets,
                    range, target, stream, ticket);
 }
@@ -1311,6 +1328,7 @@ aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs, const int32_
                             const uint64_t* seq_offsets, const void* src, uint64_t src_bytes,
                             const uint64_t* img_offsets, const aqua_swap_range* range,
                             int32_t target, void* stream, uint64_t* ticket) {
+    TraceRange trace("aqua_swap_in_ex");
     return do_swap(pool, true, num_seqs, block_ids, seq_offsets, src, src_bytes, img_offsets,
                    range, target, stream, ticket);
 }
@@ -1319,6 +1337,7 @@ aqua_status aqua_swap_noalloc(aqua_kv_pool_t pool, int32_t direction, uint32_t n
                               const int32_t* block_ids, const uint64_t* seq_offsets, void* buf,
                               uint64_t buf_bytes, const uint64_t* img_offsets, int32_t target,
                               void* stream, uint64_t* ticket) {
+    TraceRange trace("aqua_swap_noalloc");
     if (direction != 0 && direction != 1) return AQUA_ERR_INVALID;
     return do_swap(pool, direction == 1, num_seqs, block_ids, seq_offsets, buf, buf_bytes,
                    img_offsets, nullptr, target, stream, ticket, true);
@@ -1328,11 +1347,13 @@ aqua_status aqua_migrate(aqua_kv_pool_t pool, const void* src, uint64_t src_byte
                          int32_t src_target, void* dst, uint64_t dst_bytes, int32_t dst_target,
                          uint32_t n, const uint64_t* src_offsets, const uint64_t* dst_offsets,
                          const uint64_t* lengths, void* stream, uint64_t* ticket) {
+    TraceRange trace("aqua_migrate");
     return do_migrate(pool, src, src_bytes, src_target, dst, dst_bytes, dst_target, n,
                       src_offsets, dst_offsets, lengths, stream, ticket);
 }
 
 aqua_status aqua_sync(aqua_kv_pool_t p, uint64_t ticket) {
+    TraceRange trace("aqua_sync");
     if (!p) return AQUA_ERR_INVALID;
     if (ticket >= p->next_ticket) return AQUA_ERR_INVALID;
     if (p->sticky != hipSuccess) return AQUA_ERR_HIP;
@@ -1343,6 +1364,7 @@ aqua_status aqua_sync(aqua_kv_pool_t p, uint64_t ticket) {
 }
 
 aqua_status aqua_stream_wait(aqua_kv_pool_t p, uint64_t ticket, void* stream) {
+    TraceRange trace("aqua_stream_wait");
     if (!p) return AQUA_ERR_INVALID;
     if (ticket >= p->next_ticket) return AQUA_ERR_INVALID;
     if (p->sticky != hipSuccess) return AQUA_ERR_STATE;
@@ -1416,6 +1438,7 @@ aqua_status aqua_pool_stats_get(aqua_kv_pool_t p, aqua_pool_stats* out) {
 
 aqua_status aqua_swap_space_create(aqua_kv_pool_t pool, uint64_t device_bytes,
                                    uint64_t host_bytes, aqua_swap_space_t* out) {
+    TraceRange trace("aqua_swap_space_create");
     if (!pool || !out) return AQUA_ERR_INVALID;
     if (pool->sticky != hipSuccess) return AQUA_ERR_STATE;
     DeviceGuard dg(pool->device);
@@ -1445,6 +1468,7 @@ aqua_status aqua_swap_space_create(aqua_kv_pool_t pool, uint64_t device_bytes,
 }
 
 aqua_status aqua_swap_space_destroy(aqua_swap_space_t s) {
+    TraceRange trace("aqua_swap_space_destroy");
     if (!s) return AQUA_ERR_INVALID;
     aqua_status st = AQUA_OK;
     {
@@ -1494,6 +1518,7 @@ aqua_status aqua_swap_locate(aqua_swap_space_t s, uint64_t handle, void** ptr, u
 
 aqua_status aqua_swap_reclaim(aqua_swap_space_t s, uint64_t bytes, void* stream,
                               uint64_t* ticket) {
+    TraceRange trace("aqua_swap_reclaim");
     if (!s) return AQUA_ERR_INVALID;
     if (ticket) *ticket = 0;
     auto& dev = s->ranges[AQUA_TARGET_DEVICE];
@@ -1517,6 +1542,7 @@ aqua_status aqua_swap_reclaim(aqua_swap_space_t s, uint64_t bytes, void* stream,
 }
 
 aqua_status aqua_swap_restore(aqua_swap_space_t s, void* stream, uint64_t* ticket) {
+    TraceRange trace("aqua_swap_restore");
     if (!s) return AQUA_ERR_INVALID;
     if (ticket) *ticket = 0;
     auto& dev = s->ranges[AQUA_TARGET_DEVICE];
@@ -1544,6 +1570,7 @@ aqua_status aqua_swap_usage(aqua_swap_space_t s, uint64_t* device_free, uint64_t
 
 aqua_status aqua_hbm_yardstick(int32_t kind, void* dst, const void* src, uint64_t bytes,
                                void* stream) {
+    TraceRange trace("aqua_hbm_yardstick");
     if (kind != AQUA_YARDSTICK_COPY && kind != AQUA_YARDSTICK_READ &&
         kind != AQUA_YARDSTICK_WRITE)
         return AQUA_ERR_INVALID;
