@@ -50,6 +50,12 @@
  * swap call returns AQUA_ERR_STATE.  Copy-engine work of the failed call is
  * never left waiting on the engine, whose queue other pools may share.
  *
+ * Streams: the library tells streams apart by their handle, so a stream must
+ * not be destroyed while calls issued on it are outstanding (a new stream
+ * could get the same handle).  Any number of distinct streams may be used
+ * over a pool's life: a stream whose calls have all completed gives up its
+ * place in the pool's bookkeeping to the next new one.
+ *
  * Threads: a pool handle is used from one thread at a time.  Separate pools
  * are independent (but do not order against each other).  A pool whose
  * host-link copies run on an SDMA engine (aqua_kv_pool_set_link_engine)

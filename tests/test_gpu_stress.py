@@ -6,6 +6,7 @@ every call is several copy-engine jobs, or swapped zero-copy; or it is in
 HBM.  The library must behave as if the calls ran in issue order: pool,
 arena and region at the end equal the oracle run call by call in that
 order."""
+import ctypes
 import os
 
 import numpy as np
@@ -123,3 +124,73 @@ def test_random_calls_on_four_streams(monkeypatch, path, seed):
     assert_bytes_equal(host(pool), pool_h, "pool")
     assert_bytes_equal(host(arena), arena_h, "arena")
     assert_bytes_equal(host(region), region_h, "device region")
+
+
+@pytest.mark.gpu
+def test_random_calls_on_rotating_streams():
+    """The stream set changes as the calls go: call i runs on one of the
+    four streams of a window that moves on by one stream every five calls,
+    over 64 streams made for the test (plain HIP streams, so every handle
+    is new).  The library hands lanes whose calls have all completed to
+    streams it has not seen, and must still order conflicting calls across
+    them: pool, arena and region equal the oracle run in issue order."""
+    from tests.gpu_util import _hip_runtime
+    hip = _hip_runtime()
+    hip.hipStreamCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    handles = []
+    for _ in range(64):
+        h = ctypes.c_void_p()
+        assert hip.hipStreamCreateWithFlags(ctypes.byref(h), 1) == 0   # non-blocking
+        handles.append(h.value)
+    shape = wl.KVShape(4, 256, 2, 16, 64, wl.BF16)                # 8 KiB chunks
+    d = odesc(shape)
+    rng = np.random.default_rng(9)
+    pool = device_pool(shape, 49)
+    arena = torch.from_numpy(rng.integers(0, 256, size=ARENA, dtype=np.uint8)).cuda()
+    region = torch.from_numpy(rng.integers(0, 256, size=REGION, dtype=np.uint8)).cuda()
+    pool_h, arena_h, region_h = host(pool), host(arena).copy(), host(region)
+    ops = _ops(shape, rng, 300)
+    torch.cuda.synchronize()
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        for i, (kind, si, args) in enumerate(ops):
+            s = handles[(i // 5 + si) % len(handles)]
+            if kind == "out":
+                table, off, size = args
+                kv.swap_out([table], arena[off:off + size], stream=s)
+            elif kind == "in":
+                table, off, size = args
+                kv.swap_in([table], arena[off:off + size], stream=s)
+            elif kind == "to_host":
+                ao, ro, lens = args
+                kv.migrate(region, arena, ro, ao, lens, stream=s)
+            else:
+                ao, ro, lens = args
+                kv.migrate(arena, region, ao, ro, lens, stream=s)
+        st = kv.stats()
+        kv.sync()
+        say("rotating streams: waits inserted", st["waits_inserted"], "elided",
+            st["waits_elided"])
+    finally:
+        kv.close()
+        torch.cuda.synchronize()
+        for h in handles:
+            hip.hipStreamDestroy(ctypes.c_void_p(h))
+    for kind, _, args in ops:
+        if kind == "out":
+            table, off, size = args
+            assert oracle.swap_out(d, pool_h, [table], arena_h[off:off + size]) == 0
+        elif kind == "in":
+            table, off, size = args
+            assert oracle.swap_in(d, pool_h, [table], arena_h[off:off + size]) == 0
+        elif kind == "to_host":
+            ao, ro, lens = args
+            assert oracle.migrate(region_h, arena_h, ro, ao, lens) == 0
+        else:
+            ao, ro, lens = args
+            assert oracle.migrate(arena_h, region_h, ao, ro, lens) == 0
+    assert_bytes_equal(host(pool), pool_h, "pool")
+    assert_bytes_equal(host(arena), arena_h, "arena")
+    assert_bytes_equal(host(region), region_h, "device region")
+    assert st["waits_inserted"] > 0
