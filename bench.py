@@ -35,20 +35,20 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 --pmc
 # (FETCH_SIZE, WRITE_SIZE), each scaled by the same counters' reading for a
-# plain copy of known size.  Keyed by _kernel_hash(): a change to the kernels
+# plain copy of known size (a call split into several launches: per launch).  Keyed by _kernel_hash(): a change to the kernels
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "3422048267d3bf17"): {
-        "gather (swap-out)": 21477213692, "scatter (swap-in)": 21476730776},
-    ("llama8b_hbm", "3422048267d3bf17"): {
-        "gather (swap-out)": 4295931177, "scatter (swap-in)": 4295796729},
-    ("llama70b_tp2_hbm", "3422048267d3bf17"): {
-        "gather (swap-out)": 10739804971, "scatter (swap-in)": 10739346734},
-    ("llama70b_tp4_hbm", "3422048267d3bf17"): {
-        "gather (swap-out)": 5369633473, "scatter (swap-in)": 5369288799},
-    ("llama8b_fp8_hbm", "3422048267d3bf17"): {
-        "gather (swap-out)": 2148165621, "scatter (swap-in)": 2148153121},
+    ("llama70b_hbm", "7a3f1174d6cecb85"): {
+        "gather (swap-out)": 21477193110, "scatter (swap-in)": 21476689304},
+    ("llama8b_hbm", "7a3f1174d6cecb85"): {
+        "gather (swap-out)": 4295909878, "scatter (swap-in)": 4295782905},
+    ("llama70b_tp2_hbm", "7a3f1174d6cecb85"): {
+        "gather (swap-out)": 1074662352, "scatter (swap-in)": 1074440146},
+    ("llama70b_tp4_hbm", "7a3f1174d6cecb85"): {
+        "gather (swap-out)": 5369621799, "scatter (swap-in)": 5369291461},
+    ("llama8b_fp8_hbm", "7a3f1174d6cecb85"): {
+        "gather (swap-out)": 1074142713, "scatter (swap-in)": 1074327434},
 }
 
 # Every source that decides what the swap kernels do and how they are
@@ -367,6 +367,10 @@ def run_pair(args, res_common):
     else:
         bound, peak, alg = "hbm", HBM_PEAK_GBS, 2 * payload
     achieved = alg / (dom_ms.mean() * 1e-3) / 1e9
+    # A call may be carried by several launches of the kernel (whole layers
+    # each); the roofline is stated per launch, as a kernel trace lists it.
+    calls = max(1, st["calls_out"] + st["calls_in"])
+    per_call = st["launches"] / calls
     khash = _kernel_hash(max_workgroups=args.max_workgroups)
     res = dict(res_common)
     res.update({
@@ -391,7 +395,9 @@ def run_pair(args, res_common):
             "unit": "GB/s", "frac": round(achieved / peak, 4),
             "traffic": (None if two_step else
                         MEASURED_TRAFFIC.get((args.workload, khash), {}).get(dom)),
-            "algorithmic_bytes_per_launch": alg,
+            "algorithmic_bytes_per_launch": round(alg / per_call) if per_call else alg,
+            "launches_per_call": round(per_call, 3),
+            "launch_ms_mean": round(float(dom_ms.mean()) / per_call, 4) if per_call else None,
         },
         "kernel_ms": {"swap_out_mean": round(float(out_ms.mean()), 4),
                       "swap_out_min": round(float(out_ms.min()), 4),

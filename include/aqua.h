@@ -132,6 +132,11 @@ typedef struct {
                                              used by earlier calls is free */
     int32_t hip_error;                    /* latched hipError_t, 0 if none */
     int32_t reserved;
+    uint64_t launches;                    /* gather and scatter kernel launches
+                                             (a call may take several: one per
+                                             layer group of a staged call, and
+                                             calls of 16..64 KiB chunks to an
+                                             HBM buffer in pieces of 512 MiB) */
 } aqua_pool_stats;
 
 /* Bind a pool to caller-owned device memory.

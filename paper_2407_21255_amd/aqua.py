@@ -72,7 +72,8 @@ class aqua_pool_stats(ctypes.Structure):
         "calls_out", "calls_in", "bytes_out", "bytes_in", "bytes_host",
         "descriptors", "waits_inserted", "waits_elided", "calls_migrate",
         "bytes_migrated", "host_ns", "wait_ns")] + [
-        ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+        ("hip_error", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("launches", ctypes.c_uint64)]
 
 
 class aqua_cfs_request(ctypes.Structure):

@@ -597,6 +597,8 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     L.max_workgroups = p->max_wg[target];
     L.nt_pool_store = aqua::nt_pool_store(p->shape.C, (uint64_t)nl * p->call_blocks * p->shape.C);
     L.threads = aqua::swap_threads(p->shape.C, AQUA_MIN_THREADS);
+    L.layer_bytes = p->call_blocks * p->shape.C;
+    L.max_launch_bytes = target == AQUA_TARGET_DEVICE ? aqua::max_launch_bytes(p->shape.C) : 0;
     return L;
 }
 
@@ -688,13 +690,15 @@ aqua_status enqueue_staged_runtime(aqua_kv_pool* p, bool is_in, const void* buf,
             if ((e = copies(pieces)) != hipSuccess) return latch(p, e);
         } else {
             (void)hipGetLastError();
-            if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
+            if ((e = aqua::launch_swap(Lk, stream, &p->stats.launches)) != hipSuccess)
+                return latch(p, e);
         }
         if ((e = hipEventRecord(e1, first)) != hipSuccess) return latch(p, e);
         if ((e = hipStreamWaitEvent(second, e1, 0)) != hipSuccess) return latch(p, e);
         if (is_in) {
             (void)hipGetLastError();
-            if ((e = aqua::launch_swap(Lk, stream)) != hipSuccess) return latch(p, e);
+            if ((e = aqua::launch_swap(Lk, stream, &p->stats.launches)) != hipSuccess)
+                return latch(p, e);
         } else {
             if ((e = copies(pieces)) != hipSuccess) return latch(p, e);
         }
@@ -749,7 +753,8 @@ aqua_status enqueue_staged_engine(aqua_kv_pool* p, bool is_in, const void* buf,
         uint32_t l0, nl;
         uint8_t* s = group(k, &l0, &nl);
         (void)hipGetLastError();
-        return aqua::launch_swap(slot_launch(p, is_in, s, descs, ndesc, l0, nl), stream);
+        return aqua::launch_swap(slot_launch(p, is_in, s, descs, ndesc, l0, nl), stream,
+                                 &p->stats.launches);
     };
     // A flag is held from its job's submission until its release kernel is
     // enqueued; a failure in between hands it to fail_held.
@@ -990,7 +995,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
                             (uint32_t)p->plan.size(), target, l_begin, l_count);
             (void)hipGetLastError();
-            e = aqua::launch_swap(L, stream);
+            e = aqua::launch_swap(L, stream, &p->stats.launches);
             if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));
         }
     }

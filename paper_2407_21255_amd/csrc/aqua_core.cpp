@@ -190,6 +190,17 @@ void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
     runs->swap(*tmp);
 }
 
+uint64_t max_launch_bytes(uint64_t chunk_bytes) {
+    return (chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk) ? kSplitLaunchBytes
+                                                                           : 0;
+}
+
+uint32_t layers_per_launch(uint32_t ndesc, uint64_t layer_bytes, uint64_t max_bytes) {
+    uint64_t per = std::max<uint64_t>(1, (1ull << 31) / std::max<uint32_t>(1, ndesc));
+    if (max_bytes && layer_bytes) per = std::min(per, std::max<uint64_t>(1, max_bytes / layer_bytes));
+    return (uint32_t)std::min<uint64_t>(per, UINT32_MAX);
+}
+
 uint32_t launch_grid(uint64_t units, uint32_t max_workgroups) {
     uint64_t g = units;
     if (max_workgroups && g > max_workgroups) g = max_workgroups;

@@ -135,6 +135,24 @@ bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_b
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
                    std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp);
 
+// Launch size, measured on MI355X.  An HBM-target call of chunks between 16
+// and 64 KiB is carried by launches of at most 512 MiB of payload each (whole
+// layers, one after another on the stream); other calls by one launch.  At
+// 32 KiB: one TP2 rank's 5 GiB swaps 5 % shorter, the fp8 preemption cycle
+// (about 4.4 GB per call) 3-4 % shorter, the fp8 8B pool's 1 GiB calls
+// unchanged; pieces of 1-2 GiB gained less, of 64-256 MiB less or lost.
+// Split the same way, 64 KiB calls (70B, 8B) and 16 KiB calls (TP4) ran
+// 1-6 % longer.  0: no limit.
+constexpr uint64_t kSplitMinChunk = 16ull << 10;  // exclusive
+constexpr uint64_t kSplitMaxChunk = 64ull << 10;  // exclusive
+constexpr uint64_t kSplitLaunchBytes = 512ull << 20;
+uint64_t max_launch_bytes(uint64_t chunk_bytes);
+
+// Layers per launch of a call with `ndesc` runs per layer and `layer_bytes`
+// of payload per layer: fewer than 2^31 units per launch, and at most
+// `max_bytes` of payload when that is non-zero (but at least one layer).
+uint32_t layers_per_launch(uint32_t ndesc, uint64_t layer_bytes, uint64_t max_bytes);
+
 // Reusable scratch for duplicate detection (epoch-stamped marks, O(n)).
 struct DupMarks {
     std::vector<uint32_t> mark;

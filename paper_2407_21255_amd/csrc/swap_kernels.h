@@ -23,6 +23,8 @@ struct SwapLaunch {
     uint32_t max_workgroups;  // 0: one workgroup per (layer, run)
     bool nt_pool_store;       // scatter: nontemporal stores into the pool
     uint32_t threads;         // lanes per workgroup: 64, 128, 256, 512 or 1024
+    uint64_t layer_bytes;     // payload of one layer of the call (its runs' chunks)
+    uint64_t max_launch_bytes;  // 0: one launch, else whole layers up to this payload
 };
 
 // Scatter store hint, measured on MI355X.  Nontemporal pool stores pay for
@@ -38,8 +40,9 @@ inline bool nt_pool_store(uint64_t chunk_bytes, uint64_t launch_bytes) {
     return chunk_bytes >= kNtPoolStoreMinChunk || launch_bytes >= kNtPoolStoreMinBytes;
 }
 
-// Enqueues the copy on `stream`; returns the first launch error.
-hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream);
+// Enqueues the copy on `stream`; returns the first launch error.  Adds the
+// number of kernel launches it made to *launches when that is given.
+hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream, uint64_t* launches = nullptr);
 
 // Enqueues one HBM yardstick over `bytes` (a multiple of 16) of device
 // memory with the swap kernels' copy loop: mode 0 copies src to dst, mode 1

@@ -201,10 +201,11 @@ hipError_t launch_copy(const uint8_t* src, uint8_t* dst, const CopyDesc* descs, 
     return hipGetLastError();
 }
 
-hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
+hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream, uint64_t* launches) {
     if (!a.ndesc || !a.num_layers) return hipSuccess;
-    // Split by layers so that every launch has fewer than 2^31 units.
-    const uint32_t per = (uint32_t)std::max<uint64_t>(1, (1ull << 31) / a.ndesc);
+    // Whole layers per launch: fewer than 2^31 units, and at most
+    // max_launch_bytes of payload when that is set.
+    const uint32_t per = layers_per_launch(a.ndesc, a.layer_bytes, a.max_launch_bytes);
     const uint32_t end = a.first_layer + a.num_layers;
     for (uint32_t l0 = a.first_layer; l0 < end; l0 += per) {
         const uint32_t nl = std::min<uint32_t>(per, end - l0);
@@ -220,6 +221,7 @@ hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream) {
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if (launches) ++*launches;
     }
     return hipSuccess;
 }

@@ -75,6 +75,10 @@ def lib():
         L.aqua_core_sort_by_block.argtypes = [P, u64, u32]
         L.aqua_core_sort_runs.argtypes = [i32, u64, u64, u32]
         L.aqua_core_sort_runs.restype = i32
+        L.aqua_core_max_launch_bytes.argtypes = [u64]
+        L.aqua_core_max_launch_bytes.restype = u64
+        L.aqua_core_layers_per_launch.argtypes = [u32, u64, u64]
+        L.aqua_core_layers_per_launch.restype = u32
         L.aqua_core_launch_grid.argtypes = [u64, u32]
         L.aqua_core_launch_grid.restype = u32
         L.aqua_core_tracker_live_ranges.restype = u64
@@ -270,3 +274,11 @@ def sort_by_block(descs: np.ndarray, num_blocks: int) -> np.ndarray:
     out = np.ascontiguousarray(descs.copy())
     lib().aqua_core_sort_by_block(out.ctypes.data if len(out) else None, len(out), num_blocks)
     return out
+
+
+def max_launch_bytes(chunk_bytes: int) -> int:
+    return int(lib().aqua_core_max_launch_bytes(chunk_bytes))
+
+
+def layers_per_launch(ndesc: int, layer_bytes: int, max_bytes: int) -> int:
+    return int(lib().aqua_core_layers_per_launch(ndesc, layer_bytes, max_bytes))

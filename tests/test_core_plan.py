@@ -267,3 +267,23 @@ def test_sort_by_block_matches_a_stable_sort():
         want = d[np.argsort(d["block"], kind="stable")]
         assert got.tobytes() == want.tobytes(), trial
     assert len(sort_by_block(np.zeros(0, dtype=RUN_DESC), 7)) == 0
+
+
+def test_launch_size_rule():
+    """Calls of chunks between 16 and 64 KiB go out in launches of at most
+    512 MiB of whole layers; others in one launch (up to 2^31 units)."""
+    from tests.core_lib import layers_per_launch, max_launch_bytes
+    K, M = 1 << 10, 1 << 20
+    assert max_launch_bytes(32 * K) == 512 * M
+    assert max_launch_bytes(48 * K) == 512 * M
+    assert max_launch_bytes(16 * K) == 0 and max_launch_bytes(64 * K) == 0
+    assert max_launch_bytes(48) == 0 and max_launch_bytes(1 << 20) == 0
+    # One TP2 rank: 2048 runs of 32 KiB per layer, 64 MiB per layer -> 8 layers.
+    assert layers_per_launch(2048, 64 * M, 512 * M) == 8
+    # The preemption cycle: about 136 MB per layer -> 3 layers.
+    assert layers_per_launch(4168, 4168 * 32 * K, 512 * M) == 3
+    # A layer larger than the limit still goes out whole.
+    assert layers_per_launch(100, 600 * M, 512 * M) == 1
+    # No limit: only the 2^31-unit bound.
+    assert layers_per_launch(2048, 64 * M, 0) == (1 << 31) // 2048
+    assert layers_per_launch(1 << 31, 1, 0) == 1
