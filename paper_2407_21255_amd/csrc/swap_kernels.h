@@ -28,16 +28,19 @@ struct SwapLaunch {
 };
 
 // Scatter store hint, measured on MI355X.  Nontemporal pool stores pay for
-// large chunks and for launches that write much more than the 256 MB
-// last-level cache holds.  A smaller launch of smaller chunks ends sooner with
-// ordinary stores, which L2 and that cache partly absorb:
-//   64 KiB chunks: 0-7 % shorter with nontemporal stores, 2 to 10 GiB launches;
-//   32 KiB chunks: 10 % longer at 1 GiB per launch, 0.5-2 % shorter at 4.4-5 GiB;
-//   16 KiB chunks: 20 % longer at 512 MiB per launch, 7 % shorter at 2.5 GiB.
+// large chunks and for calls that write much more than the 256 MB last-level
+// cache holds.  A smaller call of smaller chunks ends sooner with ordinary
+// stores, which L2 and that cache partly absorb:
+//   64 KiB chunks: 0-7 % shorter with nontemporal stores, 2 to 10 GiB calls;
+//   32 KiB chunks: 10 % longer at 1 GiB per call, 0.5-2 % shorter at 4.4-5 GiB;
+//   16 KiB chunks: 20 % longer at 512 MiB per call, 7 % shorter at 2.5 GiB.
+// The bytes are the whole call's, also when several launches carry it: ordinary
+// stores chosen for each 512 MiB launch of a larger call made its scatter
+// 2-15 % longer.
 constexpr uint64_t kNtPoolStoreMinChunk = 64ull << 10;
 constexpr uint64_t kNtPoolStoreMinBytes = 2ull << 30;
-inline bool nt_pool_store(uint64_t chunk_bytes, uint64_t launch_bytes) {
-    return chunk_bytes >= kNtPoolStoreMinChunk || launch_bytes >= kNtPoolStoreMinBytes;
+inline bool nt_pool_store(uint64_t chunk_bytes, uint64_t call_bytes) {
+    return chunk_bytes >= kNtPoolStoreMinChunk || call_bytes >= kNtPoolStoreMinBytes;
 }
 
 // Enqueues the copy on `stream`; returns the first launch error.  Adds the
