@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "7a3f1174d6cecb85"): {
-        "gather (swap-out)": 21477193110, "scatter (swap-in)": 21476689304},
-    ("llama8b_hbm", "7a3f1174d6cecb85"): {
-        "gather (swap-out)": 4295909878, "scatter (swap-in)": 4295782905},
-    ("llama70b_tp2_hbm", "7a3f1174d6cecb85"): {
-        "gather (swap-out)": 1074662352, "scatter (swap-in)": 1074440146},
-    ("llama70b_tp4_hbm", "7a3f1174d6cecb85"): {
-        "gather (swap-out)": 5369621799, "scatter (swap-in)": 5369291461},
-    ("llama8b_fp8_hbm", "7a3f1174d6cecb85"): {
-        "gather (swap-out)": 1074142713, "scatter (swap-in)": 1074327434},
+    ("llama70b_hbm", "e616aeea13c11358"): {
+        "gather (swap-out)": 21477201711, "scatter (swap-in)": 21476722584},
+    ("llama8b_hbm", "e616aeea13c11358"): {
+        "gather (swap-out)": 4295897897, "scatter (swap-in)": 4295790483},
+    ("llama70b_tp2_hbm", "e616aeea13c11358"): {
+        "gather (swap-out)": 1074663130, "scatter (swap-in)": 1074436828},
+    ("llama70b_tp4_hbm", "e616aeea13c11358"): {
+        "gather (swap-out)": 5369607463, "scatter (swap-in)": 5369283986},
+    ("llama8b_fp8_hbm", "e616aeea13c11358"): {
+        "gather (swap-out)": 1074138104, "scatter (swap-in)": 1074329379},
 }
 
 # Every source that decides what the swap kernels do and how they are
