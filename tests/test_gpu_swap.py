@@ -179,6 +179,52 @@ def test_more_units_than_one_dispatch_can_count():
     _roundtrip(shape, 67, out_tables, in_tables, None)
 
 
+def test_split_launches_over_layer_ranges():
+    """32 KiB chunks to an HBM buffer: a call is carried by launches of whole
+    layers that move at most 512 MiB each (3 layers of 4500 chunks here).
+    Whole calls and layer ranges that the split cuts (layers 1-7 go out as
+    launches of layers 1-3, 4-6 and 7) match the oracle byte for byte, guard
+    bytes included, the swap-ins in pool order (they cover 49 % of the
+    pool), and the pool counts the launches it made."""
+    shape = wl.KVShape(10, 9216, 8, 16, 128, wl.FP8_E4M3)    # 32 KiB chunks, 2.8 GiB
+    C = shape.chunk_bytes
+    assert C == 32 << 10
+    d = odesc(shape)
+    perm = wl.permutation(shape.num_blocks, 71)
+    out_t = [perm[:2500], perm[2500:4500]]
+    in_t = [perm[4600:7100], perm[7100:9100]]
+    n = 4500
+    assert (512 << 20) // (n * C) == 3
+    pool = device_pool(shape, 71)
+    pool_h = host(pool)
+    size = shape.image_bytes(n)
+    buf = guarded_buffer(size, G)
+    inner = buf[G:G + size]
+    want = np.full(size + 2 * G, wl.GUARD_BYTE, dtype=np.uint8)
+    kv = aqua.KVPool(shape.as_tuple(), pool)
+    try:
+        for l0, nl, launches in [(0, 0, 4), (1, 7, 3), (4, 2, 1), (9, 1, 1)]:
+            layers = None if nl == 0 else (l0, nl)
+            say("split launches, layers", layers)
+            before = kv.stats()["launches"]
+            kv.swap_out(out_t, inner, layers=layers)
+            mid = kv.stats()["launches"]
+            kv.swap_in(in_t, inner, layers=layers)
+            kv.sync()
+            after = kv.stats()["launches"]
+            assert (mid - before, after - mid) == (launches, launches)
+            assert oracle.swap_out_ex(d, pool_h, out_t, want[G:G + size], None, None,
+                                      l0, nl) == 0
+            assert oracle.swap_in_ex(d, pool_h, in_t, want[G:G + size], None, None,
+                                     l0, nl) == 0
+            assert_bytes_equal(host(buf), want, f"image after layers {layers}")
+            assert_bytes_equal(host(pool), pool_h, f"pool after layers {layers}")
+    finally:
+        kv.close()
+        del pool, buf
+        torch.cuda.empty_cache()
+
+
 def test_pinned_host_zero_copy_round_trip():
     """The offload image in pinned host memory, written and read zero-copy."""
     case = wl.tiny_case(seed=11)
