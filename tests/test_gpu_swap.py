@@ -107,6 +107,11 @@ RAGGED = [
     wl.KVShape(2, 96, 8, 16, 128, wl.FP8_E4M3),
     wl.KVShape(3, 64, 8, 16, 128, wl.F16),
     wl.KVShape(2, 48, 32, 32, 256, wl.F16),
+    # 24 and 40 KiB chunks end inside a workgroup's second and third rows of 1024
+    # vectors; 96 KiB chunks split into a 64 KiB unit and a 32 KiB remainder.
+    wl.KVShape(3, 80, 3, 16, 128, wl.F16),
+    wl.KVShape(2, 64, 5, 16, 128, wl.BF16),
+    wl.KVShape(2, 48, 12, 16, 128, wl.BF16),
 ]
 
 
