@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "e616aeea13c11358"): {
-        "gather (swap-out)": 21477201711, "scatter (swap-in)": 21476722584},
-    ("llama8b_hbm", "e616aeea13c11358"): {
-        "gather (swap-out)": 4295897897, "scatter (swap-in)": 4295790483},
-    ("llama70b_tp2_hbm", "e616aeea13c11358"): {
-        "gather (swap-out)": 1074663130, "scatter (swap-in)": 1074436828},
-    ("llama70b_tp4_hbm", "e616aeea13c11358"): {
-        "gather (swap-out)": 5369607463, "scatter (swap-in)": 5369283986},
-    ("llama8b_fp8_hbm", "e616aeea13c11358"): {
-        "gather (swap-out)": 1074138104, "scatter (swap-in)": 1074329379},
+    ("llama70b_hbm", "43a1f5fadae31295"): {
+        "gather (swap-out)": 21477320496, "scatter (swap-in)": 21476752382},
+    ("llama8b_hbm", "43a1f5fadae31295"): {
+        "gather (swap-out)": 4295918173, "scatter (swap-in)": 4295791507},
+    ("llama70b_tp2_hbm", "43a1f5fadae31295"): {
+        "gather (swap-out)": 1074826169, "scatter (swap-in)": 1074440945},
+    ("llama70b_tp4_hbm", "43a1f5fadae31295"): {
+        "gather (swap-out)": 5369617908, "scatter (swap-in)": 5369321772},
+    ("llama8b_fp8_hbm", "43a1f5fadae31295"): {
+        "gather (swap-out)": 1074386314, "scatter (swap-in)": 1074797027},
 }
 
 # Every source that decides what the swap kernels do and how they are
@@ -117,6 +117,10 @@ WORKLOADS = {
            "out and those rejoining it in",
     "cycle_host": "the preemption cycle with pinned host memory as swap space: each slice "
                   "swaps 16 prompts out to host memory on one stream and 16 in on another",
+    "sizes": "swap rate against payload size on the Llama-3-8B-shaped bf16 pool (64 KiB "
+             "chunks, 2 MiB per block over 32 layers): one fragmented prompt of 2 to 2048 blocks "
+             "(4 MiB to 4 GiB) out to an HBM region and back, and to pinned host memory and "
+             "back, beside one runtime copy of the same bytes and one runtime copy per chunk",
     "cycle": "time-sliced preemption on a Llama-3-8B-shaped fp8 e4m3 pool (16384 blocks): "
              "64 prompts of 128..8192 tokens, each slice swaps the 16 longest-resident out "
              "on one stream and the 16 longest-waiting in on another",
@@ -1054,6 +1058,192 @@ def run_next(args, res_common):
     return res, s
 
 
+SWEEP_BLOCKS = (2, 8, 32, 128, 512, 2048)   # prompt lengths of the size sweep, in blocks
+
+
+def _timed_on(stream, reps, fn):
+    """Mean HIP-event time (ms) of ``fn()`` over ``reps`` calls on ``stream``,
+    after one untimed call, and the host wall time per call (ms)."""
+    import torch
+    fn()
+    stream.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    stream.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / reps
+    return e0.elapsed_time(e1) / reps, wall
+
+
+def _round_trips(kv, stream, a, b, buf, reps):
+    """``reps`` round trips (swap-out of one table into ``buf``, swap-in into
+    the other, the two tables trading places each time, as in the pair
+    workloads) after one untimed round trip: mean HIP-event time of the
+    swap-outs and of the swap-ins (ms), and the host wall time per round trip
+    (ms, enqueue to completion)."""
+    import numpy as np
+    import torch
+    kv.swap_out(a, buf, stream=stream)
+    kv.swap_in(b, buf, stream=stream)
+    stream.synchronize()
+    evs = []
+    t0 = time.perf_counter()
+    for i in range(reps):
+        src, dst = (a, b) if i % 2 else (b, a)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        kv.swap_out(src, buf, stream=stream)
+        e[1].record(stream)
+        kv.swap_in(dst, buf, stream=stream)
+        e[2].record(stream)
+        evs.append(e)
+    stream.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / reps
+    out_ms = float(np.mean([x.elapsed_time(y) for x, y, _ in evs]))
+    in_ms = float(np.mean([y.elapsed_time(z) for _, y, z in evs]))
+    return out_ms, in_ms, wall
+
+
+def run_sizes(args, res_common):
+    """Swap rate against payload size, the measurement behind the paper's case
+    for a gather (a copy's rate grows with its size, so one prompt's many small
+    chunks move slowly one by one).  For each prompt length: the library's
+    gather and scatter to an HBM region and, staged, to pinned host memory;
+    one contiguous runtime copy of the same bytes (device to device, and
+    device to pinned host); and the runtime's copies of the same chunks one
+    chunk at a time (hipMemcpyAsync per (layer, block), as a serving engine
+    without a gather kernel would issue them)."""
+    import numpy as np
+    import torch
+
+    from paper_2407_21255_amd import aqua
+    from paper_2407_21255_amd import workload as wl
+
+    s = wl.LLAMA8B
+    C, L, N = s.chunk_bytes, s.num_layers, s.num_blocks
+    pool = torch.empty(s.pool_bytes, dtype=torch.uint8, device="cuda")
+    wl.fill_pool(pool, s, 41)
+    perm = wl.permutation(N, 41)
+    biggest = s.image_bytes(max(SWEEP_BLOCKS))
+    dimg = torch.zeros(biggest, dtype=torch.uint8, device="cuda")
+    himg = torch.zeros(biggest, dtype=torch.uint8, pin_memory=True)
+    torch.cuda.synchronize()
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
+    memcpy = hip.hipMemcpyAsync
+    stream = torch.cuda.Stream()
+    sh = stream.cuda_stream
+    kv = aqua.KVPool(s.as_tuple(), pool)
+    _configure_host(kv, "staged")   # host-target calls only; HBM calls are unaffected
+    rows = []
+    with _no_gc():
+        # The swaps to the HBM region first, every size, before any host-target
+        # call; then the staged host swaps and the runtime's copies.
+        hbm = {}
+        for n in SWEEP_BLOCKS:
+            payload = s.image_bytes(n)
+            a, b = aqua._csr([perm[:n]]), aqua._csr([perm[n:2 * n]])
+            reps = max(8, min(50, (1 << 30) // payload))
+            hbm[n] = _round_trips(kv, stream, a, b, dimg[:payload], reps)
+        for n in SWEEP_BLOCKS:
+            payload = s.image_bytes(n)
+            a, b = aqua._csr([perm[:n]]), aqua._csr([perm[n:2 * n]])
+            d, h = dimg[:payload], himg[:payload]
+            out_ms, in_ms, rt_wall = hbm[n]
+            reps = max(8, min(50, (1 << 30) // payload))
+            hreps = max(2, min(20, (256 << 20) // payload))
+            hout_ms, hin_ms, _ = _round_trips(kv, stream, a, b, h, hreps)
+            src = pool[:payload]
+
+            def bulk_d2d():
+                with torch.cuda.stream(stream):
+                    d.copy_(src)
+
+            def bulk_d2h():
+                with torch.cuda.stream(stream):
+                    h.copy_(src, non_blocking=True)
+
+            d2d_ms, _ = _timed_on(stream, reps, bulk_d2d)
+            d2h_ms, _ = _timed_on(stream, hreps, bulk_d2h)
+            # One runtime copy per (layer, block) chunk of the same prompt.
+            blk = np.asarray(perm[:n], dtype=np.int64)
+            lay = np.arange(L, dtype=np.int64)[:, None]
+            srcs = (pool.data_ptr() + (lay * N + blk[None, :]) * C).ravel().tolist()
+            offs = (np.arange(L * n, dtype=np.int64) * C).tolist()
+            dd = [d.data_ptr() + o for o in offs]
+            hh = [h.data_ptr() + o for o in offs]
+
+            def chunks(dsts, kind):
+                def go():
+                    for x, y in zip(dsts, srcs):
+                        if memcpy(x, y, C, kind, sh):
+                            raise RuntimeError("hipMemcpyAsync failed")
+                return go
+
+            preps = max(1, min(10, 4096 // (L * n)))
+            pc_d2d_ms, pc_d2d_wall = _timed_on(stream, preps, chunks(dd, 3))
+            pc_d2h_ms, pc_d2h_wall = _timed_on(stream, preps, chunks(hh, 2))
+            gbs = lambda ms: round(payload / (ms * 1e-3) / 1e9, 2)  # noqa: E731
+            rows.append({
+                "blocks": n, "payload_bytes": payload, "chunks": L * n,
+                "hbm": {"gather_GBps": gbs(out_ms), "scatter_GBps": gbs(in_ms),
+                        "gather_ms": round(out_ms, 4), "scatter_ms": round(in_ms, 4),
+                        "round_trip_wall_ms": round(rt_wall, 4),
+                        "runtime_copy_GBps": gbs(d2d_ms),
+                        "per_chunk_copies_GBps": gbs(pc_d2d_ms),
+                        "per_chunk_copies_wall_GBps": gbs(pc_d2d_wall)},
+                "pinned_host_staged": {"swap_out_GBps": gbs(hout_ms),
+                                       "swap_in_GBps": gbs(hin_ms),
+                                       "runtime_copy_d2h_GBps": gbs(d2h_ms),
+                                       "per_chunk_copies_d2h_GBps": gbs(pc_d2h_ms),
+                                       "per_chunk_copies_d2h_wall_GBps": gbs(pc_d2h_wall)},
+            })
+            row = rows[-1]["hbm"]
+            print(f"size sweep: {payload >> 20} MiB gather {row['gather_GBps']} GB/s, "
+                  f"per-chunk copies {row['per_chunk_copies_GBps']} GB/s",
+                  file=sys.stderr, flush=True)
+        # The largest HBM round trip again, after the host-target calls.
+        n = SWEEP_BLOCKS[-1]
+        again = _round_trips(kv, stream, aqua._csr([perm[:n]]), aqua._csr([perm[n:2 * n]]),
+                             dimg[:s.image_bytes(n)], 4)
+    kv.close()
+    top = rows[-1]
+    t_out, t_in = top["hbm"]["gather_ms"], top["hbm"]["scatter_ms"]
+    payload = top["payload_bytes"]
+    dom_ms = max(t_out, t_in)
+    achieved = 2 * payload / (dom_ms * 1e-3) / 1e9
+    res = dict(res_common)
+    res.update({
+        "value": round(2 * payload / ((t_out + t_in) * 1e-3) / 1e9, 2),
+        "ms_per_step": round(t_out + t_in, 4),
+        "dtype": wl.DTYPE_NAME[s.dtype],
+        "config": {
+            "workload": WORKLOADS["sizes"],
+            "layers": L, "kv_heads": s.num_kv_heads, "head_dim": s.head_dim,
+            "block_tokens": s.block_tokens, "pool_blocks": N, "chunk_bytes": C,
+            "swapped_blocks": list(SWEEP_BLOCKS),
+            "offload_target": "hbm and pinned_host", "parallelism": "single_gpu",
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "gather (swap-out)" if t_out >= t_in else
+            "scatter (swap-in)", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": 2 * payload,
+        },
+        "sweep": rows,
+        "largest_hbm_after_host_calls": {
+            "gather_GBps": round(payload / (again[0] * 1e-3) / 1e9, 2),
+            "scatter_GBps": round(payload / (again[1] * 1e-3) / 1e9, 2)},
+        "kernel_source": _kernel_hash(),
+    })
+    return res, s
+
+
 def secondary_legs(args, common) -> dict:
     """Two shorter legs reported beside the default line, outside its timed
     region: the same 32768-token prompt swapped out to pinned host memory
@@ -1149,6 +1339,8 @@ def main():
         res, shape = run_cfs(args, common)
     elif args.workload == "elastic":
         res, shape = run_elastic(args, common)
+    elif args.workload == "sizes":
+        res, shape = run_sizes(args, common)
     elif args.workload in ("prefix", "prefix_host", "prefix_mixed", "layered", "layered_host",
                            "migrate"):
         res, shape = run_next(args, common)

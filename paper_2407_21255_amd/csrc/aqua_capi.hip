@@ -599,6 +599,7 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     L.threads = aqua::swap_threads(p->shape.C, AQUA_MIN_THREADS);
     L.layer_bytes = p->call_blocks * p->shape.C;
     L.max_launch_bytes = target == AQUA_TARGET_DEVICE ? aqua::max_launch_bytes(p->shape.C) : 0;
+    L.xcd_order = false;
     return L;
 }
 
@@ -886,8 +887,11 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
     }
-    if (AQUA_SORT_RUNS && aqua::sort_runs(is_in, p->shape.C, total, p->shape.N))
+    const bool sorted = AQUA_SORT_RUNS && aqua::sort_runs(is_in, p->shape.C, total, p->shape.N);
+    if (sorted) {
         aqua::sort_by_block(&p->plan, p->shape.N, &p->sort_counts, &p->sort_tmp);
+        aqua::interleave_runs(&p->plan, aqua::kXcdWays, &p->sort_tmp);
+    }
     aqua::image_ranges(p->shape, a, &p->ranges);
     for (auto& r : p->ranges) {  // tracked by the caller's address of the buffer
         r.first += a.buf;
@@ -991,9 +995,10 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
                 return fail_enqueued(stream, st);
             }
         } else {
-            const aqua::SwapLaunch L =
+            aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
                             (uint32_t)p->plan.size(), target, l_begin, l_count);
+            L.xcd_order = target == AQUA_TARGET_DEVICE && aqua::xcd_unit_order(p->shape.C, sorted);
             (void)hipGetLastError();
             e = aqua::launch_swap(L, stream, &p->stats.launches);
             if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));

@@ -190,6 +190,22 @@ void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
     runs->swap(*tmp);
 }
 
+void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunDesc>* tmp) {
+    const size_t n = runs->size();
+    if (ways < 2 || n < 2 * (size_t)ways) return;
+    const size_t seg = (n + ways - 1) / ways;  // runs per eighth (the last may be short)
+    tmp->clear();
+    tmp->reserve(n);
+    for (size_t i = 0; i < seg; ++i)
+        for (size_t s = 0; s < ways; ++s)
+            if (s * seg + i < n) tmp->push_back((*runs)[s * seg + i]);
+    runs->swap(*tmp);
+}
+
+bool xcd_unit_order(uint64_t chunk_bytes, bool sorted) {
+    return !sorted && chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk;
+}
+
 uint64_t max_launch_bytes(uint64_t chunk_bytes) {
     return (chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk) ? kSplitLaunchBytes
                                                                            : 0;

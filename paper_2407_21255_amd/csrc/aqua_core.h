@@ -135,6 +135,41 @@ bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_b
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
                    std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp);
 
+// XCD-aware order of sorted runs.  A launch's workgroups go to MI355X's 8
+// XCDs (each with its own L2) in turn, and the kernels take one unit per
+// workgroup, layer by layer.  Dealing a layer's sorted runs out 8 ways (run
+// j of the result is run j / 8 of the (j % 8)-th contiguous eighth of the
+// input) gives each XCD one contiguous eighth of the pool range in every
+// layer, instead of every XCD taking every eighth block of one shared range.
+// Measured on MI355X against sorted order, same box, 3 to 6 runs each: 70B
+// pair +1.4 to +3.3 % (three boxes), one TP4 rank +2.7 to +3.3 %, the Yi-34B
+// prefix load +2.1 to +3.6 %, one TP2 rank +1.0 %; the fair-scheduling
+// reschedules -0.4 to -1.7 % (within their run-to-run spread).  Applied to
+// unsorted calls instead, it sped a long prompt's gather by 8-11 % but
+// slowed one of 64 short prompts by 4-7 %, so table order stays there.
+// Runs only ever change order, so no byte changes.  `tmp` is reusable
+// scratch.
+constexpr uint32_t kXcdWays = 8;
+void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunDesc>* tmp);
+
+// XCD-aware unit order inside the kernels, for the calls that keep table
+// order.  On a launch of one workgroup per unit, workgroup b (sent to XCD
+// b % 8) takes unit xcd_unit(b, units), so that each XCD copies one
+// contiguous eighth of the launch's units in order (XCD x gets the x-th
+// eighth; the first units % 8 eighths hold one unit more).  A bijection on
+// [0, units).  Used for unsorted calls of chunks between 16 and 64 KiB
+// (exclusive) to an HBM buffer, where it measured, against plain order on
+// the same box (3 to 4 runs each): the fp8 preemption cycle +4.2 %, one TP2
+// rank +0.5 %, the fp8 8B pair +0.5 %; on the fp8 8B pool, one prompt of
+// 1024 or 2048 blocks +3 to +8 %, 64 short prompts +1 to +16 %, the gather of
+// 8 prompts -0.4 to -1.9 %.  With 64 KiB chunks it slowed 64 short prompts by
+// 6 %, with 16 KiB chunks a TP4 rank by 1.2 %, so those keep plain order.
+constexpr uint32_t xcd_unit(uint32_t block, uint32_t units) {
+    const uint32_t x = block % kXcdWays, q = units / kXcdWays, r = units % kXcdWays;
+    return x * q + (x < r ? x : r) + block / kXcdWays;
+}
+bool xcd_unit_order(uint64_t chunk_bytes, bool sorted);
+
 // Launch size, measured on MI355X.  An HBM-target call of chunks between 16
 // and 64 KiB is carried by launches of at most 512 MiB of payload each (whole
 // layers, one after another on the stream); other calls by one launch.  At

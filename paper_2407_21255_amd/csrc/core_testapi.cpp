@@ -263,6 +263,22 @@ void aqua_core_sort_by_block(void* descs, uint64_t n, uint32_t num_blocks) {
     if (n) std::memcpy(descs, v.data(), n * sizeof(aqua::RunDesc));
 }
 
+// Reorders n descriptors (32 bytes each) in place with interleave_runs.
+void aqua_core_interleave_runs(void* descs, uint64_t n, uint32_t ways) {
+    std::vector<aqua::RunDesc> v(n), tmp;
+    if (n) std::memcpy(v.data(), descs, n * sizeof(aqua::RunDesc));
+    aqua::interleave_runs(&v, ways, &tmp);
+    if (n) std::memcpy(descs, v.data(), n * sizeof(aqua::RunDesc));
+}
+
+uint32_t aqua_core_xcd_ways() { return aqua::kXcdWays; }
+
+uint32_t aqua_core_xcd_unit(uint32_t block, uint32_t units) { return aqua::xcd_unit(block, units); }
+
+int aqua_core_xcd_unit_order(uint64_t chunk_bytes, int sorted) {
+    return aqua::xcd_unit_order(chunk_bytes, sorted != 0) ? 1 : 0;
+}
+
 int aqua_core_sort_runs(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
     return aqua::sort_runs(is_in != 0, chunk_bytes, blocks, num_blocks) ? 1 : 0;
 }

@@ -25,6 +25,7 @@ struct SwapLaunch {
     uint32_t threads;         // lanes per workgroup: 64, 128, 256, 512 or 1024
     uint64_t layer_bytes;     // payload of one layer of the call (its runs' chunks)
     uint64_t max_launch_bytes;  // 0: one launch, else whole layers up to this payload
+    bool xcd_order;           // one-pass launches: each XCD takes a contiguous eighth of units
 };
 
 // Scatter store hint, measured on MI355X.  Nontemporal pool stores pay for

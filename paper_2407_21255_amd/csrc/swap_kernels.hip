@@ -108,8 +108,12 @@ template <bool OUT, bool NT_POOL_ST, int THREADS>
 __global__ __launch_bounds__(THREADS) void swap_runs_kernel(
     uint8_t* __restrict__ pool, uint8_t* __restrict__ img,
     const RunDesc* __restrict__ descs, uint32_t ndesc, uint32_t l0, uint32_t img_l0,
-    uint32_t units, uint64_t chunk_bytes, uint64_t pool_lstride) {
-    for (uint32_t u = blockIdx.x; u < units; u += gridDim.x) {
+    uint32_t units, uint64_t chunk_bytes, uint64_t pool_lstride, uint32_t xcd_order) {
+    // With one workgroup per unit, xcd_order gives each XCD (workgroups go
+    // to the 8 XCDs in turn) a contiguous eighth of the units.
+    const uint32_t u0 =
+        (xcd_order && gridDim.x == units) ? xcd_unit(blockIdx.x, units) : blockIdx.x;
+    for (uint32_t u = u0; u < units; u += gridDim.x) {
         const uint32_t l = l0 + u / ndesc;
         const uint32_t k = u - (u / ndesc) * ndesc;
         const RunDesc dsc = descs[k];
@@ -185,15 +189,15 @@ void launch_swap_t(const SwapLaunch& a, uint32_t grid, uint32_t l0, uint32_t uni
     if (a.out)
         hipLaunchKernelGGL((swap_runs_kernel<true, false, THREADS>), dim3(grid), dim3(THREADS),
                            0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
-                           a.chunk_bytes, a.pool_lstride);
+                           a.chunk_bytes, a.pool_lstride, (uint32_t)a.xcd_order);
     else if (a.nt_pool_store)
         hipLaunchKernelGGL((swap_runs_kernel<false, true, THREADS>), dim3(grid), dim3(THREADS),
                            0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
-                           a.chunk_bytes, a.pool_lstride);
+                           a.chunk_bytes, a.pool_lstride, (uint32_t)a.xcd_order);
     else
         hipLaunchKernelGGL((swap_runs_kernel<false, false, THREADS>), dim3(grid), dim3(THREADS),
                            0, stream, a.pool, a.img, a.descs, a.ndesc, l0, a.img_l0, units,
-                           a.chunk_bytes, a.pool_lstride);
+                           a.chunk_bytes, a.pool_lstride, (uint32_t)a.xcd_order);
 }
 
 }  // namespace

@@ -73,6 +73,12 @@ def lib():
         L.aqua_core_swap_threads.argtypes = [u64, u32]
         L.aqua_core_swap_threads.restype = u32
         L.aqua_core_sort_by_block.argtypes = [P, u64, u32]
+        L.aqua_core_interleave_runs.argtypes = [P, u64, u32]
+        L.aqua_core_xcd_ways.restype = u32
+        L.aqua_core_xcd_unit.argtypes = [u32, u32]
+        L.aqua_core_xcd_unit.restype = u32
+        L.aqua_core_xcd_unit_order.argtypes = [u64, i32]
+        L.aqua_core_xcd_unit_order.restype = i32
         L.aqua_core_sort_runs.argtypes = [i32, u64, u64, u32]
         L.aqua_core_sort_runs.restype = i32
         L.aqua_core_max_launch_bytes.argtypes = [u64]
@@ -274,6 +280,25 @@ def sort_by_block(descs: np.ndarray, num_blocks: int) -> np.ndarray:
     out = np.ascontiguousarray(descs.copy())
     lib().aqua_core_sort_by_block(out.ctypes.data if len(out) else None, len(out), num_blocks)
     return out
+
+
+def interleave_runs(descs: np.ndarray, ways: int) -> np.ndarray:
+    """The core's XCD-aware reordering of RUN_DESC records (a copy)."""
+    out = np.ascontiguousarray(descs.copy())
+    lib().aqua_core_interleave_runs(out.ctypes.data if len(out) else None, len(out), ways)
+    return out
+
+
+def xcd_ways() -> int:
+    return int(lib().aqua_core_xcd_ways())
+
+
+def xcd_unit(block: int, units: int) -> int:
+    return int(lib().aqua_core_xcd_unit(block, units))
+
+
+def xcd_unit_order(chunk_bytes: int, sorted_runs: bool) -> bool:
+    return bool(lib().aqua_core_xcd_unit_order(chunk_bytes, int(sorted_runs)))
 
 
 def max_launch_bytes(chunk_bytes: int) -> int:

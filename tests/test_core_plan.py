@@ -269,6 +269,73 @@ def test_sort_by_block_matches_a_stable_sort():
     assert len(sort_by_block(np.zeros(0, dtype=RUN_DESC), 7)) == 0
 
 
+def test_interleave_runs_deals_eighths_to_the_xcds():
+    """Sorted runs are dealt out 8 ways: position j holds run j // 8 of the
+    (j % 8)-th contiguous eighth, so the units a round-robin dispatch sends
+    to one XCD cover one contiguous eighth of the sorted range.  The result
+    is a permutation of the input for every length (a short last eighth
+    included), and lists shorter than two runs per way stay as they are."""
+    import numpy as np
+    from tests.core_lib import RUN_DESC, interleave_runs, xcd_ways
+    W = xcd_ways()
+    assert W == 8
+    # 2048 sorted runs (one 70B layer): XCD x (= position % 8) gets runs
+    # 256x .. 256x + 255, in order.
+    d = np.zeros(2048, dtype=RUN_DESC)
+    d["block"] = np.arange(2048)
+    got = interleave_runs(d, W)["block"]
+    for x in range(W):
+        assert list(got[x::W]) == list(range(256 * x, 256 * x + 256))
+    # A worked case with a short last eighth: 19 runs, segments of 3.
+    d = np.zeros(19, dtype=RUN_DESC)
+    d["block"] = np.arange(19)
+    assert list(interleave_runs(d, W)["block"]) == [
+        0, 3, 6, 9, 12, 15, 18, 1, 4, 7, 10, 13, 16, 2, 5, 8, 11, 14, 17]
+    rng = np.random.default_rng(9)
+    for n in list(range(0, 40)) + [int(x) for x in rng.integers(40, 5000, 30)]:
+        d = np.zeros(n, dtype=RUN_DESC)
+        d["block"] = rng.permutation(n)
+        d["img_off"] = np.arange(n) * 64
+        got = interleave_runs(d, W)
+        assert sorted(got.tobytes()[i:i + 32] for i in range(0, 32 * n, 32)) == \
+            sorted(d.tobytes()[i:i + 32] for i in range(0, 32 * n, 32)), n
+        if n < 2 * W:
+            assert got.tobytes() == d.tobytes(), n
+        else:
+            seg = -(-n // W)
+            order = [s * seg + i for i in range(seg) for s in range(W) if s * seg + i < n]
+            assert got.tobytes() == d[order].tobytes(), n
+    d = np.zeros(100, dtype=RUN_DESC)
+    d["block"] = np.arange(100)
+    assert interleave_runs(d, 1).tobytes() == d.tobytes()
+
+
+def test_xcd_unit_order_gives_each_xcd_a_contiguous_eighth():
+    """On a one-pass launch, workgroup b goes to XCD b % 8 and takes unit
+    xcd_unit(b, units): a bijection on the units in which each XCD's
+    workgroups, in dispatch order, take consecutive units of one contiguous
+    eighth (the first units % 8 eighths one unit longer).  Only unsorted
+    calls of chunks between 16 and 64 KiB use it."""
+    from tests.core_lib import xcd_unit, xcd_unit_order
+    for units in list(range(1, 70)) + [163840, 16384, 4168 * 3, 2 ** 21 - 1, 1000003]:
+        got = [xcd_unit(b, units) for b in range(units)]
+        assert sorted(got) == list(range(units)), units
+        q, r = divmod(units, 8)
+        for x in range(8):
+            mine = got[x::8]
+            start = x * q + min(x, r)
+            assert mine == list(range(start, start + len(mine))), (units, x)
+            assert len(mine) == q + (1 if x < r else 0)
+    # Worked case: 19 units, eighths of 3, 3, 3, 2, 2, 2, 2, 2.
+    assert [xcd_unit(b, 19) for b in range(19)] == [
+        0, 3, 6, 9, 11, 13, 15, 17, 1, 4, 7, 10, 12, 14, 16, 18, 2, 5, 8]
+    K = 1 << 10
+    assert xcd_unit_order(32 * K, False) and xcd_unit_order(48 * K, False)
+    assert not xcd_unit_order(32 * K, True)
+    assert not xcd_unit_order(16 * K, False) and not xcd_unit_order(64 * K, False)
+    assert not xcd_unit_order(48, False) and not xcd_unit_order(1 << 20, False)
+
+
 def test_launch_size_rule():
     """Calls of chunks between 16 and 64 KiB go out in launches of at most
     512 MiB of whole layers; others in one launch (up to 2^31 units)."""
