@@ -157,17 +157,28 @@ def test_unit_size_extremes(unit, monkeypatch):
     _roundtrip(shape, 9, out_tables, in_tables, None)
 
 
-@pytest.mark.parametrize("cap,pinned", [(1, False), (7, False), (300, False), (3, True)])
-def test_capped_grids_loop_over_every_unit(cap, pinned):
+@pytest.mark.parametrize("cap,pinned,chunk_kib", [(1, False, 8), (7, False, 8), (300, False, 8),
+                                                (3, True, 8), (0, False, 32), (7, False, 32),
+                                                (1000, False, 32)])
+def test_capped_grids_loop_over_every_unit(cap, pinned, chunk_kib):
     """A grid capped below the number of (layer, run) units: each workgroup
-    loops over units a grid apart, and every byte still moves once."""
-    shape = wl.KVShape(3, 512, 2, 16, 64, wl.BF16)            # 8 KiB chunks
+    loops over units a grid apart, and every byte still moves once.  With
+    32 KiB chunks the unsorted swap-out asks for the XCD unit order: used on
+    the uncapped grid (cap 0), set aside on a capped one.
+    The swap-ins cover 45 % of the pool, so their runs are sorted and dealt
+    out to the XCDs."""
+    if chunk_kib == 8:
+        shape = wl.KVShape(3, 512, 2, 16, 64, wl.BF16)
+    else:
+        shape = wl.KVShape(3, 512, 8, 16, 128, wl.FP8_E4M3)
+    assert shape.chunk_bytes == chunk_kib << 10
     perm = wl.permutation(shape.num_blocks, 61)
     out_tables = [perm[:150], perm[150:151], perm[151:233]]
     in_tables = [perm[233:383], perm[383:384], perm[384:466]]
-    say("cap", cap, "pinned", pinned)
+    say("cap", cap, "pinned", pinned, "chunk", shape.chunk_bytes)
     _roundtrip(shape, 61, out_tables, in_tables, None, pinned=pinned,
-               host_path=aqua.AQUA_HOST_ZERO_COPY if pinned else None, max_workgroups=cap)
+               host_path=aqua.AQUA_HOST_ZERO_COPY if pinned else None,
+               max_workgroups=cap or None)
 
 
 def test_more_units_than_one_dispatch_can_count():
