@@ -45,7 +45,7 @@ constexpr uint32_t kHostZeroCopyWorkgroups = 16;
 #ifndef AQUA_DESC_DEVICE
 #define AQUA_DESC_DEVICE 0
 #endif
-// 0: runs stay in table order (see aqua::sort_runs for the shipped rule).
+// 0: runs stay in table order (see aqua::run_order for the shipped rule).
 #ifndef AQUA_SORT_RUNS
 #define AQUA_SORT_RUNS 1
 #endif
@@ -887,11 +887,13 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
     }
-    const bool sorted = AQUA_SORT_RUNS && aqua::sort_runs(is_in, p->shape.C, total, p->shape.N);
-    if (sorted) {
+    const aqua::RunOrder order = AQUA_SORT_RUNS ? aqua::run_order(is_in, p->shape.C, total,
+                                                                   p->shape.N)
+                                                : aqua::RunOrder::kTable;
+    if (order == aqua::RunOrder::kSortedDealt)
         aqua::sort_by_block(&p->plan, p->shape.N, &p->sort_counts, &p->sort_tmp);
-        aqua::interleave_runs(&p->plan, aqua::kXcdWays, &p->sort_tmp);
-    }
+    const bool dealt = order != aqua::RunOrder::kTable;
+    if (dealt) aqua::interleave_runs(&p->plan, aqua::kXcdWays, &p->sort_tmp);
     aqua::image_ranges(p->shape, a, &p->ranges);
     for (auto& r : p->ranges) {  // tracked by the caller's address of the buffer
         r.first += a.buf;
@@ -998,7 +1000,7 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
             aqua::SwapLaunch L =
                 make_launch(p, is_in, dbuf, reinterpret_cast<const RunDesc*>(descs),
                             (uint32_t)p->plan.size(), target, l_begin, l_count);
-            L.xcd_order = target == AQUA_TARGET_DEVICE && aqua::xcd_unit_order(p->shape.C, sorted);
+            L.xcd_order = target == AQUA_TARGET_DEVICE && aqua::xcd_unit_order(p->shape.C, dealt);
             (void)hipGetLastError();
             e = aqua::launch_swap(L, stream, &p->stats.launches);
             if (e != hipSuccess) return fail_enqueued(stream, latch(p, e));

@@ -175,9 +175,10 @@ uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
     return t;
 }
 
-bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
-    if (!num_blocks || blocks * 1000 < kSortMinPermille * num_blocks) return false;
-    return is_in || chunk_bytes >= kSortOutMinChunk;
+RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
+    if (!num_blocks || blocks * 1000 < kDenseMinPermille * num_blocks) return RunOrder::kTable;
+    if (is_in) return RunOrder::kSortedDealt;
+    return chunk_bytes >= kDealOutMinChunk ? RunOrder::kTableDealt : RunOrder::kTable;
 }
 
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
@@ -202,8 +203,8 @@ void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunD
     runs->swap(*tmp);
 }
 
-bool xcd_unit_order(uint64_t chunk_bytes, bool sorted) {
-    return !sorted && chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk;
+bool xcd_unit_order(uint64_t chunk_bytes, bool dealt) {
+    return !dealt && chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk;
 }
 
 uint64_t max_launch_bytes(uint64_t chunk_bytes) {

@@ -110,54 +110,62 @@ uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads);
 constexpr uint32_t kMaxGrid = 1u << 21;
 uint32_t launch_grid(uint64_t units, uint32_t max_workgroups);
 
-// Whether a call's runs go to the kernels sorted by pool block rather than
-// in table order (each run is independent, so the order changes no byte).
-// Sorted, the pool side of consecutive workgroups moves through the pool in
-// address order and the image side jumps; that pays only where the call
-// covers a large share of the pool, so that the pool accesses of the
-// resident workgroups fall close together.  Measured on MI355X:
-//   swap-in (pool written in order), calls covering half the pool: 70B
-//     scatter 3.3 % shorter, one TP2 rank's 1.6 %, one TP4 rank's 2.8 %;
-//     a sixteenth of the pool (8B, fp8 8B): no gain;
-//   swap-out (pool read in order), half the pool: 64 KiB chunks 4.5 %
-//     shorter, 32 KiB chunks 1.6 % and 16 KiB chunks 6 % longer (the image
-//     writes, scattered in smaller pieces, lose more); a sixteenth of the
-//     pool and the preemption cycle (a quarter): 2-7 % longer.
-constexpr uint64_t kSortMinPermille = 400;      // share of the pool's blocks
-constexpr uint64_t kSortOutMinChunk = 64ull << 10;
-bool sort_runs(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks);
+// The order in which a call's runs go to the kernels (each run is
+// independent, so the order changes no byte).  Calls that cover at least
+// 40 % of the pool's blocks are dealt out to the XCDs (interleave_runs):
+// swap-ins sorted by pool block first, swap-outs of chunks of 64 KiB or more
+// in table order; every other call keeps table order.  Sorted, the pool side
+// of consecutive units moves through the pool in address order and the image
+// side jumps; in table order the reverse.  Measured on MI355X, same box:
+//   swap-ins (pool written in order), calls covering half the pool: sorted
+//     against table order, 70B scatter 3.3 % shorter, one TP2 rank's 1.6 %,
+//     one TP4 rank's 2.8 %; a sixteenth of the pool (8B, fp8 8B): no gain,
+//     a quarter (the preemption cycle): 3-7 % longer;
+//   swap-outs (image written in order in table order), half the pool: sorted
+//     against table order, 64 KiB chunks 4.5 % shorter but 32 KiB chunks
+//     1.6 % and 16 KiB chunks 6 % longer; once dealt to the XCDs, the 70B
+//     gather in table order took 2.8 % less than sorted (3.53 against
+//     3.63 ms, four runs each), the pair +1.4 %.
+//   Sorting or dealing sparser calls too (every call, or from a tenth of the
+//   pool) lost 1.8-2.6 % on the fair-scheduling reschedules and the fp8 8B
+//   pair.
+enum class RunOrder { kTable, kSortedDealt, kTableDealt };
+constexpr uint64_t kDenseMinPermille = 400;     // share of the pool's blocks
+constexpr uint64_t kDealOutMinChunk = 64ull << 10;
+RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks);
 
 // Puts the runs in ascending order of their first block, keeping the table
 // order of runs that start at the same block (a swap-out may name a block
 // twice).  A counting sort over the pool's blocks: O(runs + num_blocks), and
-// sort_runs only asks for it when the runs number at least 40 % of the
+// run_order only asks for it when the runs number at least 40 % of the
 // blocks.  `counts` and `tmp` are reusable scratch.
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
                    std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp);
 
-// XCD-aware order of sorted runs.  A launch's workgroups go to MI355X's 8
-// XCDs (each with its own L2) in turn, and the kernels take one unit per
-// workgroup, layer by layer.  Dealing a layer's sorted runs out 8 ways (run
+// XCD-aware order of a dense call's runs.  A launch's workgroups go to
+// MI355X's 8 XCDs (each with its own L2) in turn, and the kernels take one
+// unit per workgroup, layer by layer.  Dealing a layer's runs out 8 ways (run
 // j of the result is run j / 8 of the (j % 8)-th contiguous eighth of the
-// input) gives each XCD one contiguous eighth of the pool range in every
-// layer, instead of every XCD taking every eighth block of one shared range.
-// Measured on MI355X against sorted order, same box, 3 to 6 runs each: 70B
-// pair +1.4 to +3.3 % (three boxes), one TP4 rank +2.7 to +3.3 %, the Yi-34B
-// prefix load +2.1 to +3.6 %, one TP2 rank +1.0 %; the fair-scheduling
-// reschedules -0.4 to -1.7 % (within their run-to-run spread).  Applied to
-// unsorted calls instead, it sped a long prompt's gather by 8-11 % but
-// slowed one of 64 short prompts by 4-7 %, so table order stays there.
-// Runs only ever change order, so no byte changes.  `tmp` is reusable
-// scratch.
+// input) gives each XCD one contiguous eighth of the runs in every layer:
+// of the pool range when they are sorted, of the image when they are in
+// table order, instead of every XCD taking every eighth run of one shared
+// range.  Measured on MI355X against sorted order, same box, 3 to 6 runs
+// each: 70B pair +1.4 to +3.3 % (four comparisons), one TP4 rank +2.7 to
+// +3.3 %, the Yi-34B prefix load +2.1 to +3.6 %, one TP2 rank +1.0 %; the
+// fair-scheduling reschedules -0.4 to -1.7 % (within their run-to-run
+// spread).  2 ways gained about half as much, 16 or 32 ways lost 1-4 %
+// against 8.  On sparse calls it sped a long prompt's gather by 8-11 % but
+// slowed one of 64 short prompts by 4-7 %, so they keep table order.  Runs
+// only ever change order, so no byte changes.  `tmp` is reusable scratch.
 constexpr uint32_t kXcdWays = 8;
 void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunDesc>* tmp);
 
-// XCD-aware unit order inside the kernels, for the calls that keep table
-// order.  On a launch of one workgroup per unit, workgroup b (sent to XCD
+// XCD-aware unit order inside the kernels, for calls whose runs are not
+// dealt out.  On a launch of one workgroup per unit, workgroup b (sent to XCD
 // b % 8) takes unit xcd_unit(b, units), so that each XCD copies one
 // contiguous eighth of the launch's units in order (XCD x gets the x-th
 // eighth; the first units % 8 eighths hold one unit more).  A bijection on
-// [0, units).  Used for unsorted calls of chunks between 16 and 64 KiB
+// [0, units).  Used for undealt calls of chunks between 16 and 64 KiB
 // (exclusive) to an HBM buffer, where it measured, against plain order on
 // the same box (3 to 4 runs each): the fp8 preemption cycle +4.2 %, one TP2
 // rank +0.5 %, the fp8 8B pair +0.5 %; on the fp8 8B pool, one prompt of
@@ -168,7 +176,7 @@ constexpr uint32_t xcd_unit(uint32_t block, uint32_t units) {
     const uint32_t x = block % kXcdWays, q = units / kXcdWays, r = units % kXcdWays;
     return x * q + (x < r ? x : r) + block / kXcdWays;
 }
-bool xcd_unit_order(uint64_t chunk_bytes, bool sorted);
+bool xcd_unit_order(uint64_t chunk_bytes, bool dealt);
 
 // Launch size, measured on MI355X.  An HBM-target call of chunks between 16
 // and 64 KiB is carried by launches of at most 512 MiB of payload each (whole

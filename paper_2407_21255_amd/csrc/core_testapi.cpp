@@ -275,12 +275,13 @@ uint32_t aqua_core_xcd_ways() { return aqua::kXcdWays; }
 
 uint32_t aqua_core_xcd_unit(uint32_t block, uint32_t units) { return aqua::xcd_unit(block, units); }
 
-int aqua_core_xcd_unit_order(uint64_t chunk_bytes, int sorted) {
-    return aqua::xcd_unit_order(chunk_bytes, sorted != 0) ? 1 : 0;
+int aqua_core_xcd_unit_order(uint64_t chunk_bytes, int dealt) {
+    return aqua::xcd_unit_order(chunk_bytes, dealt != 0) ? 1 : 0;
 }
 
-int aqua_core_sort_runs(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
-    return aqua::sort_runs(is_in != 0, chunk_bytes, blocks, num_blocks) ? 1 : 0;
+// 0: table order, 1: sorted and dealt out, 2: table order dealt out.
+int aqua_core_run_order(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
+    return (int)aqua::run_order(is_in != 0, chunk_bytes, blocks, num_blocks);
 }
 
 uint64_t aqua_core_max_launch_bytes(uint64_t chunk_bytes) {

@@ -79,8 +79,8 @@ def lib():
         L.aqua_core_xcd_unit.restype = u32
         L.aqua_core_xcd_unit_order.argtypes = [u64, i32]
         L.aqua_core_xcd_unit_order.restype = i32
-        L.aqua_core_sort_runs.argtypes = [i32, u64, u64, u32]
-        L.aqua_core_sort_runs.restype = i32
+        L.aqua_core_run_order.argtypes = [i32, u64, u64, u32]
+        L.aqua_core_run_order.restype = i32
         L.aqua_core_max_launch_bytes.argtypes = [u64]
         L.aqua_core_max_launch_bytes.restype = u64
         L.aqua_core_layers_per_launch.argtypes = [u32, u64, u64]
@@ -271,8 +271,11 @@ def tracker_soak(n_calls: int, num_blocks: int, streams: int, rotate: int, depth
     return int(kept.value), int(lanes.value)
 
 
-def sort_runs(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int) -> bool:
-    return bool(lib().aqua_core_sort_runs(int(is_in), chunk_bytes, blocks, num_blocks))
+TABLE, SORTED_DEALT, TABLE_DEALT = 0, 1, 2   # aqua::RunOrder
+
+
+def run_order(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int) -> int:
+    return int(lib().aqua_core_run_order(int(is_in), chunk_bytes, blocks, num_blocks))
 
 
 def sort_by_block(descs: np.ndarray, num_blocks: int) -> np.ndarray:
@@ -297,8 +300,8 @@ def xcd_unit(block: int, units: int) -> int:
     return int(lib().aqua_core_xcd_unit(block, units))
 
 
-def xcd_unit_order(chunk_bytes: int, sorted_runs: bool) -> bool:
-    return bool(lib().aqua_core_xcd_unit_order(chunk_bytes, int(sorted_runs)))
+def xcd_unit_order(chunk_bytes: int, dealt: bool) -> bool:
+    return bool(lib().aqua_core_xcd_unit_order(chunk_bytes, int(dealt)))
 
 
 def max_launch_bytes(chunk_bytes: int) -> int:

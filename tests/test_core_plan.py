@@ -235,18 +235,23 @@ def test_workgroup_is_sized_to_the_chunk():
 
 
 def test_run_order_rule():
-    """Runs are sorted by pool block for calls that cover at least 40 % of
-    the pool: every swap-in, and swap-outs of chunks of 64 KiB or more."""
-    from tests.core_lib import sort_runs
+    """Calls that cover at least 40 % of the pool are dealt out to the XCDs:
+    swap-ins sorted by pool block first, swap-outs of chunks of 64 KiB or
+    more in table order.  Everything else keeps table order."""
+    from tests.core_lib import SORTED_DEALT, TABLE, TABLE_DEALT, run_order
     K = 1 << 10
-    assert sort_runs(True, 64 * K, 2048, 4096)          # 70B scatter: half the pool
-    assert sort_runs(True, 16 * K, 2048, 4096)          # TP4 scatter
-    assert sort_runs(False, 64 * K, 2048, 4096)         # 70B gather
-    assert not sort_runs(False, 32 * K, 2048, 4096)     # TP2 gather
-    assert not sort_runs(True, 64 * K, 1024, 16384)     # 8B: a sixteenth of the pool
-    assert not sort_runs(True, 32 * K, 4168, 16384)     # preemption cycle: a quarter
-    assert sort_runs(True, 64 * K, 1639, 4096) and not sort_runs(True, 64 * K, 1638, 4096)
-    assert not sort_runs(True, 64 * K, 0, 0)
+    assert run_order(True, 64 * K, 2048, 4096) == SORTED_DEALT    # 70B scatter: half the pool
+    assert run_order(True, 16 * K, 2048, 4096) == SORTED_DEALT    # TP4 scatter
+    assert run_order(False, 64 * K, 2048, 4096) == TABLE_DEALT    # 70B gather
+    assert run_order(False, 1 << 20, 2048, 4096) == TABLE_DEALT
+    assert run_order(False, 32 * K, 2048, 4096) == TABLE          # TP2 gather
+    assert run_order(True, 64 * K, 1024, 16384) == TABLE          # 8B: a sixteenth of the pool
+    assert run_order(True, 32 * K, 4168, 16384) == TABLE          # preemption cycle: a quarter
+    assert run_order(True, 64 * K, 1639, 4096) == SORTED_DEALT
+    assert run_order(True, 64 * K, 1638, 4096) == TABLE
+    assert run_order(False, 64 * K, 1639, 4096) == TABLE_DEALT
+    assert run_order(False, 64 * K, 1638, 4096) == TABLE
+    assert run_order(True, 64 * K, 0, 0) == TABLE
 
 
 def test_sort_by_block_matches_a_stable_sort():
@@ -314,8 +319,8 @@ def test_xcd_unit_order_gives_each_xcd_a_contiguous_eighth():
     """On a one-pass launch, workgroup b goes to XCD b % 8 and takes unit
     xcd_unit(b, units): a bijection on the units in which each XCD's
     workgroups, in dispatch order, take consecutive units of one contiguous
-    eighth (the first units % 8 eighths one unit longer).  Only unsorted
-    calls of chunks between 16 and 64 KiB use it."""
+    eighth (the first units % 8 eighths one unit longer).  Only calls of
+    chunks between 16 and 64 KiB whose runs are not dealt out use it."""
     from tests.core_lib import xcd_unit, xcd_unit_order
     for units in list(range(1, 70)) + [163840, 16384, 4168 * 3, 2 ** 21 - 1, 1000003]:
         got = [xcd_unit(b, units) for b in range(units)]
@@ -331,7 +336,7 @@ def test_xcd_unit_order_gives_each_xcd_a_contiguous_eighth():
         0, 3, 6, 9, 11, 13, 15, 17, 1, 4, 7, 10, 12, 14, 16, 18, 2, 5, 8]
     K = 1 << 10
     assert xcd_unit_order(32 * K, False) and xcd_unit_order(48 * K, False)
-    assert not xcd_unit_order(32 * K, True)
+    assert not xcd_unit_order(32 * K, True)   # runs dealt out on the host instead
     assert not xcd_unit_order(16 * K, False) and not xcd_unit_order(64 * K, False)
     assert not xcd_unit_order(48, False) and not xcd_unit_order(1 << 20, False)
 
