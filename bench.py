@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "ddd4ba38094b02b0"): {
-        "gather (swap-out)": 21478139490, "scatter (swap-in)": 21476867684},
-    ("llama8b_hbm", "ddd4ba38094b02b0"): {
-        "gather (swap-out)": 4295908342, "scatter (swap-in)": 4295812703},
-    ("llama70b_tp2_hbm", "ddd4ba38094b02b0"): {
-        "gather (swap-out)": 1074827684, "scatter (swap-in)": 1074436214},
-    ("llama70b_tp4_hbm", "ddd4ba38094b02b0"): {
-        "gather (swap-out)": 5369602855, "scatter (swap-in)": 5369299448},
-    ("llama8b_fp8_hbm", "ddd4ba38094b02b0"): {
-        "gather (swap-out)": 1074409763, "scatter (swap-in)": 1074794466},
+    ("llama70b_hbm", "8ba82e36225d1e2d"): {
+        "gather (swap-out)": 21478118805, "scatter (swap-in)": 21476930148},
+    ("llama8b_hbm", "8ba82e36225d1e2d"): {
+        "gather (swap-out)": 4295901686, "scatter (swap-in)": 4295771641},
+    ("llama70b_tp2_hbm", "8ba82e36225d1e2d"): {
+        "gather (swap-out)": 10739648400, "scatter (swap-in)": 10739236244},
+    ("llama70b_tp4_hbm", "8ba82e36225d1e2d"): {
+        "gather (swap-out)": 5369617908, "scatter (swap-in)": 5369324844},
+    ("llama8b_fp8_hbm", "8ba82e36225d1e2d"): {
+        "gather (swap-out)": 2148318499, "scatter (swap-in)": 2149333965},
 }
 
 # Every source that decides what the swap kernels do and how they are

@@ -597,8 +597,6 @@ aqua::SwapLaunch make_launch(aqua_kv_pool* p, bool is_in, uint8_t* img, const Ru
     L.max_workgroups = p->max_wg[target];
     L.nt_pool_store = aqua::nt_pool_store(p->shape.C, (uint64_t)nl * p->call_blocks * p->shape.C);
     L.threads = aqua::swap_threads(p->shape.C, AQUA_MIN_THREADS);
-    L.layer_bytes = p->call_blocks * p->shape.C;
-    L.max_launch_bytes = target == AQUA_TARGET_DEVICE ? aqua::max_launch_bytes(p->shape.C) : 0;
     L.xcd_order = false;
     return L;
 }

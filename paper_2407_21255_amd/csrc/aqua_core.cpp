@@ -204,17 +204,11 @@ void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunD
 }
 
 bool xcd_unit_order(uint64_t chunk_bytes, bool dealt) {
-    return !dealt && chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk;
+    return !dealt && chunk_bytes > kXcdUnitMinChunk && chunk_bytes < kXcdUnitMaxChunk;
 }
 
-uint64_t max_launch_bytes(uint64_t chunk_bytes) {
-    return (chunk_bytes > kSplitMinChunk && chunk_bytes < kSplitMaxChunk) ? kSplitLaunchBytes
-                                                                           : 0;
-}
-
-uint32_t layers_per_launch(uint32_t ndesc, uint64_t layer_bytes, uint64_t max_bytes) {
-    uint64_t per = std::max<uint64_t>(1, (1ull << 31) / std::max<uint32_t>(1, ndesc));
-    if (max_bytes && layer_bytes) per = std::min(per, std::max<uint64_t>(1, max_bytes / layer_bytes));
+uint32_t layers_per_launch(uint32_t ndesc) {
+    const uint64_t per = std::max<uint64_t>(1, (1ull << 31) / std::max<uint32_t>(1, ndesc));
     return (uint32_t)std::min<uint64_t>(per, UINT32_MAX);
 }
 

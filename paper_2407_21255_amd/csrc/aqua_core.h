@@ -167,8 +167,9 @@ void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunD
 // eighth; the first units % 8 eighths hold one unit more).  A bijection on
 // [0, units).  Used for undealt calls of chunks between 16 and 64 KiB
 // (exclusive) to an HBM buffer, where it measured, against plain order on
-// the same box (3 to 4 runs each): the fp8 preemption cycle +4.2 %, one TP2
-// rank +0.5 %, the fp8 8B pair +0.5 %; on the fp8 8B pool, one prompt of
+// the same box (3 to 4 runs each, with launches of at most 512 MiB then):
+// the fp8 preemption cycle +4.2 %, one TP2 rank +0.5 %, the fp8 8B pair
+// +0.5 %; on the fp8 8B pool, one prompt of
 // 1024 or 2048 blocks +3 to +8 %, 64 short prompts +1 to +16 %, the gather of
 // 8 prompts -0.4 to -1.9 %.  With 64 KiB chunks it slowed 64 short prompts by
 // 6 %, with 16 KiB chunks a TP4 rank by 1.2 %, so those keep plain order.
@@ -176,25 +177,18 @@ constexpr uint32_t xcd_unit(uint32_t block, uint32_t units) {
     const uint32_t x = block % kXcdWays, q = units / kXcdWays, r = units % kXcdWays;
     return x * q + (x < r ? x : r) + block / kXcdWays;
 }
+constexpr uint64_t kXcdUnitMinChunk = 16ull << 10;  // exclusive
+constexpr uint64_t kXcdUnitMaxChunk = 64ull << 10;  // exclusive
 bool xcd_unit_order(uint64_t chunk_bytes, bool dealt);
 
-// Launch size, measured on MI355X.  An HBM-target call of chunks between 16
-// and 64 KiB is carried by launches of at most 512 MiB of payload each (whole
-// layers, one after another on the stream); other calls by one launch.  At
-// 32 KiB: one TP2 rank's 5 GiB swaps 5 % shorter, the fp8 preemption cycle
-// (about 4.4 GB per call) 3-4 % shorter, the fp8 8B pool's 1 GiB calls
-// unchanged; pieces of 1-2 GiB gained less, of 64-256 MiB less or lost.
-// Split the same way, 64 KiB calls (70B, 8B) and 16 KiB calls (TP4) ran
-// 1-6 % longer.  0: no limit.
-constexpr uint64_t kSplitMinChunk = 16ull << 10;  // exclusive
-constexpr uint64_t kSplitMaxChunk = 64ull << 10;  // exclusive
-constexpr uint64_t kSplitLaunchBytes = 512ull << 20;
-uint64_t max_launch_bytes(uint64_t chunk_bytes);
-
-// Layers per launch of a call with `ndesc` runs per layer and `layer_bytes`
-// of payload per layer: fewer than 2^31 units per launch, and at most
-// `max_bytes` of payload when that is non-zero (but at least one layer).
-uint32_t layers_per_launch(uint32_t ndesc, uint64_t layer_bytes, uint64_t max_bytes);
+// Layers per launch of a call with `ndesc` runs per layer: whole layers and
+// fewer than 2^31 units per launch, so that almost every call is one launch.
+// Launches of at most 512 MiB had made calls of 32 KiB chunks 3-5 % shorter
+// in plain unit order; with the XCD unit order, which gives each XCD an
+// eighth of a whole launch, one launch per call measured faster again (one
+// TP2 rank +2.4 %, the fp8 preemption cycle and 8B pair +0.4 %, four runs
+// each), and splitting 16 or 64 KiB calls lost 2-4 %.
+uint32_t layers_per_launch(uint32_t ndesc);
 
 // Reusable scratch for duplicate detection (epoch-stamped marks, O(n)).
 struct DupMarks {

@@ -284,13 +284,7 @@ int aqua_core_run_order(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32
     return (int)aqua::run_order(is_in != 0, chunk_bytes, blocks, num_blocks);
 }
 
-uint64_t aqua_core_max_launch_bytes(uint64_t chunk_bytes) {
-    return aqua::max_launch_bytes(chunk_bytes);
-}
-
-uint32_t aqua_core_layers_per_launch(uint32_t ndesc, uint64_t layer_bytes, uint64_t max_bytes) {
-    return aqua::layers_per_launch(ndesc, layer_bytes, max_bytes);
-}
+uint32_t aqua_core_layers_per_launch(uint32_t ndesc) { return aqua::layers_per_launch(ndesc); }
 
 uint32_t aqua_core_launch_grid(uint64_t units, uint32_t max_workgroups) {
     return aqua::launch_grid(units, max_workgroups);

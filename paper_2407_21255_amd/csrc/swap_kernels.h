@@ -23,8 +23,6 @@ struct SwapLaunch {
     uint32_t max_workgroups;  // 0: one workgroup per (layer, run)
     bool nt_pool_store;       // scatter: nontemporal stores into the pool
     uint32_t threads;         // lanes per workgroup: 64, 128, 256, 512 or 1024
-    uint64_t layer_bytes;     // payload of one layer of the call (its runs' chunks)
-    uint64_t max_launch_bytes;  // 0: one launch, else whole layers up to this payload
     bool xcd_order;           // one-pass launches: each XCD takes a contiguous eighth of units
 };
 

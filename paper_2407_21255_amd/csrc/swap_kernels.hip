@@ -212,9 +212,8 @@ hipError_t launch_copy(const uint8_t* src, uint8_t* dst, const CopyDesc* descs, 
 
 hipError_t launch_swap(const SwapLaunch& a, hipStream_t stream, uint64_t* launches) {
     if (!a.ndesc || !a.num_layers) return hipSuccess;
-    // Whole layers per launch: fewer than 2^31 units, and at most
-    // max_launch_bytes of payload when that is set.
-    const uint32_t per = layers_per_launch(a.ndesc, a.layer_bytes, a.max_launch_bytes);
+    // Whole layers per launch, fewer than 2^31 units each.
+    const uint32_t per = layers_per_launch(a.ndesc);
     const uint32_t end = a.first_layer + a.num_layers;
     for (uint32_t l0 = a.first_layer; l0 < end; l0 += per) {
         const uint32_t nl = std::min<uint32_t>(per, end - l0);

@@ -81,9 +81,7 @@ def lib():
         L.aqua_core_xcd_unit_order.restype = i32
         L.aqua_core_run_order.argtypes = [i32, u64, u64, u32]
         L.aqua_core_run_order.restype = i32
-        L.aqua_core_max_launch_bytes.argtypes = [u64]
-        L.aqua_core_max_launch_bytes.restype = u64
-        L.aqua_core_layers_per_launch.argtypes = [u32, u64, u64]
+        L.aqua_core_layers_per_launch.argtypes = [u32]
         L.aqua_core_layers_per_launch.restype = u32
         L.aqua_core_launch_grid.argtypes = [u64, u32]
         L.aqua_core_launch_grid.restype = u32
@@ -304,9 +302,5 @@ def xcd_unit_order(chunk_bytes: int, dealt: bool) -> bool:
     return bool(lib().aqua_core_xcd_unit_order(chunk_bytes, int(dealt)))
 
 
-def max_launch_bytes(chunk_bytes: int) -> int:
-    return int(lib().aqua_core_max_launch_bytes(chunk_bytes))
-
-
-def layers_per_launch(ndesc: int, layer_bytes: int, max_bytes: int) -> int:
-    return int(lib().aqua_core_layers_per_launch(ndesc, layer_bytes, max_bytes))
+def layers_per_launch(ndesc: int) -> int:
+    return int(lib().aqua_core_layers_per_launch(ndesc))

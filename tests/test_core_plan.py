@@ -342,20 +342,13 @@ def test_xcd_unit_order_gives_each_xcd_a_contiguous_eighth():
 
 
 def test_launch_size_rule():
-    """Calls of chunks between 16 and 64 KiB go out in launches of at most
-    512 MiB of whole layers; others in one launch (up to 2^31 units)."""
-    from tests.core_lib import layers_per_launch, max_launch_bytes
-    K, M = 1 << 10, 1 << 20
-    assert max_launch_bytes(32 * K) == 512 * M
-    assert max_launch_bytes(48 * K) == 512 * M
-    assert max_launch_bytes(16 * K) == 0 and max_launch_bytes(64 * K) == 0
-    assert max_launch_bytes(48) == 0 and max_launch_bytes(1 << 20) == 0
-    # One TP2 rank: 2048 runs of 32 KiB per layer, 64 MiB per layer -> 8 layers.
-    assert layers_per_launch(2048, 64 * M, 512 * M) == 8
-    # The preemption cycle: about 136 MB per layer -> 3 layers.
-    assert layers_per_launch(4168, 4168 * 32 * K, 512 * M) == 3
-    # A layer larger than the limit still goes out whole.
-    assert layers_per_launch(100, 600 * M, 512 * M) == 1
-    # No limit: only the 2^31-unit bound.
-    assert layers_per_launch(2048, 64 * M, 0) == (1 << 31) // 2048
-    assert layers_per_launch(1 << 31, 1, 0) == 1
+    """A call goes out in launches of whole layers of fewer than 2^31 units
+    each: one launch for every workload here, several only where one layer
+    holds a large share of 2^31 runs."""
+    from tests.core_lib import layers_per_launch
+    assert layers_per_launch(2048) == (1 << 31) // 2048          # 70B or TP2: all 80 layers
+    assert layers_per_launch(4168) == (1 << 31) // 4168          # preemption cycle call
+    assert layers_per_launch(131072) == 16384                     # 131072 runs per layer
+    assert layers_per_launch((1 << 31) - 1) == 1
+    assert layers_per_launch(1 << 31) == 1
+    assert layers_per_launch(0) == 1 << 31
