@@ -885,9 +885,9 @@ aqua_status do_swap(aqua_kv_pool* p, bool is_in, uint32_t num_seqs,
     } else {
         aqua::plan_runs(p->shape, a, p->unit_bytes, &p->plan);
     }
-    const aqua::RunOrder order = AQUA_SORT_RUNS ? aqua::run_order(is_in, p->shape.C, total,
-                                                                   p->shape.N)
-                                                : aqua::RunOrder::kTable;
+    const aqua::RunOrder order =
+        AQUA_SORT_RUNS ? aqua::run_order(is_in, p->shape.C, total, p->shape.N, num_seqs)
+                       : aqua::RunOrder::kTable;
     if (order == aqua::RunOrder::kSortedDealt)
         aqua::sort_by_block(&p->plan, p->shape.N, &p->sort_counts, &p->sort_tmp);
     const bool dealt = order != aqua::RunOrder::kTable;

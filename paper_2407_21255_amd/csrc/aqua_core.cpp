@@ -175,14 +175,26 @@ uint32_t swap_threads(uint64_t chunk_bytes, uint32_t min_threads) {
     return t;
 }
 
-RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
-    if (!num_blocks || blocks * 1000 < kDenseMinPermille * num_blocks) return RunOrder::kTable;
-    if (is_in) return RunOrder::kSortedDealt;
-    return chunk_bytes >= kDealOutMinChunk ? RunOrder::kTableDealt : RunOrder::kTable;
+RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks,
+                   uint32_t num_seqs) {
+    // Fewer blocks than two per XCD: nothing to deal out.
+    if (!num_blocks || blocks < 2 * kXcdWays) return RunOrder::kTable;
+    const bool dense = blocks * 1000 >= kDenseMinPermille * num_blocks;
+    if (chunk_bytes >= kDealMinChunk) {
+        if (is_in) return RunOrder::kSortedDealt;
+        const bool long_seqs = blocks >= kDealOutMinMeanBlocks * std::max<uint64_t>(1, num_seqs);
+        return dense || long_seqs ? RunOrder::kTableDealt : RunOrder::kTable;
+    }
+    return dense && is_in ? RunOrder::kSortedDealt : RunOrder::kTable;
 }
 
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
                    std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp) {
+    if ((uint64_t)runs->size() * kSortCountingMinRatio < num_blocks) {
+        std::stable_sort(runs->begin(), runs->end(),
+                         [](const RunDesc& a, const RunDesc& b) { return a.block < b.block; });
+        return;
+    }
     counts->assign((size_t)num_blocks + 1, 0);
     for (const RunDesc& r : *runs) ++(*counts)[r.block + 1];
     for (uint32_t b = 0; b < num_blocks; ++b) (*counts)[b + 1] += (*counts)[b];

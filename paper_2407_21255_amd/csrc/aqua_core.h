@@ -111,12 +111,16 @@ constexpr uint32_t kMaxGrid = 1u << 21;
 uint32_t launch_grid(uint64_t units, uint32_t max_workgroups);
 
 // The order in which a call's runs go to the kernels (each run is
-// independent, so the order changes no byte).  Calls that cover at least
-// 40 % of the pool's blocks are dealt out to the XCDs (interleave_runs):
-// swap-ins sorted by pool block first, swap-outs of chunks of 64 KiB or more
-// in table order; every other call keeps table order.  Sorted, the pool side
-// of consecutive units moves through the pool in address order and the image
-// side jumps; in table order the reverse.  Measured on MI355X, same box:
+// independent, so the order changes no byte).  Runs dealt out to the XCDs
+// (interleave_runs), swap-ins sorted by pool block first:
+//   chunks of 64 KiB or more: every swap-in; a swap-out when it covers at
+//     least 40 % of the pool's blocks or its sequences average at least 32
+//     blocks (the others keep table order);
+//   smaller chunks: a swap-in that covers at least 40 % of the pool; every
+//     other call keeps table order.
+// Sorted, the pool side of consecutive units moves through the pool in
+// address order and the image side jumps; in table order the reverse.
+// Measured on MI355X, same box:
 //   swap-ins (pool written in order), calls covering half the pool: sorted
 //     against table order, 70B scatter 3.3 % shorter, one TP2 rank's 1.6 %,
 //     one TP4 rank's 2.8 %; a sixteenth of the pool (8B, fp8 8B): no gain,
@@ -126,19 +130,27 @@ uint32_t launch_grid(uint64_t units, uint32_t max_workgroups);
 //     1.6 % and 16 KiB chunks 6 % longer; once dealt to the XCDs, the 70B
 //     gather in table order took 2.8 % less than sorted (3.53 against
 //     3.63 ms, four runs each), the pair +1.4 %.
-//   Sorting or dealing sparser calls too (every call, or from a tenth of the
-//   pool) lost 1.8-2.6 % on the fair-scheduling reschedules and the fp8 8B
-//   pair.
+//   sparse calls of 64 KiB chunks, dealt as above against table order
+//     (three runs each): one prompt of 1024 or 2048 blocks +3 to +7.5 %,
+//     8 prompts +1.3 to +2.7 %, the 8B pair +1.1 %, prefix loads beside
+//     other swaps +3.6 %, 64 prompts of 32 blocks +3 to +4 %; dealing the
+//     gather of 64 prompts of 16 blocks too cost it 8 %, hence the 32-block
+//     mean.  Sorting or dealing sparse calls of smaller chunks lost 2.6 %
+//     (the fp8 8B pair, whose scatter then leaves the XCD unit order).
 enum class RunOrder { kTable, kSortedDealt, kTableDealt };
 constexpr uint64_t kDenseMinPermille = 400;     // share of the pool's blocks
-constexpr uint64_t kDealOutMinChunk = 64ull << 10;
-RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks);
+constexpr uint64_t kDealMinChunk = 64ull << 10;
+constexpr uint64_t kDealOutMinMeanBlocks = 32;  // sparse swap-outs: blocks per sequence
+RunOrder run_order(bool is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks,
+                   uint32_t num_seqs);
 
 // Puts the runs in ascending order of their first block, keeping the table
 // order of runs that start at the same block (a swap-out may name a block
-// twice).  A counting sort over the pool's blocks: O(runs + num_blocks), and
-// run_order only asks for it when the runs number at least 40 % of the
-// blocks.  `counts` and `tmp` are reusable scratch.
+// twice).  A counting sort over the pool's blocks, O(runs + num_blocks), when
+// the runs number at least a sixteenth of the blocks; a stable comparison
+// sort, O(runs log runs), below that, so that a small call does not pay for
+// the whole pool.  `counts` and `tmp` are reusable scratch.
+constexpr uint64_t kSortCountingMinRatio = 16;
 void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
                    std::vector<uint32_t>* counts, std::vector<RunDesc>* tmp);
 

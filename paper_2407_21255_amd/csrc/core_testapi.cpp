@@ -280,8 +280,9 @@ int aqua_core_xcd_unit_order(uint64_t chunk_bytes, int dealt) {
 }
 
 // 0: table order, 1: sorted and dealt out, 2: table order dealt out.
-int aqua_core_run_order(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks) {
-    return (int)aqua::run_order(is_in != 0, chunk_bytes, blocks, num_blocks);
+int aqua_core_run_order(int is_in, uint64_t chunk_bytes, uint64_t blocks, uint32_t num_blocks,
+                        uint32_t num_seqs) {
+    return (int)aqua::run_order(is_in != 0, chunk_bytes, blocks, num_blocks, num_seqs);
 }
 
 uint32_t aqua_core_layers_per_launch(uint32_t ndesc) { return aqua::layers_per_launch(ndesc); }

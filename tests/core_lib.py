@@ -79,7 +79,7 @@ def lib():
         L.aqua_core_xcd_unit.restype = u32
         L.aqua_core_xcd_unit_order.argtypes = [u64, i32]
         L.aqua_core_xcd_unit_order.restype = i32
-        L.aqua_core_run_order.argtypes = [i32, u64, u64, u32]
+        L.aqua_core_run_order.argtypes = [i32, u64, u64, u32, u32]
         L.aqua_core_run_order.restype = i32
         L.aqua_core_layers_per_launch.argtypes = [u32]
         L.aqua_core_layers_per_launch.restype = u32
@@ -272,8 +272,9 @@ def tracker_soak(n_calls: int, num_blocks: int, streams: int, rotate: int, depth
 TABLE, SORTED_DEALT, TABLE_DEALT = 0, 1, 2   # aqua::RunOrder
 
 
-def run_order(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int) -> int:
-    return int(lib().aqua_core_run_order(int(is_in), chunk_bytes, blocks, num_blocks))
+def run_order(is_in: bool, chunk_bytes: int, blocks: int, num_blocks: int,
+              num_seqs: int = 1) -> int:
+    return int(lib().aqua_core_run_order(int(is_in), chunk_bytes, blocks, num_blocks, num_seqs))
 
 
 def sort_by_block(descs: np.ndarray, num_blocks: int) -> np.ndarray:

@@ -235,23 +235,38 @@ def test_workgroup_is_sized_to_the_chunk():
 
 
 def test_run_order_rule():
-    """Calls that cover at least 40 % of the pool are dealt out to the XCDs:
-    swap-ins sorted by pool block first, swap-outs of chunks of 64 KiB or
-    more in table order.  Everything else keeps table order."""
+    """Chunks of 64 KiB or more: every swap-in sorted by pool block and
+    dealt out to the XCDs; a swap-out dealt in table order when it covers at
+    least 40 % of the pool or its sequences average at least 32 blocks.
+    Smaller chunks: swap-ins that cover 40 % of the pool sorted and dealt;
+    everything else keeps table order."""
     from tests.core_lib import SORTED_DEALT, TABLE, TABLE_DEALT, run_order
     K = 1 << 10
-    assert run_order(True, 64 * K, 2048, 4096) == SORTED_DEALT    # 70B scatter: half the pool
-    assert run_order(True, 16 * K, 2048, 4096) == SORTED_DEALT    # TP4 scatter
-    assert run_order(False, 64 * K, 2048, 4096) == TABLE_DEALT    # 70B gather
-    assert run_order(False, 1 << 20, 2048, 4096) == TABLE_DEALT
-    assert run_order(False, 32 * K, 2048, 4096) == TABLE          # TP2 gather
-    assert run_order(True, 64 * K, 1024, 16384) == TABLE          # 8B: a sixteenth of the pool
-    assert run_order(True, 32 * K, 4168, 16384) == TABLE          # preemption cycle: a quarter
-    assert run_order(True, 64 * K, 1639, 4096) == SORTED_DEALT
-    assert run_order(True, 64 * K, 1638, 4096) == TABLE
-    assert run_order(False, 64 * K, 1639, 4096) == TABLE_DEALT
-    assert run_order(False, 64 * K, 1638, 4096) == TABLE
+    # 64 KiB chunks.
+    assert run_order(True, 64 * K, 2048, 4096) == SORTED_DEALT       # 70B scatter: half the pool
+    assert run_order(False, 64 * K, 2048, 4096) == TABLE_DEALT       # 70B gather
+    assert run_order(True, 64 * K, 1024, 16384, 8) == SORTED_DEALT   # 8B pair: a sixteenth
+    assert run_order(False, 64 * K, 1024, 16384, 8) == TABLE_DEALT   # 128 blocks per prompt
+    assert run_order(False, 64 * K, 1024, 16384, 64) == TABLE        # 16 blocks per prompt
+    assert run_order(False, 64 * K, 2048, 16384, 64) == TABLE_DEALT  # 32 blocks per prompt
+    assert run_order(False, 64 * K, 2047, 16384, 64) == TABLE
+    assert run_order(True, 64 * K, 1024, 16384, 64) == SORTED_DEALT
+    assert run_order(False, 1 << 20, 31, 4096, 1) == TABLE
+    assert run_order(False, 1 << 20, 32, 4096, 1) == TABLE_DEALT
+    assert run_order(False, 64 * K, 1639, 4096, 1000) == TABLE_DEALT # dense, short prompts
+    assert run_order(False, 64 * K, 1638, 4096, 1000) == TABLE
+    # Smaller chunks.
+    assert run_order(True, 16 * K, 2048, 4096) == SORTED_DEALT       # TP4 scatter
+    assert run_order(False, 32 * K, 2048, 4096) == TABLE             # TP2 gather
+    assert run_order(True, 32 * K, 4168, 16384, 16) == TABLE         # preemption cycle: a quarter
+    assert run_order(True, 32 * K, 1639, 4096) == SORTED_DEALT
+    assert run_order(True, 32 * K, 1638, 4096) == TABLE
+    # Nothing to order: no blocks, or fewer than two per XCD.
     assert run_order(True, 64 * K, 0, 0) == TABLE
+    assert run_order(False, 64 * K, 0, 4096, 0) == TABLE
+    assert run_order(True, 64 * K, 15, 4096) == TABLE
+    assert run_order(True, 64 * K, 16, 4096) == SORTED_DEALT
+    assert run_order(True, 64 * K, 15, 20) == TABLE
 
 
 def test_sort_by_block_matches_a_stable_sort():
@@ -271,6 +286,14 @@ def test_sort_by_block_matches_a_stable_sort():
         got = sort_by_block(d, N)
         want = d[np.argsort(d["block"], kind="stable")]
         assert got.tobytes() == want.tobytes(), trial
+    # Few runs on a large pool take the comparison sort, many the counting
+    # sort: both stable.
+    for n, N in ((3, 16384), (1023, 16384), (1024, 16384), (5000, 16384), (40, 40)):
+        d = np.zeros(n, dtype=RUN_DESC)
+        d["block"] = rng.integers(0, N, n)
+        d["img_off"] = np.arange(n) * 4096
+        want = d[np.argsort(d["block"], kind="stable")]
+        assert sort_by_block(d, N).tobytes() == want.tobytes(), (n, N)
     assert len(sort_by_block(np.zeros(0, dtype=RUN_DESC), 7)) == 0
 
 
