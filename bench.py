@@ -590,12 +590,15 @@ def _configure_host(kv, host_path):
     _configure_link(kv)
 
 
-def _time_slices(sched, pool, region, ids, warmup, host_path=None):
+def _time_slices(sched, pool, region, ids, warmup, host_path=None, streams=2, legs="both"):
     """Issues slices ``ids`` of a swap schedule (the first ``warmup`` of them
     untimed): out on one stream, in on another, ``aqua_sync`` at the end of
     each, as a scheduler's loop boundary does.  (Issued without it, slices
     stay correct -- the library orders reused blocks and slots -- but
-    consecutive slices then contend for HBM.)"""
+    consecutive slices then contend for HBM.)  ``streams=1`` issues both
+    calls on one stream, one after the other; ``legs`` "out" or "in" issues
+    only that direction of every slice (a breakdown of the slice's time, not
+    the workload itself)."""
     import numpy as np
     import torch
 
@@ -604,25 +607,33 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
 
     s = sched.shape
     prepared = {k: slice_tables(sched, k) for k in ids}
-    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    sa = torch.cuda.Stream()
+    sb = torch.cuda.Stream() if streams == 2 else sa
     kv = aqua.KVPool(s.as_tuple(), pool)
     if host_path is not None:
         _configure_host(kv, host_path)
     evs = []
+    do_out, do_in = legs != "in", legs != "out"
 
     def one(k, timed):
         out, out_off, inn, in_off = prepared[k]
+        ev = [None] * 4
         if timed:
-            a0, a1, b0, b1 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
-            a0.record(sa)
-            b0.record(sb)
-        kv.swap_out(out, region, out_off, stream=sa)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        if do_out:
+            if timed:
+                ev[0].record(sa)
+            kv.swap_out(out, region, out_off, stream=sa)
+            if timed:
+                ev[1].record(sa)
+        if do_in:
+            if timed:
+                ev[2].record(sb)
+            kv.swap_in(inn, region, in_off, stream=sb)
+            if timed:
+                ev[3].record(sb)
         if timed:
-            a1.record(sa)
-        kv.swap_in(inn, region, in_off, stream=sb)
-        if timed:
-            b1.record(sb)
-            evs.append((a0, a1, b0, b1, len(out[0]), len(inn[0])))
+            evs.append((*ev, len(out[0]) if do_out else 0, len(inn[0]) if do_in else 0))
         kv.sync(0)
 
     for k in ids[:warmup]:
@@ -642,12 +653,30 @@ def _time_slices(sched, pool, region, ids, warmup, host_path=None):
     unit = s.num_layers * s.chunk_bytes
     out_b = np.array([e[4] for e in evs], dtype=np.float64) * unit
     in_b = np.array([e[5] for e in evs], dtype=np.float64) * unit
-    out_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    in_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
-    # Union of the two calls' intervals in each slice, from the swap-out's start.
-    both_ms = np.array([max(e[0].elapsed_time(e[1]), e[0].elapsed_time(e[3]))
-                        - min(0.0, e[0].elapsed_time(e[2])) for e in evs])
+    out_ms = np.array([e[0].elapsed_time(e[1]) if do_out else 0.0 for e in evs])
+    in_ms = np.array([e[2].elapsed_time(e[3]) if do_in else 0.0 for e in evs])
+
+    def union(e):
+        # Union of the issued calls' intervals in a slice, from the first start.
+        starts = [x for x, on in ((e[0], do_out), (e[2], do_in)) if on]
+        ends = [x for x, on in ((e[1], do_out), (e[3], do_in)) if on]
+        ref = starts[0]
+        return (max(ref.elapsed_time(x) for x in ends)
+                - min([0.0] + [ref.elapsed_time(x) for x in starts[1:]]))
+
+    both_ms = np.array([union(e) for e in evs])
     return wall, st, out_b, in_b, out_ms, in_ms, both_ms
+
+
+def _slice_kernel(config, host):
+    """What the slice roofline covers: the calls issued and their streams."""
+    legs = config.get("slice_legs", "both")
+    if legs != "both":
+        return ("gather" if legs == "out" else "scatter") + " of a slice"
+    if config.get("slice_streams", 2) == 1:
+        return "gather then scatter of a slice, on one stream"
+    return "gather and scatter of a slice, on two streams" + (
+        " (one link direction each)" if host else " (sharing HBM)")
 
 
 def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, both_ms, steps, config,
@@ -674,8 +703,7 @@ def _slice_result(res_common, s, wall, st, out_b, in_b, out_ms, in_ms, both_ms, 
         "config": config,
         "roofline": {
             "bound": "host_link" if host else "hbm",
-            "kernel": "gather and scatter of a slice, on two streams"
-                      + (" (one link direction each)" if host else " (sharing HBM)"),
+            "kernel": _slice_kernel(config, host),
             "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
             "frac": round(achieved / peak, 4), "traffic": None,
             "algorithmic_bytes_per_launch": round(float(per * (out_b + in_b)[both].mean()))
@@ -713,15 +741,18 @@ def run_cycle(args, res_common):
         wl.fill_region(region, sched)
     torch.cuda.synchronize()
     timed = _time_slices(sched, pool, region, list(range(n)), args.warmup,
-                         host_path=args.host_path if on_host else None)
-    out_b = timed[2]
+                         host_path=args.host_path if on_host else None,
+                         streams=args.slice_streams, legs=args.slice_legs)
+    out_b, in_b = timed[2], timed[3]
     config = {
         "workload": WORKLOADS[args.workload], "layers": s.num_layers,
         "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "block_tokens": s.block_tokens,
         "pool_blocks": s.num_blocks, "chunk_bytes": s.chunk_bytes,
         "prompts": len(sched.nblocks), "swaps_per_slice": 16, "slices_timed": args.steps,
-        "host_sync_per_slice": True,
-        "mean_payload_bytes_per_direction": round(float(out_b.mean())),
+        "host_sync_per_slice": True, "slice_streams": args.slice_streams,
+        "slice_legs": args.slice_legs,
+        "mean_payload_bytes_per_direction":
+            round(float((in_b if args.slice_legs == "in" else out_b).mean())),
         "offload_target": "pinned_host" if on_host else "hbm",
         "host_path": args.host_path if on_host else None, "parallelism": "single_gpu",
     }
@@ -846,7 +877,8 @@ def run_cfs(args, res_common):
     region = torch.empty(sched.region_bytes, dtype=torch.uint8, device="cuda")
     wl.fill_region(region, sched)
     torch.cuda.synchronize()
-    timed = _time_slices(sched, pool, region, ids, args.warmup)
+    timed = _time_slices(sched, pool, region, ids, args.warmup, streams=args.slice_streams,
+                         legs=args.slice_legs)
     out_b, in_b = timed[2], timed[3]
     config = {
         "workload": WORKLOADS["cfs"], "layers": s.num_layers, "kv_heads": s.num_kv_heads,
@@ -855,7 +887,9 @@ def run_cfs(args, res_common):
         "decode_slots": d, "k": cfg.k, "iterations": len(log), "reschedules": len(sched.slices),
         "swapping_slices": len([1 for sl in sched.slices if sl.out_tables or sl.in_tables]),
         "slices_timed": steps, "host_sync_per_slice": True,
-        "mean_payload_bytes_per_direction": round(float(out_b.mean())) if len(out_b) else 0,
+        "slice_streams": args.slice_streams, "slice_legs": args.slice_legs,
+        "mean_payload_bytes_per_direction":
+            round(float((in_b if args.slice_legs == "in" else out_b).mean())) if len(out_b) else 0,
         "offload_target": "hbm", "parallelism": "single_gpu",
     }
     res = _slice_result(res_common, s, *timed, steps, config)
@@ -1307,6 +1341,12 @@ def main():
                          "runtime's copies) or an SDMA engine index 0..15")
     ap.add_argument("--copy-reference", action="store_true",
                     help="one plain device copy of the payload size before timing")
+    ap.add_argument("--slice-streams", type=int, default=2, choices=[1, 2],
+                    help="cycle, cycle_host, cfs: each slice's swap-out and swap-in on two "
+                         "streams (the workload as defined) or on one, one after the other")
+    ap.add_argument("--slice-legs", default="both", choices=["both", "out", "in"],
+                    help="cycle, cycle_host, cfs: issue only the swap-outs or only the "
+                         "swap-ins of every slice (a breakdown of the slice's time)")
     ap.add_argument("--no-secondary", action="store_true",
                     help="default workload: skip the two shorter legs reported beside it (the "
                          "same prompt to pinned host memory, and the preemption cycle)")
