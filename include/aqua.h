@@ -232,8 +232,11 @@ AQUA_API aqua_status aqua_swap_in_ex(aqua_kv_pool_t pool, uint32_t num_seqs,
  *
  * aqua_swap_noalloc is aqua_swap_out (direction 0) or aqua_swap_in
  * (direction 1) with the same arguments, results, ordering and errors,
- * except that it allocates nothing: no device or pinned memory, no HIP
- * event or stream.  Its run descriptors go through the pool's pinned ring
+ * except that it allocates no device or pinned memory and creates no HIP
+ * event or stream.  (Its host-side planning, like that of the other
+ * calls, uses ordinary host memory: the pool's planning buffers, which
+ * keep the capacity of the largest call seen, and the sort of a swap-in's
+ * runs.)  Its run descriptors go through the pool's pinned ring
  * (allocated when the pool was created; the call never grows it) to a
  * device scratch array of 2 MiB that the library holds on each device for
  * the life of the process, and its completion event is one of the 16 the
