@@ -206,12 +206,15 @@ void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
 void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunDesc>* tmp) {
     const size_t n = runs->size();
     if (ways < 2 || n < 2 * (size_t)ways) return;
-    const size_t seg = (n + ways - 1) / ways;  // runs per eighth (the last may be short)
+    // Segment s holds q + 1 runs for s < r and q runs after that, so that
+    // every row of the result holds one run of each segment in turn (the
+    // last row, of r runs, one of each of the first r segments).
+    const size_t q = n / ways, r = n % ways;
     tmp->clear();
     tmp->reserve(n);
-    for (size_t i = 0; i < seg; ++i)
-        for (size_t s = 0; s < ways; ++s)
-            if (s * seg + i < n) tmp->push_back((*runs)[s * seg + i]);
+    for (size_t i = 0; i <= q; ++i)
+        for (size_t s = 0; s < (i < q ? (size_t)ways : r); ++s)
+            tmp->push_back((*runs)[s * q + std::min(s, r) + i]);
     runs->swap(*tmp);
 }
 

@@ -158,7 +158,8 @@ void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
 // MI355X's 8 XCDs (each with its own L2) in turn, and the kernels take one
 // unit per workgroup, layer by layer.  Dealing a layer's runs out 8 ways (run
 // j of the result is run j / 8 of the (j % 8)-th contiguous eighth of the
-// input) gives each XCD one contiguous eighth of the runs in every layer:
+// input; the first n % 8 eighths hold one run more) gives each XCD one
+// contiguous eighth of the runs in every layer:
 // of the pool range when they are sorted, of the image when they are in
 // table order, instead of every XCD taking every eighth run of one shared
 // range.  Measured on MI355X against sorted order, same box, 3 to 6 runs
@@ -166,18 +167,19 @@ void sort_by_block(std::vector<RunDesc>* runs, uint32_t num_blocks,
 // +3.3 %, the Yi-34B prefix load +2.1 to +3.6 %, one TP2 rank +1.0 %; the
 // fair-scheduling reschedules -0.4 to -1.7 % (within their run-to-run
 // spread).  2 ways gained about half as much, 16 or 32 ways lost 1-4 %
-// against 8.  On sparse calls it sped a long prompt's gather by 8-11 % but
-// slowed one of 64 short prompts by 4-7 %, so they keep table order.  Runs
-// only ever change order, so no byte changes.  `tmp` is reusable scratch.
+// against 8.  Which calls are dealt is run_order's rule.  A launch may start
+// its turn at another XCD than the first (where the previous launch left
+// off); that only changes which XCD takes which eighth.  Runs only ever
+// change order, so no byte changes.  `tmp` is reusable scratch.
 constexpr uint32_t kXcdWays = 8;
 void interleave_runs(std::vector<RunDesc>* runs, uint32_t ways, std::vector<RunDesc>* tmp);
 
 // XCD-aware unit order inside the kernels, for calls whose runs are not
 // dealt out.  On a launch of one workgroup per unit, workgroup b (sent to XCD
-// b % 8) takes unit xcd_unit(b, units), so that each XCD copies one
-// contiguous eighth of the launch's units in order (XCD x gets the x-th
-// eighth; the first units % 8 eighths hold one unit more).  A bijection on
-// [0, units).  Used for undealt calls of chunks between 16 and 64 KiB
+// (b + c) % 8, c fixed for the launch) takes unit xcd_unit(b, units), so that
+// each XCD copies one contiguous eighth of the launch's units in order (the
+// (b % 8)-th eighth; the first units % 8 eighths hold one unit more).  A
+// bijection on [0, units).  Used for undealt calls of chunks between 16 and 64 KiB
 // (exclusive) to an HBM buffer, where it measured, against plain order on
 // the same box (3 to 4 runs each, with launches of at most 512 MiB then):
 // the fp8 preemption cycle +4.2 %, one TP2 rank +0.5 %, the fp8 8B pair

@@ -68,7 +68,8 @@ __device__ __forceinline__ void st(v4u* p, v4u v) {
 // partial pass the gfx950 code waits for each conditional load before issuing
 // the next; a form without lane branches that kept them all in flight
 // measured no faster on 32 and 16 KiB chunks (within 1 %; one 32 KiB
-// gather 2.5 % slower).
+// gather 2.5 % slower), and neither did workgroups that copy two 32 KiB
+// units with all four loads of each lane in flight (1.5-8 % slower).
 template <int THREADS, bool NT_LD, bool NT_ST>
 __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
                                           v4u* __restrict__ d, uint32_t nvec) {
@@ -101,9 +102,10 @@ __device__ __forceinline__ void copy_span(const v4u* __restrict__ s,
 // nontemporal pool stores when NT_POOL_ST.
 // Work unit u in [0, units) is (layer l0 + u / ndesc, descriptor u % ndesc);
 // layer l of the image side starts img_l0 layers before img_off's origin
-// (0 for whole images, the first staged layer for a staging slot);
-// consecutive workgroups take consecutive runs of one layer, so the image
-// side of a gather is written front to back.
+// (0 for whole images, the first staged layer for a staging slot).  In
+// plain order consecutive workgroups take consecutive units; with xcd_order
+// each XCD takes a contiguous eighth of them (xcd_unit), and the host may
+// have dealt each layer's runs out to the XCDs already (interleave_runs).
 template <bool OUT, bool NT_POOL_ST, int THREADS>
 __global__ __launch_bounds__(THREADS) void swap_runs_kernel(
     uint8_t* __restrict__ pool, uint8_t* __restrict__ img,

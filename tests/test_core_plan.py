@@ -300,9 +300,11 @@ def test_sort_by_block_matches_a_stable_sort():
 def test_interleave_runs_deals_eighths_to_the_xcds():
     """Sorted runs are dealt out 8 ways: position j holds run j // 8 of the
     (j % 8)-th contiguous eighth, so the units a round-robin dispatch sends
-    to one XCD cover one contiguous eighth of the sorted range.  The result
-    is a permutation of the input for every length (a short last eighth
-    included), and lists shorter than two runs per way stay as they are."""
+    to one XCD cover one contiguous eighth of the sorted range.  That holds
+    for every length: the first n % 8 eighths hold one run more, so the
+    last row, which is short, holds one run of each of them.  The result is
+    a permutation of the input, and lists shorter than two runs per way
+    stay as they are."""
     import numpy as np
     from tests.core_lib import RUN_DESC, interleave_runs, xcd_ways
     W = xcd_ways()
@@ -314,11 +316,12 @@ def test_interleave_runs_deals_eighths_to_the_xcds():
     got = interleave_runs(d, W)["block"]
     for x in range(W):
         assert list(got[x::W]) == list(range(256 * x, 256 * x + 256))
-    # A worked case with a short last eighth: 19 runs, segments of 3.
+    # A worked case: 19 runs, eighths of 3, 3, 3, 2, 2, 2, 2, 2 (0-2, 3-5,
+    # 6-8, 9-10, 11-12, 13-14, 15-16, 17-18).
     d = np.zeros(19, dtype=RUN_DESC)
     d["block"] = np.arange(19)
     assert list(interleave_runs(d, W)["block"]) == [
-        0, 3, 6, 9, 12, 15, 18, 1, 4, 7, 10, 13, 16, 2, 5, 8, 11, 14, 17]
+        0, 3, 6, 9, 11, 13, 15, 17, 1, 4, 7, 10, 12, 14, 16, 18, 2, 5, 8]
     rng = np.random.default_rng(9)
     for n in list(range(0, 40)) + [int(x) for x in rng.integers(40, 5000, 30)]:
         d = np.zeros(n, dtype=RUN_DESC)
@@ -330,9 +333,14 @@ def test_interleave_runs_deals_eighths_to_the_xcds():
         if n < 2 * W:
             assert got.tobytes() == d.tobytes(), n
         else:
-            seg = -(-n // W)
-            order = [s * seg + i for i in range(seg) for s in range(W) if s * seg + i < n]
+            # Eighths as contiguous index ranges; position j must hold
+            # element j // 8 of eighth j % 8.
+            q, r = divmod(n, W)
+            starts = [s * q + min(s, r) for s in range(W)]
+            order = [starts[j % W] + j // W for j in range(n)]
             assert got.tobytes() == d[order].tobytes(), n
+            sizes = [q + (s < r) for s in range(W)]
+            assert sum(sizes) == n and all(j // W < sizes[j % W] for j in range(n)), n
     d = np.zeros(100, dtype=RUN_DESC)
     d["block"] = np.arange(100)
     assert interleave_runs(d, 1).tobytes() == d.tobytes()
