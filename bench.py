@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "cb7c25f9576d92fe"): {
-        "gather (swap-out)": 21478172053, "scatter (swap-in)": 21476918167},
-    ("llama8b_hbm", "cb7c25f9576d92fe"): {
-        "gather (swap-out)": 4296087232, "scatter (swap-in)": 4295533052},
-    ("llama70b_tp2_hbm", "cb7c25f9576d92fe"): {
-        "gather (swap-out)": 10739675229, "scatter (swap-in)": 10739217198},
-    ("llama70b_tp4_hbm", "cb7c25f9576d92fe"): {
-        "gather (swap-out)": 5369614631, "scatter (swap-in)": 5369331397},
-    ("llama8b_fp8_hbm", "cb7c25f9576d92fe"): {
-        "gather (swap-out)": 2148297917, "scatter (swap-in)": 2149329663},
+    ("llama70b_hbm", "2d3015926e9d2c12"): {
+        "gather (swap-out)": 21478204924, "scatter (swap-in)": 21476938647},
+    ("llama8b_hbm", "2d3015926e9d2c12"): {
+        "gather (swap-out)": 4296120307, "scatter (swap-in)": 4295575958},
+    ("llama70b_tp2_hbm", "2d3015926e9d2c12"): {
+        "gather (swap-out)": 10739657309, "scatter (swap-in)": 10739216583},
+    ("llama70b_tp4_hbm", "2d3015926e9d2c12"): {
+        "gather (swap-out)": 5369614324, "scatter (swap-in)": 5369358943},
+    ("llama8b_fp8_hbm", "2d3015926e9d2c12"): {
+        "gather (swap-out)": 2148293923, "scatter (swap-in)": 2149328435},
 }
 
 # Every source that decides what the swap kernels do and how they are
