@@ -141,6 +141,10 @@ size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
                  std::vector<RunDesc>* out) {
     const size_t before = out->size();
     const uint64_t max_run = std::max<uint64_t>(1, max_unit_bytes / s.C);
+    // At most one run per block: size once, fill through a pointer (a
+    // push_back per run measured several times slower), then trim.
+    out->resize(before + (size_t)(a.num_seqs ? a.offs[a.num_seqs] : 0));
+    RunDesc* o = out->data() + before;
     for (uint32_t k = 0; k < a.num_seqs; ++k) {
         const uint64_t first = a.offs[k], n = a.offs[k + 1] - first;
         if (!n) continue;
@@ -153,16 +157,16 @@ size_t plan_runs(const Shape& s, const CallArgs& a, uint64_t max_unit_bytes,
             while (i + len < n && len < max_run &&
                    bt[i + len] == bt[i + len - 1] + 1)
                 ++len;
-            RunDesc d;
-            d.img_off = base + i * s.C;
-            d.img_lstride = lstride;
-            d.block = (uint32_t)bt[i];
-            d.nchunks = (uint32_t)len;
-            d.reserved0 = d.reserved1 = 0;
-            out->push_back(d);
+            o->img_off = base + i * s.C;
+            o->img_lstride = lstride;
+            o->block = (uint32_t)bt[i];
+            o->nchunks = (uint32_t)len;
+            o->reserved0 = o->reserved1 = 0;
+            ++o;
             i += len;
         }
     }
+    out->resize((size_t)(o - out->data()));
     return out->size() - before;
 }
 
@@ -282,13 +286,14 @@ size_t plan_copies(uint32_t n, const uint64_t* src_off, const uint64_t* dst_off,
 // ---------------------------------------------------------------------------
 
 void HazardTracker::reset(uint32_t num_blocks) {
-    last_writer_.assign(num_blocks, 0);
-    readers_.assign(num_blocks, {});
+    blocks_.assign(num_blocks, BlockRec{});
+    more_.clear();
     ranges_.clear();
     done_.clear();
     last_.clear();
     dep_.clear();
     ticket_lane_.clear();
+    head_ = 0;
     base_ = 1;
     last_ticket_ = 0;
 }
@@ -303,11 +308,16 @@ void HazardTracker::ensure_lane(uint32_t lane) {
 
 // Drops the lanes of the oldest tickets while they are complete.
 void HazardTracker::prune() {
-    while (!ticket_lane_.empty()) {
-        const uint32_t m = ticket_lane_.front();
+    while (head_ < ticket_lane_.size()) {
+        const uint32_t m = ticket_lane_[head_];
         if (m != kNoLane && base_ > done_[m]) break;
-        ticket_lane_.pop_front();
+        ++head_;
         ++base_;
+    }
+    // Drop the dropped entries once they are most of the vector.
+    if (head_ >= 1024 && head_ * 2 >= ticket_lane_.size()) {
+        ticket_lane_.erase(ticket_lane_.begin(), ticket_lane_.begin() + (ptrdiff_t)head_);
+        head_ = 0;
     }
 }
 
@@ -328,8 +338,8 @@ uint32_t LaneMap::lane_for(uintptr_t stream, const HazardTracker& t) {
 }
 
 uint32_t HazardTracker::lane_of(uint64_t ticket) const {
-    if (ticket < base_ || ticket - base_ >= ticket_lane_.size()) return kNoLane;
-    const uint32_t m = ticket_lane_[ticket - base_];
+    if (ticket < base_ || ticket - base_ >= ticket_lane_.size() - head_) return kNoLane;
+    const uint32_t m = ticket_lane_[head_ + (ticket - base_)];
     return (m != kNoLane && ticket > done_[m]) ? m : kNoLane;
 }
 
@@ -347,15 +357,13 @@ void HazardTracker::complete(uint32_t lane, uint64_t ticket) {
     prune();
 }
 
-void HazardTracker::need(uint64_t ticket, uint32_t lane, uint64_t* elided) {
-    if (!ticket) return;
+HazardTracker::Need HazardTracker::need(uint64_t ticket, uint32_t lane) {
+    if (!ticket) return Need::kNone;
     const uint32_t m = lane_of(ticket);
-    if (m == kNoLane) {  // known complete
-        ++*elided;
-        return;
-    }
-    if (m == lane) return;  // same stream: ordered by the stream itself
+    if (m == kNoLane) return Need::kComplete;   // known complete: no wait
+    if (m == lane) return Need::kSameLane;      // ordered by the stream itself
     if (ticket > dep_[m]) dep_[m] = ticket;
+    return Need::kWait;
 }
 
 uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
@@ -364,11 +372,33 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
     deps->clear();
     std::fill(dep_.begin(), dep_.end(), 0);
     // Tickets skipped since the last issue were never issued: complete.
-    while (base_ + ticket_lane_.size() < ticket) ticket_lane_.push_back(kNoLane);
+    while (base_ + (ticket_lane_.size() - head_) < ticket) ticket_lane_.push_back(kNoLane);
     ticket_lane_.push_back(lane);
     last_[lane] = ticket;
     last_ticket_ = ticket;
     uint64_t elided = 0;
+    // The blocks of one call mostly name the same few earlier tickets (a
+    // block's last writer and its last reader), and nothing need() reads
+    // changes during the call: the answers for the last two tickets are
+    // kept.  Each conflict with a complete ticket still counts.
+    uint64_t memo_t[2] = {0, 0};
+    Need memo[2] = {Need::kNone, Need::kNone};
+    auto after = [&](uint64_t t) {
+        if (!t) return;
+        Need n;
+        if (t == memo_t[0]) {
+            n = memo[0];
+        } else if (t == memo_t[1]) {
+            n = memo[1];
+        } else {
+            n = need(t, lane);
+            memo_t[1] = memo_t[0];
+            memo[1] = memo[0];
+            memo_t[0] = t;
+            memo[0] = n;
+        }
+        if (n == Need::kComplete) ++elided;
+    };
 
     // Offload ranges: drop finished records, then look for overlaps.  A
     // read conflicts with earlier writes; a write with every earlier access.
@@ -381,14 +411,14 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
         const uint64_t lo = a.ranges_read[r].first, hi = a.ranges_read[r].second;
         for (size_t k = 0; k < old; ++k) {
             const RangeRec& q = ranges_[k];
-            if (q.write && q.lo < hi && lo < q.hi) need(q.ticket, lane, &elided);
+            if (q.write && q.lo < hi && lo < q.hi) after(q.ticket);
         }
     }
     for (size_t r = 0; r < a.n_ranges_written; ++r) {
         const uint64_t lo = a.ranges_written[r].first, hi = a.ranges_written[r].second;
         for (size_t k = 0; k < old; ++k) {
             const RangeRec& q = ranges_[k];
-            if (q.lo < hi && lo < q.hi) need(q.ticket, lane, &elided);
+            if (q.lo < hi && lo < q.hi) after(q.ticket);
         }
     }
     if (a.n_ranges_written) {
@@ -411,35 +441,65 @@ uint64_t HazardTracker::issue(uint64_t ticket, uint32_t lane, const Access& a,
         ranges_.push_back(
             {a.ranges_written[r].first, a.ranges_written[r].second, ticket, lane, true});
 
-    // Pool blocks read: after their last writer; join the readers.
+    // Pool blocks read: after their last writer; join the readers (one
+    // entry per lane, finished readers forgotten when another lane joins).
     for (size_t j = 0; j < a.n_blocks_read; ++j) {
         const uint32_t b = (uint32_t)a.blocks_read[j];
-        need(last_writer_[b], lane, &elided);
-        std::vector<Reader>& rd = readers_[b];
+        BlockRec& r = blocks_[b];
+        after(r.writer);
+        if (r.reader && r.reader_lane == lane) {
+            r.reader = ticket;
+            continue;
+        }
+        if (!r.more) {
+            if (!r.reader || done(r.reader)) {
+                r.reader = ticket;
+                r.reader_lane = lane;
+            } else {
+                more_[b].assign(1, Reader{lane, ticket});
+                r.more = 1;
+            }
+            continue;
+        }
+        std::vector<Reader>& rd = more_[b];
         bool found = false;
         for (Reader& q : rd)
             if (q.lane == lane) {
                 q.ticket = ticket;
                 found = true;
             }
-        if (!found) {
-            // Forget readers that have finished before adding one.
-            size_t k = 0;
-            for (size_t i = 0; i < rd.size(); ++i)
-                if (!done(rd[i].ticket)) rd[k++] = rd[i];
-            rd.resize(k);
+        if (found) continue;
+        size_t k = 0;
+        for (size_t i = 0; i < rd.size(); ++i)
+            if (!done(rd[i].ticket)) rd[k++] = rd[i];
+        rd.resize(k);
+        if (!r.reader || done(r.reader)) {
+            r.reader = ticket;
+            r.reader_lane = lane;
+        } else {
             rd.push_back({lane, ticket});
+        }
+        if (rd.empty()) {
+            more_.erase(b);
+            r.more = 0;
         }
     }
     // Pool blocks written: after their last writer and every reader since.
     for (size_t j = 0; j < a.n_blocks_written; ++j) {
         const uint32_t b = (uint32_t)a.blocks_written[j];
-        need(last_writer_[b], lane, &elided);
-        std::vector<Reader>& rd = readers_[b];
-        for (const Reader& q : rd)
-            if (q.ticket != ticket) need(q.ticket, lane, &elided);
-        rd.clear();
-        last_writer_[b] = ticket;
+        BlockRec& r = blocks_[b];
+        after(r.writer);
+        if (r.reader && r.reader != ticket) after(r.reader);
+        if (r.more) {
+            const auto it = more_.find(b);
+            for (const Reader& q : it->second)
+                if (q.ticket != ticket) after(q.ticket);
+            more_.erase(it);
+            r.more = 0;
+        }
+        r.reader = 0;
+        r.reader_lane = 0;
+        r.writer = ticket;
     }
 
     for (uint32_t m = 0; m < dep_.size(); ++m)

@@ -6,8 +6,8 @@
 
 #include <cstddef>
 #include <cstdint>
-#include <deque>
 #include <map>
+#include <unordered_map>
 #include <utility>
 #include <vector>
 
@@ -290,7 +290,7 @@ public:
     uint64_t last_ticket() const { return last_ticket_; }
     // Tickets whose lane is still kept (from the oldest one not known
     // complete to the newest) and lanes known to the tracker.
-    size_t tickets_kept() const { return ticket_lane_.size(); }
+    size_t tickets_kept() const { return ticket_lane_.size() - head_; }
     size_t lanes() const { return done_.size(); }
 
 private:
@@ -298,23 +298,36 @@ private:
         uint32_t lane;
         uint64_t ticket;
     };
+    // One pool block: its last writer and its readers since then, at most
+    // one per lane.  The first reader is kept in the record, so that a call
+    // touches one 24-byte record per block; readers on further lanes at
+    // once (several streams reading one block) go to more_.
+    struct BlockRec {
+        uint64_t writer = 0;       // ticket of the last writer, 0: none
+        uint64_t reader = 0;       // ticket of the kept reader, 0: none
+        uint32_t reader_lane = 0;
+        uint32_t more = 0;         // 1: more_ holds further readers of the block
+    };
     struct RangeRec {
         uint64_t lo, hi, ticket;
         uint32_t lane;
         bool write;
     };
+    // What issue() found for one earlier ticket (see need()).
+    enum class Need : uint8_t { kNone, kComplete, kSameLane, kWait };
     void ensure_lane(uint32_t lane);
     void prune();
-    void need(uint64_t ticket, uint32_t lane, uint64_t* elided);
+    Need need(uint64_t ticket, uint32_t lane);
 
-    std::vector<uint64_t> last_writer_;
-    std::vector<std::vector<Reader>> readers_;
+    std::vector<BlockRec> blocks_;
+    std::unordered_map<uint32_t, std::vector<Reader>> more_;
     std::vector<RangeRec> ranges_;
-    std::vector<uint64_t> done_;        // per lane watermark
-    std::vector<uint64_t> last_;        // per lane, newest ticket issued on it
-    std::vector<uint64_t> dep_;         // per lane, scratch of one issue()
-    std::deque<uint32_t> ticket_lane_;  // lanes of tickets base_, base_ + 1, ...
-    uint64_t base_ = 1;                 // every ticket below is complete
+    std::vector<uint64_t> done_;         // per lane watermark
+    std::vector<uint64_t> last_;         // per lane, newest ticket issued on it
+    std::vector<uint64_t> dep_;          // per lane, scratch of one issue()
+    std::vector<uint32_t> ticket_lane_;  // from head_: lanes of tickets base_, base_ + 1, ...
+    size_t head_ = 0;
+    uint64_t base_ = 1;                  // every ticket below is complete
     uint64_t last_ticket_ = 0;
 };
 
