@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "2d3015926e9d2c12"): {
-        "gather (swap-out)": 21478204924, "scatter (swap-in)": 21476938647},
-    ("llama8b_hbm", "2d3015926e9d2c12"): {
-        "gather (swap-out)": 4296120307, "scatter (swap-in)": 4295575958},
-    ("llama70b_tp2_hbm", "2d3015926e9d2c12"): {
-        "gather (swap-out)": 10739657309, "scatter (swap-in)": 10739216583},
-    ("llama70b_tp4_hbm", "2d3015926e9d2c12"): {
-        "gather (swap-out)": 5369614324, "scatter (swap-in)": 5369358943},
-    ("llama8b_fp8_hbm", "2d3015926e9d2c12"): {
-        "gather (swap-out)": 2148293923, "scatter (swap-in)": 2149328435},
+    ("llama70b_hbm", "d47905c249052bdd"): {
+        "gather (swap-out)": 21478140309, "scatter (swap-in)": 21476880586},
+    ("llama8b_hbm", "d47905c249052bdd"): {
+        "gather (swap-out)": 4296089485, "scatter (swap-in)": 4295525372},
+    ("llama70b_tp2_hbm", "d47905c249052bdd"): {
+        "gather (swap-out)": 10739604983, "scatter (swap-in)": 10739188935},
+    ("llama70b_tp4_hbm", "d47905c249052bdd"): {
+        "gather (swap-out)": 5369608794, "scatter (swap-in)": 5369357919},
+    ("llama8b_fp8_hbm", "d47905c249052bdd"): {
+        "gather (swap-out)": 2148309181, "scatter (swap-in)": 2149329050},
 }
 
 # Every source that decides what the swap kernels do and how they are
