@@ -189,6 +189,34 @@ def test_waits_only_where_needed():
     assert tr.issue(10, 0, True, [2], [(9000, 9096)]) == [(2, 9)]
 
 
+def test_block_read_on_several_streams_at_once():
+    """Readers of one block on several lanes at once: a later write waits
+    for the newest live reader of every other lane, a lane that reads again
+    replaces its own entry, and finished readers are forgotten when another
+    lane joins."""
+    tr = Tracker(8)
+    # Swap-outs on lanes 0, 1 and 2 all read block 5 (and nothing else).
+    assert tr.issue_rw(1, 0, [5], [], [], []) == []
+    assert tr.issue_rw(2, 1, [5], [], [], []) == []
+    assert tr.issue_rw(3, 2, [5], [], [], []) == []
+    # Lane 1 reads block 5 again: its entry moves to ticket 4.
+    assert tr.issue_rw(4, 1, [5, 6], [], [], []) == []
+    # A swap-in on lane 3 writing block 5 waits for the newest reader of
+    # each of the three lanes.
+    assert sorted(tr.issue_rw(5, 3, [], [5], [], [])) == [(0, 1), (1, 4), (2, 3)]
+    # After the write, a reader on lane 0 waits only for the writer.
+    assert tr.issue_rw(6, 0, [5], [], [], []) == [(3, 5)]
+    # Lanes 0 and 3 complete up to 6; readers join on lanes 1 and 2, and a
+    # write on lane 0 waits for those two only.
+    tr.complete(3, 5)
+    tr.complete(0, 6)
+    assert tr.issue_rw(7, 1, [5], [], [], []) == []
+    assert tr.issue_rw(8, 2, [5], [], [], []) == []
+    assert sorted(tr.issue_rw(9, 0, [], [5], [], [])) == [(1, 7), (2, 8)]
+    # Block 6, read once by lane 1 (ticket 4), is still owed a wait.
+    assert tr.issue_rw(10, 2, [], [6], [], []) == [(1, 4)]
+
+
 def test_finished_ranges_are_forgotten():
     tr = Tracker(4)
     for t in range(1, 101):
