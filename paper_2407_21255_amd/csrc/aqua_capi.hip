@@ -404,8 +404,23 @@ aqua_status ring_reserve(aqua_kv_pool* p, uint64_t bytes, uint64_t* off, bool gr
         st = alloc_rings(p, nb);
         if (st != AQUA_OK) return st;
     }
+    // Uses of calls already known complete free their space.  The uses are
+    // in allocation order and calls on different streams can complete out
+    // of order, so only finished uses at the front are dropped.
+    while (!p->ring_uses.empty() && p->tracker.done(p->ring_uses.front().ticket))
+        p->ring_uses.pop_front();
+    // Start again at the front of the ring when no live call's descriptors
+    // are there: the host then writes into lines it wrote a few calls ago,
+    // still in its caches.  Walking the whole ring wrote lines evicted long
+    // before, and copying a 135 KB plan into them took about 30 us.
+    bool front_free = true;
+    for (const RingUse& u : p->ring_uses)
+        if (u.lo < bytes) {
+            front_free = false;
+            break;
+        }
     uint64_t lo = p->ring_head;
-    if (lo + bytes > p->ring_bytes) lo = 0;
+    if (front_free || lo + bytes > p->ring_bytes) lo = 0;
     const uint64_t hi = lo + bytes;
     for (;;) {
         bool overlap = false;
