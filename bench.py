@@ -39,16 +39,16 @@ HOST_LINK_PEAK_GBS = 63.0    # PCIe 5.0 x16, one direction, after encoding
 # or to how they are launched reports null until measured again.
 # Recorded with the profile summary of the same kernel under profiles/.
 MEASURED_TRAFFIC = {
-    ("llama70b_hbm", "d47905c249052bdd"): {
-        "gather (swap-out)": 21478140309, "scatter (swap-in)": 21476880586},
-    ("llama8b_hbm", "d47905c249052bdd"): {
-        "gather (swap-out)": 4296089485, "scatter (swap-in)": 4295525372},
-    ("llama70b_tp2_hbm", "d47905c249052bdd"): {
-        "gather (swap-out)": 10739604983, "scatter (swap-in)": 10739188935},
-    ("llama70b_tp4_hbm", "d47905c249052bdd"): {
-        "gather (swap-out)": 5369608794, "scatter (swap-in)": 5369357919},
-    ("llama8b_fp8_hbm", "d47905c249052bdd"): {
-        "gather (swap-out)": 2148309181, "scatter (swap-in)": 2149329050},
+    ("llama70b_hbm", "13417f258857070b"): {
+        "gather (swap-out)": 21478084809, "scatter (swap-in)": 21476892772},
+    ("llama8b_hbm", "13417f258857070b"): {
+        "gather (swap-out)": 4296124199, "scatter (swap-in)": 4295530800},
+    ("llama70b_tp2_hbm", "13417f258857070b"): {
+        "gather (swap-out)": 10739621776, "scatter (swap-in)": 10739296865},
+    ("llama70b_tp4_hbm", "13417f258857070b"): {
+        "gather (swap-out)": 5369594663, "scatter (swap-in)": 5369299960},
+    ("llama8b_fp8_hbm", "13417f258857070b"): {
+        "gather (swap-out)": 2148315120, "scatter (swap-in)": 2149326387},
 }
 
 # Every source that decides what the swap kernels do and how they are
