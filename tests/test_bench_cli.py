@@ -83,3 +83,21 @@ def test_traffic_follows_what_the_kernels_run(tmp_path, monkeypatch):
     monkeypatch.delenv("AQUA_UNIT_BYTES")
     assert bench._kernel_hash(max_workgroups=256) != base
     assert bench._kernel_hash() == base
+
+
+def test_slice_options_parse_and_label_the_roofline():
+    """--slice-streams and --slice-legs take only their documented values,
+    and the slice roofline names what was issued and on how many streams."""
+    r = _run(["--slice-streams", "3"])
+    assert r.returncode == 2 and "--slice-streams" in r.stderr
+    r = _run(["--slice-legs", "both_ways"])
+    assert r.returncode == 2 and "--slice-legs" in r.stderr
+    sys.path.insert(0, ROOT)
+    import bench
+    both2 = bench._slice_kernel({"slice_streams": 2, "slice_legs": "both"}, host=False)
+    assert both2 == "gather and scatter of a slice, on two streams (sharing HBM)"
+    assert "one link direction each" in bench._slice_kernel({}, host=True)
+    assert bench._slice_kernel({"slice_streams": 1, "slice_legs": "both"}, False) == \
+        "gather then scatter of a slice, on one stream"
+    assert bench._slice_kernel({"slice_legs": "out"}, False) == "gather of a slice"
+    assert bench._slice_kernel({"slice_legs": "in"}, True) == "scatter of a slice"
